@@ -1,0 +1,415 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each oracle function is checked against something other than itself:
+
+- ``window_widths``: the paper's printed term counts (Table 1, Fig. 1 CASE,
+  Sec. 4 decode figures, App. C Fig. sndecomp), which fail if lambda, the
+  2*pi, the exponent sign or the <= of the keep rule is wrong; saturation.
+- ``scores``: eq:pair evaluated in the unrotated frame with an independent
+  complex-number rotation (wrong pair index, sign or scale fails it); the
+  special cases below.
+- ``attend``: (check 1) a textbook dense causal attention in numpy at an
+  infinite window, with GQA and query-position offsets; a hand-worked example;
+  two special cases that reduce to numpy dense attention (dropped prefix pairs,
+  one uniform width); sampled rows equal to the full run.
+- ``count_terms``: brute-force triple loop on tiny inputs, the per-row count
+  returned by ``attend``, the printed pins, and the paper's closed forms within
+  its stated integral-approximation error.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from conftest import kv, read_golden
+
+import workloads as W
+
+
+# ----------------------------------------------------------------------------
+# independent references written in the test
+# ----------------------------------------------------------------------------
+def dense_attention(q, k, v, q_pos0, scale):
+    """Textbook causal attention in fp64 (numpy): softmax(QK^T * scale + mask) V."""
+    B, nq, hq, d = q.shape
+    nk, hkv = k.shape[1], k.shape[2]
+    G = hq // hkv
+    kk = np.repeat(k, G, axis=2)
+    vv = np.repeat(v, G, axis=2)
+    s = np.einsum("bihd,bjhd->bhij", q, kk) * scale
+    pos = q_pos0 + np.arange(nq)
+    mask = np.arange(nk)[None, :] > pos[:, None]
+    s = np.where(mask[None, None], -np.inf, s)
+    m = s.max(-1, keepdims=True)
+    e = np.exp(s - m)
+    l_ = e.sum(-1, keepdims=True)
+    o = np.einsum("bhij,bjhd->bihd", e / l_, vv)
+    lse = (m + np.log(l_))[..., 0]
+    return o, lse
+
+
+def dense_from_scores(s, v, hq, G):
+    """Softmax over a given [nq, nk] score matrix (with -inf) and PV, numpy."""
+    m = s.max(-1, keepdims=True)
+    e = np.exp(s - m)
+    l_ = e.sum(-1, keepdims=True)
+    return (e / l_) @ v, (m + np.log(l_))[:, 0]
+
+
+def bf16_grid(rng, shape, scale=1.0):
+    """Random values exactly representable in bf16 (so both sides see the same numbers)."""
+    import torch
+    x = torch.from_numpy(rng.standard_normal(shape) * scale).to(torch.bfloat16)
+    return x.to(torch.float64).numpy()
+
+
+def rotate_complex(x, positions, theta):
+    """RoPE by complex multiplication: u_r = x_r + i x_{r+h}, u~ = u e^{i p theta_r}."""
+    assert x.ndim == 4  # [B, N, H, d]
+    h = x.shape[-1] // 2
+    u = x[..., :h] + 1j * x[..., h:]
+    ph = np.exp(1j * positions[:, None] * theta[None, :]).reshape(1, len(positions), 1, h)
+    r = u * ph
+    return np.concatenate([r.real, r.imag], axis=-1)
+
+
+# ----------------------------------------------------------------------------
+# hand-worked example (tests/golden/hand_example.txt)
+# ----------------------------------------------------------------------------
+def test_hand_example(oracle_lib):
+    recs = read_golden("hand_example.txt")
+    q = np.array([[1, 0, 0, 0], [0, 1, 0, 0], [1, 1, 1, 1]], dtype=np.float64)[None, :, None, :]
+    k = np.array([[2, 0, 2, 0], [0, 2, 0, 0], [0, 0, 0, 0]], dtype=np.float64)[None, :, None, :]
+    v = np.array([[1, 0, 0, 0], [0, 1, 0, 0], [0, 0, 1, 0]], dtype=np.float64)[None, :, None, :]
+    w = np.array([1.0, np.inf])
+    o, lse, terms = oracle_lib.attend(q, k, v, 0, w, scale=0.5)
+    of, lsef, termsf = oracle_lib.attend(q, k, v, 0, np.array([np.inf, np.inf]), scale=0.5)
+    for r in recs:
+        f = kv(r)
+        if r[0] == "row":
+            i = int(r[1])
+            np.testing.assert_allclose(o[0, i, 0], [float(x) for x in f["o"].split(",")],
+                                       atol=1e-15)
+            assert abs(lse[0, 0, i] - float(f["lse"])) < 1e-15
+        elif r[0] == "full_row":
+            i = int(r[1])
+            np.testing.assert_allclose(of[0, i, 0], [float(x) for x in f["o"].split(",")],
+                                       atol=1e-15)
+            assert abs(lsef[0, 0, i] - float(f["lse"])) < 1e-14
+        elif r[0] == "terms":
+            assert int(terms.sum()) == int(r[1])
+            assert oracle_lib.count_terms(w, 3, 0, 3)[0] == int(r[1])
+        elif r[0] == "full_terms":
+            assert int(termsf.sum()) == int(r[1])
+    # rows 0 and 1 are untouched by the window (every distance there is <= 1)
+    np.testing.assert_allclose(o[0, :2], of[0, :2], atol=0)
+
+
+def test_empty_score_sum_is_zero(oracle_lib):
+    """d=2 with w_0 = 0: every off-diagonal cell keeps no term, so its score is 0
+    and the token stays in the softmax (terms dropped, never tokens: Sec. 3.2)."""
+    rng = np.random.default_rng(1)
+    q = bf16_grid(rng, (1, 5, 1, 2))
+    k = bf16_grid(rng, (1, 5, 1, 2))
+    s = oracle_lib.scores(q, k, 0, np.array([0.0]))
+    for i in range(5):
+        for j in range(5):
+            if j > i:
+                assert s[i, j] == -np.inf
+            elif j < i:
+                assert s[i, j] == 0.0
+            else:
+                assert s[i, j] == pytest.approx(q[0, i, 0] @ k[0, j, 0] / math.sqrt(2), abs=1e-15)
+
+
+# ----------------------------------------------------------------------------
+# check 1: infinite window == ordinary causal RoPE attention (numpy dense)
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("B,nq,nk,q0,hq,hkv,d", [
+    (1, 33, 33, 0, 1, 1, 8),
+    (2, 37, 37, 0, 4, 2, 8),
+    (1, 17, 40, 23, 6, 2, 16),     # chunk at the end of a longer context
+    (1, 20, 12, 5, 3, 3, 4),       # keys end before the last query position
+    (2, 16, 16, 0, 7, 1, 64),
+])
+@pytest.mark.parametrize("kwin", [math.inf, 1e9])
+def test_check1_matches_dense(oracle_lib, B, nq, nk, q0, hq, hkv, d, kwin):
+    rng = np.random.default_rng(B * 1000 + nq * 7 + d)
+    q = bf16_grid(rng, (B, nq, hq, d))
+    k = bf16_grid(rng, (B, nk, hkv, d))
+    v = bf16_grid(rng, (B, nk, hkv, d))
+    w = oracle_lib.window_widths(d, 1e4, kwin, n_ctx=max(nk, q0 + nq))
+    o, lse, terms = oracle_lib.attend(q, k, v, q0, w)
+    od, lsed = dense_attention(q, k, v, q0, 1 / math.sqrt(d))
+    np.testing.assert_allclose(o, od, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12, rtol=0)
+    causal = sum(min(q0 + i, nk - 1) + 1 for i in range(nq))
+    assert int(terms[0, 0].sum()) == causal * d // 2
+
+
+def test_sampled_rows_equal_full_run(oracle_lib):
+    rng = np.random.default_rng(7)
+    q = bf16_grid(rng, (2, 29, 4, 16))
+    k = bf16_grid(rng, (2, 29, 2, 16))
+    v = bf16_grid(rng, (2, 29, 2, 16))
+    w = oracle_lib.window_widths(16, 50.0, 1.0)
+    o, lse, t = oracle_lib.attend(q, k, v, 0, w)
+    rows = np.array([[1, 3, 28], [0, 0, 0], [1, 1, 13], [0, 2, 7]])
+    os_, ls, ts = oracle_lib.attend(q, k, v, 0, w, rows=rows)
+    for n, (b, h, i) in enumerate(rows):
+        assert np.array_equal(os_[n], o[b, i, h])
+        assert ls[n] == lse[b, h, i]
+        assert ts[n] == t[b, h, i]
+
+
+# ----------------------------------------------------------------------------
+# check 2: eq:pair -- the rotated score is a sum of per-pair terms
+#          a_r cos(z theta_r) + b_r sin(z theta_r) with z = n - m
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("d,base,kwin", [(8, 100.0, math.inf), (8, 100.0, 1.0),
+                                          (64, 1e6, 2.0), (128, 5e5, 0.5)])
+def test_check2_pair_decomposition(oracle_lib, d, base, kwin):
+    rng = np.random.default_rng(d + int(base) % 97)
+    h = d // 2
+    n_pos = 40
+    theta = base ** (-2.0 * np.arange(h) / d)
+    qu = rng.standard_normal((1, n_pos, 1, d))
+    ku = rng.standard_normal((1, n_pos, 1, d))
+    pos = np.arange(n_pos, dtype=np.float64)
+    qr = rotate_complex(qu, pos, theta)
+    kr = rotate_complex(ku, pos, theta)
+    w = oracle_lib.window_widths(d, base, kwin)
+    s = oracle_lib.scores(qr, kr, 0, w)
+    for i in range(n_pos):
+        for j in range(i + 1):
+            z = i - j
+            a = qu[0, i, 0, :h] * ku[0, j, 0, :h] + qu[0, i, 0, h:] * ku[0, j, 0, h:]
+            b = qu[0, i, 0, :h] * ku[0, j, 0, h:] - qu[0, i, 0, h:] * ku[0, j, 0, :h]
+            terms = a * np.cos(z * theta) + b * np.sin(z * theta)
+            expect = terms[z <= w].sum() / math.sqrt(d)
+            assert s[i, j] == pytest.approx(expect, abs=1e-12 * (1 + abs(expect)))
+    # (i) with every pair kept the per-pair sum is the plain dot product
+    s_full = oracle_lib.scores(qr, kr, 0, np.full(h, np.inf))
+    dots = qr[0, :, 0] @ kr[0, :, 0].T / math.sqrt(d)
+    tri = np.tril(np.ones((n_pos, n_pos), dtype=bool))
+    np.testing.assert_allclose(s_full[tri], dots[tri], atol=1e-12)
+
+
+def test_scores_depend_only_on_distance(oracle_lib):
+    """Shifting query and key positions together leaves every windowed score unchanged."""
+    rng = np.random.default_rng(11)
+    d, h = 16, 8
+    theta = 300.0 ** (-2.0 * np.arange(h) / d)
+    qu = rng.standard_normal((1, 1, 1, d))
+    ku = rng.standard_normal((1, 1, 1, d))
+    w = oracle_lib.window_widths(d, 300.0, 0.7)
+    vals = []
+    for shift in (0, 5, 123):
+        n, m = 9 + shift, 2 + shift
+        qr = rotate_complex(qu, np.array([float(n)]), theta)
+        kk = np.zeros((1, n + 1, 1, d))
+        kk[0, m] = rotate_complex(ku, np.array([float(m)]), theta)[0, 0]
+        vals.append(oracle_lib.scores(qr, kk, n, w)[0, m])
+    assert vals[0] == pytest.approx(vals[1], abs=1e-12)
+    assert vals[0] == pytest.approx(vals[2], abs=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# special cases that reduce to numpy dense attention
+# ----------------------------------------------------------------------------
+def test_dropped_prefix_pairs_equal_dense_on_sub_dims(oracle_lib):
+    """w_r = -1 for r < r0 (never kept), +inf otherwise == dense attention on the
+    dims of pairs r >= r0, i.e. dims [r0, h) and [h + r0, d)."""
+    rng = np.random.default_rng(3)
+    d, h, r0 = 16, 8, 3
+    q = bf16_grid(rng, (1, 21, 2, d))
+    k = bf16_grid(rng, (1, 21, 1, d))
+    v = bf16_grid(rng, (1, 21, 1, d))
+    w = np.array([-1.0] * r0 + [np.inf] * (h - r0))
+    o, lse, _ = oracle_lib.attend(q, k, v, 0, w)
+    keep = np.r_[np.arange(r0, h), np.arange(h + r0, d)]
+    od, lsed = dense_attention(q[..., keep], k[..., keep], v, 0, 1 / math.sqrt(d))
+    np.testing.assert_allclose(o, od, atol=1e-12)
+    np.testing.assert_allclose(lse, lsed, atol=1e-12)
+
+
+def test_uniform_width_zeroes_far_scores(oracle_lib):
+    """One width w0 for every pair: cells at distance z > w0 have score 0, the rest
+    the full dot product (dense scores with the far band set to zero)."""
+    rng = np.random.default_rng(5)
+    d, n, w0 = 8, 19, 4
+    q = bf16_grid(rng, (1, n, 1, d))
+    k = bf16_grid(rng, (1, n, 1, d))
+    v = bf16_grid(rng, (1, n, 1, d))
+    o, lse, _ = oracle_lib.attend(q, k, v, 0, np.full(d // 2, float(w0)))
+    s = q[0, :, 0] @ k[0, :, 0].T / math.sqrt(d)
+    z = np.arange(n)[:, None] - np.arange(n)[None, :]
+    s = np.where(z > w0, 0.0, s)
+    s = np.where(z < 0, -np.inf, s)
+    od, lsed = dense_from_scores(s, v[0, :, 0], 1, 1)
+    np.testing.assert_allclose(o[0, :, 0], od, atol=1e-12)
+    np.testing.assert_allclose(lse[0, 0], lsed, atol=1e-12)
+
+
+# ----------------------------------------------------------------------------
+# check 3: term counts
+# ----------------------------------------------------------------------------
+def brute_force_count(w, n_q, q0, n_k):
+    T = C = 0
+    for i in range(n_q):
+        p = q0 + i
+        for j in range(n_k):
+            if j > p:
+                continue
+            C += 1
+            for wr in w:
+                if p - j <= wr:
+                    T += 1
+    return T, C
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_count_brute_force(oracle_lib, seed):
+    rng = np.random.default_rng(100 + seed)
+    d = int(rng.choice([2, 4, 8]))
+    base = float(rng.uniform(2.0, 500.0))
+    kwin = float(rng.choice([0.05, 0.3, 1.0, 2.0, 7.5]))
+    n_q = int(rng.integers(1, 30))
+    q0 = int(rng.integers(0, 20))
+    n_k = int(rng.integers(1, 50))
+    w = oracle_lib.window_widths(d, base, kwin)
+    bt, bc = brute_force_count(w, n_q, q0, n_k)
+    assert oracle_lib.count_terms(w, n_q, q0, n_k) == (bt, bc)
+    if q0 + n_q - 1 >= 0:
+        rng2 = np.random.default_rng(seed)
+        q = bf16_grid(rng2, (1, n_q, 1, d))
+        k = bf16_grid(rng2, (1, n_k, 1, d))
+        _, _, terms = oracle_lib.attend(q, k, k, q0, w)
+        assert int(terms.sum()) == bt
+
+
+def _pruned(oracle_lib, rec):
+    f = kv(rec)
+    d = int(f["d"])
+    base = float(f["base"])
+    kwin = float(f["k"])
+    N = int(f["N"])
+    theta = W.llama3_theta(d, base).numpy() if rec[1] == "llama3b" else None
+    qty = rec[5]
+    if qty == "pruned_prefill":
+        w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
+        T, C = oracle_lib.count_terms(w, N, 0, N)
+        return 100.0 * (1 - T / (C * d / 2))
+    if qty == "pruned_decode":   # query at position N over keys 0..N-1
+        w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N + 1)
+        T, C = oracle_lib.count_terms(w, 1, N, N)
+        return 100.0 * (1 - T / (C * d / 2))
+    if qty == "pruned_row":      # one row with n keys at distances 0..n-1
+        w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
+        T, C = oracle_lib.count_terms(w, 1, N - 1, N)
+        return 100.0 * (1 - T / (C * d / 2))
+    if qty == "terms_last_row_z":
+        w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
+        z = int(f["z"])
+        return float(np.sum(z <= w))
+    raise AssertionError(qty)
+
+
+@pytest.mark.parametrize("rec", read_golden("paper_pins.txt"), ids=lambda r: r[0])
+def test_paper_printed_counts(oracle_lib, rec):
+    f = kv(rec)
+    got = _pruned(oracle_lib, rec)
+    assert abs(got - float(f["value"])) <= float(f["tol"]), (rec[0], got)
+
+
+def R_interval(n0, n1, d, base, kwin):
+    """eq:Rgen with eq:Fdef: reduction of the row interval [n0, n1] (App. C)."""
+    wmin = 2 * math.pi * kwin
+    F = lambda n: n * n * (math.log(n / wmin) - 1.5) + 2 * wmin * n
+    return (F(n1) - F(n0)) / ((n1 * n1 - n0 * n0) * math.log(base))
+
+
+@pytest.mark.parametrize("rec", read_golden("closed_forms.txt"), ids=lambda r: r[0])
+def test_paper_closed_forms(rec):
+    """The printed closed-form values follow from the formulas as written."""
+    f = kv(rec)
+    B = float(f["base"])
+    lnB = math.log(B)
+    q = rec[1]
+    if q == "redprefill":
+        kwin, N = float(f["k"]), int(f["N"])
+        got = 100 * (math.log(N / (2 * math.pi * kwin)) - 1.5) / lnB
+    elif q in ("row_continuous", "rhostar"):
+        d, kwin, n = int(f["d"]), float(f["k"]), int(f["n"])
+        wmin = 2 * math.pi * kwin
+        rho = (d / 2) * math.log(n / wmin) / lnB
+        s = d / (2 * lnB) * (n - wmin) + (d / 2 - rho) * n     # eq:Kn
+        got = rho if q == "rhostar" else 100 * (1 - s / (d / 2 * n))
+    elif q == "gap":
+        got = 100 / (2 * lnB)
+    elif q == "saturation_decode":
+        got = 100 * (1 - 1 / lnB)
+    elif q == "half_minus_whole":
+        got = 100 * (1.5 - 1.27) / lnB
+    else:
+        raise AssertionError(q)
+    assert abs(got - float(f["value"])) <= float(f["tol"]), (rec[0], got)
+
+
+@pytest.mark.parametrize("N", [1024, 4096, 32768, 131072, 1048576])
+@pytest.mark.parametrize("d,base", [(64, 1e6), (128, 1e7), (128, 5e5)])
+def test_count_vs_closed_form_interval(oracle_lib, N, d, base):
+    """Exact discrete whole-prefill and decode reductions sit within the paper's
+    1-2 point integral-approximation error of eq:Rgen (we allow 2 points)."""
+    w = oracle_lib.window_widths(d, base, 2.0, n_ctx=N + 1)
+    T, C = oracle_lib.count_terms(w, N, 0, N)
+    exact = 1 - T / (C * d / 2)
+    assert abs(exact - R_interval(1, N, d, base, 2.0)) < 0.02
+    T, C = oracle_lib.count_terms(w, 1, N, N)
+    exact_dec = 1 - T / (C * d / 2)
+    wmin = 4 * math.pi
+    dec = (math.log(N / wmin) - 1 + wmin / N) / math.log(base)   # App. C Step 2, exact last row
+    assert abs(exact_dec - dec) < 0.02
+    # the appended-context interval [N/2, N] of App. C
+    T, C = oracle_lib.count_terms(w, N - N // 2, N // 2, N)
+    exact_half = 1 - T / (C * d / 2)
+    assert abs(exact_half - R_interval(N // 2, N, d, base, 2.0)) < 0.02
+
+
+def test_saturation_constant_terms_per_row(oracle_lib):
+    """Past N >= k*lambda_max every row keeps the same sum over pairs (Sec. 4 fact
+    (iii); App. C Step 3): B=100, d=8, k=2 gives floor widths [12, 39, 125, 397]."""
+    w = oracle_lib.window_widths(8, 100.0, 2.0)
+    assert list(np.floor(w).astype(int)) == [12, 39, 125, 397]
+    per_row = int(np.sum(np.floor(w) + 1))
+    assert per_row == 577
+    for p in (397, 398, 1000, 5000):
+        T, C = oracle_lib.count_terms(w, 1, p, p + 1)
+        assert T == per_row
+    # O(N) total: the count grows linearly once saturated
+    T1, _ = oracle_lib.count_terms(w, 1000, 4000, 10_000)
+    T2, _ = oracle_lib.count_terms(w, 2000, 4000, 10_000)
+    assert T2 == 2 * T1 == 2 * 1000 * per_row
+    # decode reduction tends to 1 beyond saturation
+    red = [1 - oracle_lib.count_terms(w, 1, N, N)[0] / (4 * N) for N in (1000, 10_000, 100_000)]
+    assert red[0] < red[1] < red[2] < 1
+
+
+def test_window_widths_basics(oracle_lib):
+    # theta' = 0 is a position-free pair: width = N (never pruned within N)
+    w = oracle_lib.window_widths(4, 10.0, 2.0, theta=np.array([1.0, 0.0]), n_ctx=1000.0)
+    assert w[1] == 1000.0 and w[0] == pytest.approx(4 * math.pi)
+    # min(k lambda, N)
+    w = oracle_lib.window_widths(8, 100.0, 2.0, n_ctx=50.0)
+    assert math.floor(w[0]) == 12 and math.floor(w[1]) == 39
+    assert w[2] == 50.0 and w[3] == 50.0
+    # non-decreasing in r for every workload table
+    for wl in W.WORKLOADS.values():
+        th = W.workload_theta(wl)
+        ww = oracle_lib.window_widths(wl.head_dim, wl.rope_base, wl.k,
+                                      th.numpy() if th is not None else None)
+        assert np.all(np.diff(ww) >= 0)
+    with pytest.raises(ValueError):
+        oracle_lib.window_widths(8, 100.0, 0.0)
+    with pytest.raises(ValueError):
+        oracle_lib.window_widths(8, 100.0, float("nan"))
