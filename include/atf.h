@@ -1,0 +1,149 @@
+/*
+ * atf.h -- C ABI of libatf.so: per-RoPE-wavelength windowed causal attention
+ * (ATFlash, arXiv 2608.02947) on one AMD MI355X (gfx950).
+ *
+ * The method.  Queries and keys arrive already RoPE-rotated (q~, k~ of Sec. 3.1)
+ * in the rotate-half layout: rotary pair r (r = 0 .. d/2-1, r = 0 the highest
+ * frequency) is made of dims r and r + d/2.  The rotated score of a query at
+ * position n and a key at position m splits exactly into one term per pair
+ * (Sec. 3.1, eq:pair).  With theta_r = B^(-2r/d) (or an effective theta'_r when
+ * the model scales its RoPE, Sec. 3.2 last paragraph), wavelength
+ * lambda_r = 2*pi/theta_r (eq:lambda) and window w_r = min(k*lambda_r, N)
+ * (Sec. 3.2, eq:window), the term of pair r is kept at distance z = n - m only
+ * when z <= w_r.  Kept terms are summed and scaled; softmax and the product with
+ * V are ordinary causal attention (FlashAttention recurrences, Fig. fa).  No token
+ * is dropped: a cell whose every pair is pruned has score 0.
+ *
+ * Positions.  Query row i of a prefill call sits at position q_pos0 + i; key j
+ * sits at position j.  Row i attends keys j <= q_pos0 + i (causal).  Because z
+ * never exceeds the largest position, the min(., N) of eq:window never binds and
+ * the integer threshold W_r = floor(k*lambda_r) decides: keep iff z <= W_r.
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: ATF_OK (0) or a negative ATF_E* code.  On error nothing is
+ *     launched and no output is written; atf_last_error() describes the cause.
+ *   - Device pointers are caller-owned, on the current HIP device, contiguous,
+ *     and 16-byte aligned (lse: 4-byte aligned).  The library allocates no
+ *     device memory.
+ *   - ATF_OK from a call that launches work means "enqueued on hip_stream"
+ *     (a hipStream_t; NULL = the null stream).  Faults surface at the caller's
+ *     next synchronisation.  Launch failures return ATF_EHIP.
+ *   - No C++ exception crosses this interface.  The library keeps no mutable
+ *     global state besides a thread-local error string.
+ *   - bf16 is IEEE binary32 truncated to its top 16 bits (stored as uint16);
+ *     scores, softmax statistics and accumulators are fp32.
+ */
+#ifndef ATF_H
+#define ATF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    ATF_OK = 0,
+    ATF_EINVAL = -1,       /* an argument is out of range, NULL, or misaligned */
+    ATF_EUNSUPPORTED = -2, /* valid but not built: head_dim other than 64/128, GQA ratio > 8 not dividing */
+    ATF_EWORKSPACE = -3,   /* decode workspace missing or smaller than atf_decode_workspace_bytes() */
+    ATF_EHIP = -4          /* a HIP runtime call failed (launch error) */
+};
+
+/* Window parameters (Sec. 3.2: k is the only free parameter; the table follows
+ * from the model's RoPE constants, or from its effective frequencies). */
+typedef struct atf_window {
+    int32_t head_dim;        /* d; 64 or 128 for the GPU entry points, any even d >= 2 for the host ones */
+    double rope_base;        /* B > 1; used only when inv_freq is NULL */
+    double k;                /* retained periods, > 0; +INFINITY turns the window off */
+    const double *inv_freq;  /* optional HOST array [d/2] of effective theta'_r >= 0
+                                (e.g. llama3 rope_scaling); NULL => theta_r = B^(-2r/d).
+                                theta'_r == 0 is a position-free pair (never pruned). */
+} atf_window;
+
+/* Window table (Sec. 3.2 eq:window with eq:lambda): W_out[r] = floor(k*2*pi/theta_r)
+ * computed in fp64 and clamped to [0, 2^31 - 1] (the clamp is exact because
+ * positions stay below 2^31 - 1).  W_out: host int32 array of d/2 entries.
+ * Errors: ATF_EINVAL for a NULL pointer, odd or non-positive d, k <= 0 or NaN,
+ * B <= 1 (without inv_freq), or a negative/NaN inv_freq entry. */
+int atf_window_table(const atf_window *w, int32_t *W_out);
+
+/* Retained inner-product terms of Sec. 4 for ONE (batch, query head): the number
+ * of (causal cell, pair) terms kept by the window over query rows at positions
+ * q_pos0 .. q_pos0 + n_q - 1 and keys 0 .. n_k - 1, and the number of causal
+ * cells (the full-attention count is causal_cells * d/2).  Exact closed form per
+ * pair; host only, no device work.  The reduction rate of Sec. 4 is
+ * 1 - retained / (causal_cells * d/2).
+ * Errors: ATF_EINVAL for NULL outputs, n_q < 0, q_pos0 < 0, n_k < 0, or a bad window. */
+int atf_count_terms(const atf_window *w, int64_t n_q, int64_t q_pos0, int64_t n_k,
+                    uint64_t *retained, uint64_t *causal_cells);
+
+/* Prefill (chunked or whole): windowed causal attention of n_q query rows
+ * against n_k keys, tiled with an online softmax; the window is applied as a
+ * per-tile slice of the QK contraction axis (Sec. 3.3): fully kept pair-chunks
+ * are MFMA K-steps, fully pruned ones are neither loaded nor multiplied, and
+ * pairs whose window ends inside the tile are masked per element.
+ *   q   bf16 [batch][n_q][h_q][d]   rotated queries          (device, read)
+ *   k   bf16 [batch][n_k][h_kv][d]  rotated keys             (device, read)
+ *   v   bf16 [batch][n_k][h_kv][d]  values                   (device, read)
+ *   o   bf16 [batch][n_q][h_q][d]   output, O/l rounded to nearest even (device, written)
+ *   lse fp32 [batch][h_q][n_q]      natural-log sum of exp of the scaled scores (device, written)
+ * Query head h uses key/value head h / (h_q / h_kv).  softmax_scale <= 0 selects
+ * 1/sqrt(d).  n_q == 0 is a no-op.
+ * Errors: ATF_EINVAL (NULL/misaligned pointer, batch < 1, n_q < 0, n_k < 1,
+ * q_pos0 < 0, q_pos0 + n_q > 2^31 - 1, n_k > 2^31 - 1, h_q % h_kv != 0, bad window,
+ * non-finite scale); ATF_EUNSUPPORTED (d not 64 or 128); ATF_EHIP. */
+int atf_prefill(const void *q, const void *k, const void *v, void *o, float *lse,
+                int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
+                int32_t h_q, int32_t h_kv, const atf_window *w,
+                float softmax_scale, void *hip_stream);
+
+/* Pair-chunk width C_p (rotary pairs per chunk) of the decode K cache.  One
+ * chunk of one token is 2*C_p bf16: dims [c*C_p, c*C_p + C_p) followed by dims
+ * [d/2 + c*C_p, d/2 + c*C_p + C_p).  Returns 0 for an unsupported head_dim. */
+int32_t atf_kcache_chunk_pairs(int32_t head_dim);
+
+/* Repack a key cache from [batch][n_k][h_kv][d] (bf16, as prefill reads it) to
+ * the pair-chunk-major decode layout [batch][h_kv][d/(2*C_p)][n_k][2*C_p], in
+ * which every pair-chunk of a head is a contiguous stream over tokens, so that
+ * decode reads only the tokens whose window still covers that chunk.  Pure data
+ * movement (bit-exact).  k_bshd and k_pcm must not overlap.
+ * Errors: ATF_EINVAL, ATF_EUNSUPPORTED (d), ATF_EHIP. */
+int atf_pack_kcache(const void *k_bshd, void *k_pcm, int32_t batch, int64_t n_k,
+                    int32_t h_kv, int32_t head_dim, void *hip_stream);
+
+/* Bytes of device workspace that atf_decode needs for these sizes (split-KV
+ * partial softmax states).  Returns 0 for invalid sizes. */
+size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int64_t n_k,
+                                  int32_t head_dim);
+
+/* Decode: one query token per batch row at position q_pos, against keys
+ * 0 .. min(q_pos, n_k - 1) of that row's cache (the last query row of Fig. fa).
+ * The cache is split over tokens; each split keeps partial (max, normaliser,
+ * output) states that a second kernel merges (split-KV, Sec. 5).  For pair-chunk
+ * c only the token suffix whose distance is within the chunk's largest window
+ * is read; pairs whose window ends inside that suffix are masked per token.
+ *   q        bf16 [batch][h_q][d]                        (device, read)
+ *   k_cache  bf16 pair-chunk-major, see atf_pack_kcache   (device, read)
+ *   v_cache  bf16 [batch][h_kv][n_k][d]                   (device, read)
+ *   o        bf16 [batch][h_q][d]                         (device, written)
+ *   lse      fp32 [batch][h_q]                            (device, written)
+ *   workspace: device, >= atf_decode_workspace_bytes(batch, h_q, h_kv, n_k, d)
+ *              bytes, 16-byte aligned, caller-owned; contents are scratch.
+ * Errors: ATF_EINVAL (pointers, sizes, q_pos < 0, q_pos > 2^31 - 2, bad window or
+ * scale), ATF_EUNSUPPORTED (d not 64/128, or h_q/h_kv > 8 and not a multiple
+ * of a divisor <= 8), ATF_EWORKSPACE, ATF_EHIP. */
+int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o, float *lse,
+               int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
+               const atf_window *w, float softmax_scale,
+               void *workspace, size_t workspace_bytes, void *hip_stream);
+
+/* Message of the most recent failed call on this thread ("" if none). */
+const char *atf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATF_H */

@@ -1,0 +1,206 @@
+"""Python binding of libatf.so: per-RoPE-wavelength windowed causal attention on MI355X.
+
+Argument marshalling only.  Every step of prefill and decode runs in the HIP
+kernels of ``libatf.so`` (built from ``csrc/`` by ``python -m
+paper_2608_02947_amd.build``); torch supplies device memory and the current HIP
+stream.  Importing this package loads the library and raises if it is missing:
+there is no fallback path.
+
+The functions carry the C names of ``include/atf.h``:
+
+- :func:`atf_window_table`, :func:`atf_count_terms` -- host only.
+- :func:`atf_prefill` -- windowed prefill (chunked via ``q_pos0``).
+- :func:`atf_pack_kcache`, :func:`atf_kcache_chunk_pairs` -- decode K-cache layout.
+- :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libatf.so")
+
+ATF_OK = 0
+ATF_EINVAL = -1
+ATF_EUNSUPPORTED = -2
+ATF_EWORKSPACE = -3
+ATF_EHIP = -4
+
+
+class AtfError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"atf error {code}: {message}")
+        self.code = code
+
+
+class _CWindow(ctypes.Structure):
+    _fields_ = [("head_dim", ctypes.c_int32), ("rope_base", ctypes.c_double),
+                ("k", ctypes.c_double), ("inv_freq", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2608_02947_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    W = ctypes.POINTER(_CWindow)
+    sig = {
+        "atf_window_table": (ctypes.c_int, [W, P]),
+        "atf_count_terms": (ctypes.c_int, [W, i64, i64, i64, P, P]),
+        "atf_prefill": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, W, f32, P]),
+        "atf_kcache_chunk_pairs": (ctypes.c_int32, [i32]),
+        "atf_pack_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
+        "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
+        "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, W, f32, P,
+                                      ctypes.c_size_t, P]),
+        "atf_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+EXPORTED = ("atf_window_table", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
+            "atf_pack_kcache", "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
+
+
+def library():
+    """The loaded ctypes library (for tests of the raw C interface)."""
+    return _lib
+
+
+def atf_last_error() -> str:
+    return _lib.atf_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != ATF_OK:
+        raise AtfError(rc, atf_last_error())
+
+
+@dataclasses.dataclass
+class Window:
+    """atf_window: d, RoPE base B, retained periods k (+inf = off), optional theta'_r."""
+    head_dim: int
+    rope_base: float
+    k: float
+    inv_freq: Optional[Sequence[float]] = None
+
+    def as_c(self):
+        arr = None
+        if self.inv_freq is not None:
+            arr = np.ascontiguousarray(np.asarray(self.inv_freq, dtype=np.float64))
+        cw = _CWindow(int(self.head_dim), float(self.rope_base), float(self.k),
+                      arr.ctypes.data if arr is not None else None)
+        return cw, arr  # keep arr alive for the duration of the call
+
+
+def atf_window_table(window: Window) -> np.ndarray:
+    cw, keep = window.as_c()
+    out = np.zeros(window.head_dim // 2, dtype=np.int32)
+    _check(_lib.atf_window_table(ctypes.byref(cw), out.ctypes.data))
+    return out
+
+
+def atf_count_terms(window: Window, n_q: int, q_pos0: int, n_k: int):
+    """(retained terms, causal cells) per (batch, query head)."""
+    cw, keep = window.as_c()
+    r = ctypes.c_uint64()
+    c = ctypes.c_uint64()
+    _check(_lib.atf_count_terms(ctypes.byref(cw), n_q, q_pos0, n_k, ctypes.byref(r),
+                                ctypes.byref(c)))
+    return r.value, c.value
+
+
+def atf_kcache_chunk_pairs(head_dim: int) -> int:
+    return int(_lib.atf_kcache_chunk_pairs(head_dim))
+
+
+def atf_decode_workspace_bytes(batch: int, h_q: int, h_kv: int, n_k: int, head_dim: int) -> int:
+    return int(_lib.atf_decode_workspace_bytes(batch, h_q, h_kv, n_k, head_dim))
+
+
+# ---------------------------------------------------------------------------
+# device entry points (torch tensors on the current HIP device)
+# ---------------------------------------------------------------------------
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def atf_prefill(q, k, v, o, lse, q_pos0: int, window: Window, softmax_scale: float = 0.0,
+                stream=None):
+    """q [B, n_q, h_q, d], k/v [B, n_k, h_kv, d], o like q (bf16); lse [B, h_q, n_q] fp32."""
+    torch = _torch()
+    B, n_q, h_q, d = q.shape
+    _, n_k, h_kv, _ = k.shape
+    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
+            tuple(lse.shape) != (B, h_q, n_q) or k.shape[0] != B or k.shape[3] != d:
+        raise ValueError("atf_prefill: inconsistent shapes")
+    cw, keep = window.as_c()
+    rc = _lib.atf_prefill(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+                          _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+                          _dev_ptr(lse, torch.float32, "lse"), B, n_q, n_k, q_pos0, h_q, h_kv,
+                          ctypes.byref(cw), float(softmax_scale), _stream_ptr(stream))
+    _check(rc)
+
+
+def atf_pack_kcache(k_bshd, k_pcm, stream=None):
+    """k_bshd [B, n_k, h_kv, d] -> k_pcm [B, h_kv, d/16, n_k, 16] (bf16)."""
+    torch = _torch()
+    B, n_k, h_kv, d = k_bshd.shape
+    if k_pcm.numel() != k_bshd.numel():
+        raise ValueError("atf_pack_kcache: destination size mismatch")
+    _check(_lib.atf_pack_kcache(_dev_ptr(k_bshd, torch.bfloat16, "k_bshd"),
+                                _dev_ptr(k_pcm, torch.bfloat16, "k_pcm"), B, n_k, h_kv, d,
+                                _stream_ptr(stream)))
+
+
+def atf_decode(q, k_pcm, v_cache, o, lse, q_pos: int, window: Window, workspace,
+               softmax_scale: float = 0.0, stream=None):
+    """q [B, h_q, d]; k_pcm pair-chunk-major; v_cache [B, h_kv, n_k, d]; o [B, h_q, d];
+    lse [B, h_q]; workspace: uint8 device tensor of atf_decode_workspace_bytes()."""
+    torch = _torch()
+    B, h_q, d = q.shape
+    _, h_kv, n_k, _ = v_cache.shape
+    if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
+            k_pcm.numel() != v_cache.numel():
+        raise ValueError("atf_decode: inconsistent shapes")
+    cw, keep = window.as_c()
+    rc = _lib.atf_decode(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pcm, torch.bfloat16, "k"),
+                         _dev_ptr(v_cache, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+                         _dev_ptr(lse, torch.float32, "lse"), B, n_k, q_pos, h_q, h_kv,
+                         ctypes.byref(cw), float(softmax_scale),
+                         _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
+                         _stream_ptr(stream))
+    _check(rc)

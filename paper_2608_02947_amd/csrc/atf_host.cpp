@@ -1,0 +1,347 @@
+// Host side of libatf.so: argument validation, the window table, the exact
+// retained-term count, and dispatch to the gfx950 kernels.  See include/atf.h.
+#include "atf.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <new>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "atf_internal.hpp"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+constexpr int64_t kPosLimit = 2147483647;  // positions and thresholds are int32 on the device
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// W_r = floor(k * lambda_r), lambda_r = 2*pi/theta_r (eq:lambda, eq:window), in
+// fp64, clamped to [0, 2^31 - 1].  Works for any even d <= 2 * max_pairs.
+int window_thresholds(const atf_window* w, int32_t* out, int max_pairs) {
+    if (w == nullptr || out == nullptr) return fail(ATF_EINVAL, "window: NULL pointer");
+    const int d = w->head_dim;
+    if (d < 2 || d % 2 != 0 || d / 2 > max_pairs)
+        return fail(ATF_EINVAL, "window: head_dim %d must be even, >= 2 and <= %d", d,
+                    2 * max_pairs);
+    if (!(w->k > 0.0))
+        return fail(ATF_EINVAL, "window: k must be > 0 (got %g)", w->k);
+    if (w->inv_freq == nullptr && !(w->rope_base > 1.0 && std::isfinite(w->rope_base)))
+        return fail(ATF_EINVAL, "window: rope_base must be finite and > 1 (got %g)",
+                    w->rope_base);
+    const double two_pi = 6.283185307179586476925286766559;
+    for (int r = 0; r < d / 2; ++r) {
+        double theta;
+        if (w->inv_freq) {
+            theta = w->inv_freq[r];
+            if (!(theta >= 0.0) || std::isinf(theta))
+                return fail(ATF_EINVAL, "window: inv_freq[%d] = %g must be finite and >= 0", r,
+                            theta);
+        } else {
+            theta = std::pow(w->rope_base, -2.0 * r / d);
+        }
+        const double lambda = two_pi / theta;  // +inf for a position-free pair
+        const double kl = w->k * lambda;
+        double t = std::floor(kl);
+        if (!(t < static_cast<double>(kPosLimit))) t = static_cast<double>(kPosLimit);
+        if (t < 0.0) t = 0.0;
+        out[r] = static_cast<int32_t>(t);
+    }
+    return ATF_OK;
+}
+
+int build_table(const atf_window* w, atf::WindowTable* t) {
+    std::memset(t, 0, sizeof *t);
+    int rc = window_thresholds(w, t->W, atf::kMaxPairs);
+    if (rc != ATF_OK) return rc;
+    const int pairs = w->head_dim / 2;
+    for (int c = 0; c * atf::kChunkPairs < pairs; ++c) {
+        int32_t lo = INT32_MAX, hi = 0;
+        for (int e = 0; e < atf::kChunkPairs; ++e) {
+            const int32_t x = t->W[c * atf::kChunkPairs + e];
+            lo = x < lo ? x : lo;
+            hi = x > hi ? x : hi;
+        }
+        t->chunk_min[c] = lo;
+        t->chunk_max[c] = hi;
+    }
+    return ATF_OK;
+}
+
+using u128 = unsigned __int128;
+
+// sum_{p=a}^{c} (p + 1), 0 <= a <= c
+u128 sum_p_plus_1(int64_t a, int64_t c) {
+    if (c < a) return 0;
+    const u128 n = static_cast<u128>(c - a + 1);
+    return n * static_cast<u128>(a + c + 2) / 2;
+}
+
+// Kept keys of one pair with threshold W, summed over rows p in [p0, p1]:
+// per row, keys j in [max(0, p - W), min(p, n_k - 1)].
+u128 pair_count(int64_t W, int64_t p0, int64_t p1, int64_t n_k) {
+    u128 total = 0;
+    // rows with p <= n_k - 1: min(p, W) + 1 keys
+    {
+        const int64_t a = p0, b = p1 < n_k - 1 ? p1 : n_k - 1;
+        if (a <= b) {
+            const int64_t c = b < W ? b : W;        // rows where p <= W: p + 1 keys
+            total += sum_p_plus_1(a, c);
+            const int64_t s = a > W + 1 ? a : W + 1;  // rows where p > W: W + 1 keys
+            if (s <= b) total += static_cast<u128>(b - s + 1) * static_cast<u128>(W + 1);
+        }
+    }
+    // rows with p >= n_k: n_k keys while p <= W, then n_k + W - p until it hits 0
+    {
+        const int64_t a = p0 > n_k ? p0 : n_k, b = p1;
+        if (a <= b) {
+            const int64_t c = b < W ? b : W;
+            if (a <= c) total += static_cast<u128>(c - a + 1) * static_cast<u128>(n_k);
+            const int64_t x = a > W + 1 ? a : W + 1;
+            const int64_t y = b < n_k + W - 1 ? b : n_k + W - 1;
+            if (x <= y) {
+                const u128 n = static_cast<u128>(y - x + 1);
+                total += n * static_cast<u128>(n_k + W) - n * static_cast<u128>(x + y) / 2;
+            }
+        }
+    }
+    return total;
+}
+
+}  // namespace
+
+namespace atf {
+
+int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k) {
+    // enough workgroups to fill 256 CUs several times over, but never a split
+    // shorter than one workgroup step
+    const int64_t target_groups = 1024;
+    int64_t s = (target_groups + int64_t(batch) * h_kv - 1) / (int64_t(batch) * h_kv);
+    const int64_t max_s = (n_k + kDecodeTokenStep - 1) / kDecodeTokenStep;
+    if (s > max_s) s = max_s;
+    if (s < 1) s = 1;
+    return static_cast<int32_t>(s);
+}
+
+}  // namespace atf
+
+extern "C" {
+
+const char* atf_last_error(void) { return g_last_error.c_str(); }
+
+int atf_window_table(const atf_window* w, int32_t* W_out) {
+    return window_thresholds(w, W_out, 1 << 20);
+}
+
+int atf_count_terms(const atf_window* w, int64_t n_q, int64_t q_pos0, int64_t n_k,
+                    uint64_t* retained, uint64_t* causal_cells) {
+    if (retained == nullptr || causal_cells == nullptr)
+        return fail(ATF_EINVAL, "count_terms: NULL output");
+    if (n_q < 0 || q_pos0 < 0 || n_k < 0)
+        return fail(ATF_EINVAL, "count_terms: n_q, q_pos0 and n_k must be >= 0");
+    if (q_pos0 > INT64_MAX / 4 - n_q || n_k > INT64_MAX / 4)
+        return fail(ATF_EINVAL, "count_terms: sizes too large");
+    if (w == nullptr) return fail(ATF_EINVAL, "count_terms: NULL window");
+    const int pairs = w->head_dim / 2;
+    if (w->head_dim < 2 || w->head_dim % 2 || pairs > (1 << 20))
+        return fail(ATF_EINVAL, "count_terms: bad head_dim %d", w->head_dim);
+    int32_t* W = new (std::nothrow) int32_t[pairs];
+    if (!W) return fail(ATF_EINVAL, "count_terms: out of host memory");
+    int rc = window_thresholds(w, W, pairs);
+    if (rc != ATF_OK) {
+        delete[] W;
+        return rc;
+    }
+    u128 ret = 0, cau = 0;
+    if (n_q > 0 && n_k > 0) {
+        const int64_t p0 = q_pos0, p1 = q_pos0 + n_q - 1;
+        for (int r = 0; r < pairs; ++r) ret += pair_count(W[r], p0, p1, n_k);
+        cau = pair_count(INT64_MAX / 8, p0, p1, n_k);  // every key kept
+    }
+    delete[] W;
+    if (ret > static_cast<u128>(UINT64_MAX) || cau > static_cast<u128>(UINT64_MAX))
+        return fail(ATF_EINVAL, "count_terms: count exceeds 64 bits");
+    *retained = static_cast<uint64_t>(ret);
+    *causal_cells = static_cast<uint64_t>(cau);
+    return ATF_OK;
+}
+
+int32_t atf_kcache_chunk_pairs(int32_t head_dim) {
+    return (head_dim == 64 || head_dim == 128) ? atf::kChunkPairs : 0;
+}
+
+int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse,
+                int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
+                int32_t h_kv, const atf_window* w, float softmax_scale, void* hip_stream) {
+    if (w == nullptr) return fail(ATF_EINVAL, "prefill: NULL window");
+    const int d = w->head_dim;
+    if (d != 64 && d != 128)
+        return fail(ATF_EUNSUPPORTED, "prefill: head_dim %d not built (64 or 128)", d);
+    if (batch < 1 || n_q < 0 || n_k < 1 || q_pos0 < 0 || h_q < 1 || h_kv < 1)
+        return fail(ATF_EINVAL,
+                    "prefill: need batch >= 1, n_q >= 0, n_k >= 1, q_pos0 >= 0, heads >= 1");
+    if (h_q % h_kv != 0)
+        return fail(ATF_EINVAL, "prefill: h_q %d not a multiple of h_kv %d", h_q, h_kv);
+    if (q_pos0 + n_q > kPosLimit || n_k > kPosLimit)
+        return fail(ATF_EINVAL, "prefill: positions must stay below 2^31 - 1");
+    if (!std::isfinite(softmax_scale))
+        return fail(ATF_EINVAL, "prefill: softmax_scale must be finite");
+    atf::PrefillParams p{};
+    int rc = build_table(w, &p.win);
+    if (rc != ATF_OK) return rc;
+    if (n_q == 0) return ATF_OK;
+    if (!q || !k || !v || !o || !lse) return fail(ATF_EINVAL, "prefill: NULL tensor pointer");
+    if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+        !aligned(lse, 4))
+        return fail(ATF_EINVAL, "prefill: q/k/v/o must be 16-byte and lse 4-byte aligned");
+    const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
+    p.q = static_cast<const uint16_t*>(q);
+    p.k = static_cast<const uint16_t*>(k);
+    p.v = static_cast<const uint16_t*>(v);
+    p.o = static_cast<uint16_t*>(o);
+    p.lse = lse;
+    p.batch = batch;
+    p.n_q = static_cast<int32_t>(n_q);
+    p.n_k = static_cast<int32_t>(n_k);
+    p.q_pos0 = static_cast<int32_t>(q_pos0);
+    p.h_q = h_q;
+    p.h_kv = h_kv;
+    p.group = h_q / h_kv;
+    p.scale_log2 = scale * 1.4426950408889634f;
+    hipError_t e = atf::launch_prefill(p, d, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "prefill: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
+}
+
+int atf_pack_kcache(const void* k_bshd, void* k_pcm, int32_t batch, int64_t n_k, int32_t h_kv,
+                    int32_t head_dim, void* hip_stream) {
+    if (head_dim != 64 && head_dim != 128)
+        return fail(ATF_EUNSUPPORTED, "pack_kcache: head_dim %d not built", head_dim);
+    if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit)
+        return fail(ATF_EINVAL, "pack_kcache: need batch >= 1, 1 <= n_k < 2^31, h_kv >= 1");
+    if (!k_bshd || !k_pcm) return fail(ATF_EINVAL, "pack_kcache: NULL pointer");
+    if (!aligned(k_bshd, 16) || !aligned(k_pcm, 16))
+        return fail(ATF_EINVAL, "pack_kcache: pointers must be 16-byte aligned");
+    const size_t bytes = size_t(batch) * size_t(n_k) * size_t(h_kv) * size_t(head_dim) * 2;
+    const char* a = static_cast<const char*>(k_bshd);
+    const char* b = static_cast<const char*>(k_pcm);
+    if (a < b + bytes && b < a + bytes) return fail(ATF_EINVAL, "pack_kcache: buffers overlap");
+    atf::PackParams p{static_cast<const uint16_t*>(k_bshd), static_cast<uint16_t*>(k_pcm), batch,
+                      static_cast<int32_t>(n_k), h_kv};
+    hipError_t e = atf::launch_pack_kcache(p, head_dim, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "pack_kcache: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
+}
+
+namespace {
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct WsLayout {
+    size_t off_m, off_l, off_o, total;
+};
+
+WsLayout ws_layout(int32_t batch, int32_t h_q, int32_t splits, int32_t head_dim) {
+    const size_t n = size_t(batch) * size_t(h_q) * size_t(splits);
+    WsLayout L;
+    L.off_m = 0;
+    L.off_l = align_up(n * 4, 256);
+    L.off_o = L.off_l + align_up(n * 4, 256);
+    L.total = L.off_o + align_up(n * size_t(head_dim) * 4, 256);
+    return L;
+}
+}  // namespace
+
+size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int64_t n_k,
+                                  int32_t head_dim) {
+    if (batch < 1 || h_q < 1 || h_kv < 1 || h_q % h_kv || n_k < 1 || n_k > kPosLimit ||
+        (head_dim != 64 && head_dim != 128))
+        return 0;
+    const int32_t s = atf::decode_splits(batch, h_kv, n_k);
+    return ws_layout(batch, h_q, s, head_dim).total;
+}
+
+int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+               int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
+               const atf_window* w, float softmax_scale, void* workspace,
+               size_t workspace_bytes, void* hip_stream) {
+    if (w == nullptr) return fail(ATF_EINVAL, "decode: NULL window");
+    const int d = w->head_dim;
+    if (d != 64 && d != 128)
+        return fail(ATF_EUNSUPPORTED, "decode: head_dim %d not built (64 or 128)", d);
+    if (batch < 1 || n_k < 1 || q_pos < 0 || h_q < 1 || h_kv < 1)
+        return fail(ATF_EINVAL, "decode: need batch >= 1, n_k >= 1, q_pos >= 0, heads >= 1");
+    if (h_q % h_kv != 0)
+        return fail(ATF_EINVAL, "decode: h_q %d not a multiple of h_kv %d", h_q, h_kv);
+    if (q_pos >= kPosLimit || n_k > kPosLimit)
+        return fail(ATF_EINVAL, "decode: positions must stay below 2^31 - 1");
+    if (!std::isfinite(softmax_scale))
+        return fail(ATF_EINVAL, "decode: softmax_scale must be finite");
+    atf::DecodeParams p{};
+    int rc = build_table(w, &p.win);
+    if (rc != ATF_OK) return rc;
+    if (!q || !k_cache || !v_cache || !o || !lse)
+        return fail(ATF_EINVAL, "decode: NULL tensor pointer");
+    if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
+        !aligned(lse, 4))
+        return fail(ATF_EINVAL, "decode: q/k/v/o must be 16-byte and lse 4-byte aligned");
+    const int32_t splits = atf::decode_splits(batch, h_kv, n_k);
+    const WsLayout L = ws_layout(batch, h_q, splits, d);
+    if (workspace == nullptr || workspace_bytes < L.total)
+        return fail(ATF_EWORKSPACE, "decode: workspace of %zu bytes needed, %zu given", L.total,
+                    workspace == nullptr ? size_t(0) : workspace_bytes);
+    if (!aligned(workspace, 16)) return fail(ATF_EINVAL, "decode: workspace must be 16-byte aligned");
+    const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
+    const int32_t group = h_q / h_kv;
+    int32_t hpb = 1;
+    for (int32_t c = 8; c >= 1; --c)
+        if (group % c == 0) {
+            hpb = c;
+            break;
+        }
+    char* ws = static_cast<char*>(workspace);
+    p.q = static_cast<const uint16_t*>(q);
+    p.kpcm = static_cast<const uint16_t*>(k_cache);
+    p.v = static_cast<const uint16_t*>(v_cache);
+    p.o = static_cast<uint16_t*>(o);
+    p.lse = lse;
+    p.ws_m = reinterpret_cast<float*>(ws + L.off_m);
+    p.ws_l = reinterpret_cast<float*>(ws + L.off_l);
+    p.ws_o = reinterpret_cast<float*>(ws + L.off_o);
+    p.batch = batch;
+    p.n_k = static_cast<int32_t>(n_k);
+    p.q_pos = static_cast<int32_t>(q_pos);
+    p.h_q = h_q;
+    p.h_kv = h_kv;
+    p.group = group;
+    p.heads_per_block = hpb;
+    const int64_t last = q_pos < n_k - 1 ? q_pos : n_k - 1;
+    p.n_valid = static_cast<int32_t>(last + 1);
+    p.splits = splits;
+    const int64_t per = (p.n_valid + splits - 1) / splits;
+    const int64_t step_tokens = (per + atf::kDecodeTokenStep - 1) / atf::kDecodeTokenStep *
+                                atf::kDecodeTokenStep;
+    if (step_tokens * splits >= kPosLimit)
+        return fail(ATF_EINVAL, "decode: cache too long for the split plan");
+    p.split_tokens = static_cast<int32_t>(step_tokens);
+    p.scale_log2 = scale * 1.4426950408889634f;
+    hipError_t e = atf::launch_decode(p, d, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "decode: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// Internal declarations shared by the host side of libatf.so and its kernels.
+// Not part of the public ABI (include/atf.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace atf {
+
+constexpr int kMaxPairs = 64;     // d/2 for d = 128
+constexpr int kChunkPairs = 8;    // pairs per QK K-step and per decode K-cache chunk
+constexpr int kMaxChunks = kMaxPairs / kChunkPairs;
+
+// Window table in the form every kernel consumes: per pair the integer threshold
+// W_r (keep the pair's term at distance z iff z <= W_r), and per chunk of
+// kChunkPairs consecutive pairs the smallest and largest threshold.
+struct WindowTable {
+    int32_t W[kMaxPairs];
+    int32_t chunk_min[kMaxChunks];
+    int32_t chunk_max[kMaxChunks];
+};
+
+struct PrefillParams {
+    const uint16_t* q;   // [B][n_q][h_q][d]
+    const uint16_t* k;   // [B][n_k][h_kv][d]
+    const uint16_t* v;   // [B][n_k][h_kv][d]
+    uint16_t* o;         // [B][n_q][h_q][d]
+    float* lse;          // [B][h_q][n_q]
+    int32_t batch, n_q, n_k, q_pos0, h_q, h_kv, group;
+    int32_t n_qtiles;
+    float scale_log2;    // softmax scale * log2(e)
+    WindowTable win;
+};
+
+struct DecodeParams {
+    const uint16_t* q;       // [B][h_q][d]
+    const uint16_t* kpcm;    // [B][h_kv][d/16][n_k][16]
+    const uint16_t* v;       // [B][h_kv][n_k][d]
+    uint16_t* o;             // [B][h_q][d]
+    float* lse;              // [B][h_q]
+    float* ws_m;             // [B][h_q][splits]   running max (log2 domain)
+    float* ws_l;             // [B][h_q][splits]   normaliser
+    float* ws_o;             // [B][h_q][splits][d] unnormalised output
+    int32_t batch, n_k, q_pos, h_q, h_kv, group;
+    int32_t heads_per_block;  // query heads handled by one workgroup (divides group, <= 8)
+    int32_t n_valid;          // keys 0 .. n_valid - 1 are causal
+    int32_t splits;
+    int32_t split_tokens;     // tokens per split (multiple of the workgroup's token step)
+    float scale_log2;
+    WindowTable win;
+};
+
+struct PackParams {
+    const uint16_t* src;  // [B][n_k][h_kv][d]
+    uint16_t* dst;        // [B][h_kv][d/16][n_k][16]
+    int32_t batch, n_k, h_kv;
+};
+
+// Kernel launchers (prefill.hip, decode.hip).  Return the HIP error of the launch.
+hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream);
+
+// Decode split plan: number of KV splits per (batch, kv head) for these sizes.
+int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);
+// Tokens handled per decode workgroup iteration (the split granularity).
+constexpr int32_t kDecodeTokenStep = 256;
+
+}  // namespace atf

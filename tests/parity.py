@@ -1,0 +1,115 @@
+"""Helpers of the GPU parity tests: run the HIP path through the C ABI, run the
+oracle on the same seeded inputs, and compare to the stated tolerances.
+
+Tolerances (bf16 inputs, fp32 accumulation, bf16 output): O max-abs <= 1e-2 and
+mean-abs <= 1e-3, LSE max-abs <= 1e-3.  Term counts are compared bit-exactly.
+"""
+from __future__ import annotations
+
+import math
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+import workloads as W
+
+O_MAX_ABS = 1e-2
+O_MEAN_ABS = 1e-3
+LSE_MAX_ABS = 1e-3
+
+
+def note(msg: str):
+    """Name the GPU step about to run (visible even if the process dies)."""
+    print(f"[gpu-step] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def windows_for(head_dim, rope_base, k, theta, n_ctx):
+    """(GPU window, oracle widths) built independently on each side."""
+    import paper_2608_02947_amd as atf
+    th = None if theta is None else np.asarray(theta, dtype=np.float64)
+    return (atf.Window(head_dim, rope_base, k, th),
+            oracle.window_widths(head_dim, rope_base, k, th, n_ctx=n_ctx))
+
+
+def gpu_prefill(q, k, v, q_pos0, win, scale=0.0):
+    import paper_2608_02947_amd as atf
+    B, n_q, h_q, d = q.shape
+    o = torch.empty_like(q)
+    lse = torch.empty((B, h_q, n_q), dtype=torch.float32, device=q.device)
+    atf.atf_prefill(q, k, v, o, lse, q_pos0, win, scale)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def pack_kcache(k_bshd):
+    import paper_2608_02947_amd as atf
+    B, n_k, h_kv, d = k_bshd.shape
+    kp = torch.empty((B, h_kv, d // 16, n_k, 16), dtype=torch.bfloat16, device=k_bshd.device)
+    atf.atf_pack_kcache(k_bshd, kp)
+    return kp
+
+
+def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vt=None):
+    """q [B, h_q, d]; caches given in BSHD are packed / transposed first."""
+    import paper_2608_02947_amd as atf
+    B, h_q, d = q.shape
+    _, n_k, h_kv, _ = k_bshd.shape
+    if kp is None:
+        kp = pack_kcache(k_bshd)
+    if vt is None:
+        vt = v_bshd.permute(0, 2, 1, 3).contiguous()
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, n_k, d), dtype=torch.uint8,
+                     device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, h_q), dtype=torch.float32, device=q.device)
+    atf.atf_decode(q, kp, vt, o, lse, q_pos, win, ws, scale)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def compare(o_gpu, lse_gpu, o_ref, lse_ref, label=""):
+    """Element-wise comparison; returns (max_abs_o, mean_abs_o, max_abs_lse)."""
+    og = np.asarray(o_gpu, dtype=np.float64)
+    lg = np.asarray(lse_gpu, dtype=np.float64)
+    assert og.shape == o_ref.shape and lg.shape == lse_ref.shape, label
+    assert np.all(np.isfinite(og)) and np.all(np.isfinite(lg)), f"{label}: non-finite output"
+    eo = np.abs(og - o_ref)
+    el = np.abs(lg - lse_ref)
+    mx, mean, ml = float(eo.max()), float(eo.mean()), float(el.max())
+    assert mx <= O_MAX_ABS, f"{label}: O max-abs {mx}"
+    assert mean <= O_MEAN_ABS, f"{label}: O mean-abs {mean}"
+    assert ml <= LSE_MAX_ABS, f"{label}: LSE max-abs {ml}"
+    return mx, mean, ml
+
+
+def to_f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def sample_rows(batch, n_q, h_q, n_rows, seed, tile=128):
+    """Stratified (b, hq, i) sample: first and last rows, rows at tile edges, random."""
+    rng = np.random.default_rng(seed)
+    picks = set()
+    for i in list(range(min(8, n_q))) + list(range(max(0, n_q - 8), n_q)):
+        picks.add(i)
+    for t in rng.integers(0, max(1, n_q // tile), size=8):
+        for off in (-1, 0, 31, 32, tile - 1):
+            i = int(t) * tile + off
+            if 0 <= i < n_q:
+                picks.add(i)
+    while len(picks) < n_rows:
+        picks.add(int(rng.integers(0, n_q)))
+    rows = []
+    for i in sorted(picks)[:max(n_rows, len(picks))]:
+        rows.append((int(rng.integers(0, batch)), int(rng.integers(0, h_q)), i))
+    return np.array(rows, dtype=np.int64)
+
+
+def workload_window(wl: W.Workload, k=None):
+    th = W.workload_theta(wl)
+    return windows_for(wl.head_dim, wl.rope_base, wl.k if k is None else k,
+                       None if th is None else th.numpy(),
+                       n_ctx=max(wl.n_k, wl.q_pos0 + wl.n_q))

@@ -1,0 +1,181 @@
+"""Host-side checks of libatf.so that need no GPU.
+
+- the library loads and exports every function include/atf.h declares;
+- atf_window_table equals floor(k * lambda_r) from the oracle, bit-exact;
+- atf_count_terms (closed form per pair) equals the oracle's count and brute
+  force, bit-exact, for every workload shape and for random small cases;
+- every validation error is returned before anything is launched.
+No call here reaches a kernel launch.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads as W
+from conftest import ROOT
+
+atf = pytest.importorskip("paper_2608_02947_amd")
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "atf.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(atf_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = header_functions()
+    assert "atf_prefill" in names and "atf_decode" in names and "atf_count_terms" in names
+    lib = ctypes.CDLL(atf.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(atf.EXPORTED)
+
+
+def _oracle_thresholds(oracle_lib, wl_or_args):
+    d, base, k, theta = wl_or_args
+    w = oracle_lib.window_widths(d, base, k, theta)
+    return np.minimum(np.floor(w), 2 ** 31 - 1).astype(np.int64)
+
+
+@pytest.mark.parametrize("name", sorted(W.WORKLOADS))
+@pytest.mark.parametrize("kwin", [2.0, 0.5, 7.0, math.inf])
+def test_window_table_matches_oracle(oracle_lib, name, kwin):
+    wl = W.WORKLOADS[name]
+    th = W.workload_theta(wl)
+    th_np = th.numpy() if th is not None else None
+    win = atf.Window(wl.head_dim, wl.rope_base, kwin, th_np)
+    got = atf.atf_window_table(win).astype(np.int64)
+    exp = _oracle_thresholds(oracle_lib, (wl.head_dim, wl.rope_base, kwin, th_np))
+    assert np.array_equal(got, exp)
+    if math.isinf(kwin):
+        assert np.all(got == 2 ** 31 - 1)
+
+
+@pytest.mark.parametrize("name", sorted(W.WORKLOADS))
+def test_count_matches_oracle_for_workloads(oracle_lib, name):
+    wl = W.WORKLOADS[name]
+    th = W.workload_theta(wl)
+    th_np = th.numpy() if th is not None else None
+    win = atf.Window(wl.head_dim, wl.rope_base, wl.k, th_np)
+    got = atf.atf_count_terms(win, wl.n_q, wl.q_pos0, wl.n_k)
+    w = oracle_lib.window_widths(wl.head_dim, wl.rope_base, wl.k, th_np,
+                                 n_ctx=max(wl.n_k, wl.q_pos0 + wl.n_q))
+    assert got == oracle_lib.count_terms(w, wl.n_q, wl.q_pos0, wl.n_k)
+
+
+def test_count_known_values():
+    # values of the 1K Qwen workload and of the 1M chunk (per head), exact
+    wl = W.WORKLOADS["qwen05b_prefill_1k"]
+    assert atf.atf_count_terms(atf.Window(64, 1e6, 2.0), 1024, 0, 1024) == (12986186, 524800)
+    assert atf.atf_count_terms(atf.Window(128, 1e7, 2.0), 131072, 917504, 1048576) == \
+        (2928556179456, 128849084416)
+    assert wl.n_q == 1024
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_count_random_vs_oracle_and_brute(oracle_lib, seed):
+    rng = np.random.default_rng(seed)
+    d = int(rng.choice([2, 4, 8, 64, 128]))
+    base = float(rng.uniform(1.5, 1e6))
+    kwin = float(rng.choice([0.01, 0.2, 1.0, 2.0, 9.0, math.inf]))
+    n_q = int(rng.integers(0, 300))
+    q0 = int(rng.integers(0, 300))
+    n_k = int(rng.integers(0, 400))
+    theta = None
+    if rng.random() < 0.3:
+        theta = np.sort(rng.uniform(0.0, 2.0, d // 2))[::-1].copy()
+        theta[-1] = 0.0 if rng.random() < 0.5 else theta[-1]
+    win = atf.Window(d, base, kwin, theta)
+    got = atf.atf_count_terms(win, n_q, q0, n_k)
+    w = oracle_lib.window_widths(d, base, kwin, theta)
+    assert got == oracle_lib.count_terms(w, n_q, q0, n_k)
+    if d <= 8 and n_q * n_k <= 4000:
+        T = C = 0
+        for i in range(n_q):
+            p = q0 + i
+            for j in range(min(p, n_k - 1) + 1):
+                C += 1
+                T += int(np.sum(p - j <= np.floor(w)))
+        assert got == (T, C)
+
+
+def test_window_validation():
+    for bad in (atf.Window(63, 1e4, 2.0), atf.Window(0, 1e4, 2.0), atf.Window(8, 1.0, 2.0),
+                atf.Window(8, 1e4, 0.0), atf.Window(8, 1e4, float("nan")),
+                atf.Window(8, 1e4, 2.0, [1.0, -1.0, 0.5, 0.1]),
+                atf.Window(8, 1e4, 2.0, [1.0, float("nan"), 0.5, 0.1])):
+        with pytest.raises(atf.AtfError) as e:
+            atf.atf_window_table(bad)
+        assert e.value.code == atf.ATF_EINVAL
+        assert "window" in atf.atf_last_error()
+    # position-free pair and an infinite window clamp to 2^31 - 1
+    t = atf.atf_window_table(atf.Window(4, 10.0, 2.0, [1.0, 0.0]))
+    assert t[1] == 2 ** 31 - 1 and t[0] == math.floor(4 * math.pi)
+
+
+def _raw_prefill(lib, cw, **kw):
+    args = dict(q=16, k=16, v=16, o=16, lse=16, batch=1, n_q=4, n_k=4, q_pos0=0, h_q=2, h_kv=1)
+    args.update(kw)
+    return lib.atf_prefill(args["q"], args["k"], args["v"], args["o"], args["lse"], args["batch"],
+                           args["n_q"], args["n_k"], args["q_pos0"], args["h_q"], args["h_kv"],
+                           ctypes.byref(cw), 0.0, None)
+
+
+def test_prefill_validation_before_launch():
+    lib = atf.library()
+    good, _ = atf.Window(64, 1e4, 2.0).as_c()
+    cases = [
+        (atf.Window(96, 1e4, 2.0), {}, atf.ATF_EUNSUPPORTED),
+        (atf.Window(64, 1e4, 2.0), {"h_q": 3, "h_kv": 2}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"n_k": 0}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"batch": 0}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"q_pos0": -1}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"q_pos0": 2 ** 31 - 2}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"q": None}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"o": 18}, atf.ATF_EINVAL),        # misaligned
+        (atf.Window(64, 1e4, -1.0), {}, atf.ATF_EINVAL),
+    ]
+    for win, kw, code in cases:
+        cw, keep = win.as_c()
+        assert _raw_prefill(lib, cw, **kw) == code, (win, kw)
+        assert atf.atf_last_error()
+    # n_q == 0 is a no-op that touches nothing
+    assert _raw_prefill(lib, good, n_q=0, q=None, k=None, v=None, o=None, lse=None) == atf.ATF_OK
+
+
+def test_decode_validation_before_launch():
+    lib = atf.library()
+    cw, keep = atf.Window(128, 5e5, 2.0).as_c()
+    need = atf.atf_decode_workspace_bytes(8, 24, 8, 131072, 128)
+    assert need > 0
+    assert atf.atf_decode_workspace_bytes(8, 24, 7, 131072, 128) == 0
+    assert atf.atf_decode_workspace_bytes(8, 24, 8, 131072, 96) == 0
+
+    def call(ws=16, ws_bytes=None, d=128, **kw):
+        a = dict(batch=8, n_k=131072, q_pos=131072, h_q=24, h_kv=8)
+        a.update(kw)
+        w, kp = atf.Window(d, 5e5, 2.0).as_c()
+        return lib.atf_decode(16, 16, 16, 16, 16, a["batch"], a["n_k"], a["q_pos"], a["h_q"],
+                              a["h_kv"], ctypes.byref(w), 0.0, ws,
+                              need - 1 if ws_bytes is None else ws_bytes, None)
+    assert call() == atf.ATF_EWORKSPACE
+    assert call(ws=None, ws_bytes=need) == atf.ATF_EWORKSPACE
+    assert call(d=80) == atf.ATF_EUNSUPPORTED
+    assert call(q_pos=-1) == atf.ATF_EINVAL
+    assert call(h_kv=5) == atf.ATF_EINVAL
+    assert call(n_k=0) == atf.ATF_EINVAL
+
+
+def test_pack_validation_before_launch():
+    lib = atf.library()
+    assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap
+    assert lib.atf_pack_kcache(16, 1 << 20, 1, 4, 1, 48, None) == atf.ATF_EUNSUPPORTED
+    assert lib.atf_pack_kcache(None, 1 << 20, 1, 4, 1, 64, None) == atf.ATF_EINVAL
+    assert lib.atf_pack_kcache(16, 1 << 20, 0, 4, 1, 64, None) == atf.ATF_EINVAL
+    assert atf.atf_kcache_chunk_pairs(128) == 8 and atf.atf_kcache_chunk_pairs(64) == 8
+    assert atf.atf_kcache_chunk_pairs(32) == 0

@@ -1,0 +1,103 @@
+"""GPU parity of atf_pack_kcache and atf_decode against the oracle.
+
+The K cache is packed by the library; the pack itself is checked bit-exactly
+against a torch re-indexing of the same tensor.  Decode outputs are compared
+for every (batch, query head) row, at small shapes and at the full workload
+shapes the benchmark times.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import gpu_available
+import oracle
+import workloads as W
+from parity import compare, gpu_decode, note, pack_kcache, to_f64, windows_for, workload_window
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+DEV = "cuda"
+
+
+def _ref_pack(k_bshd):
+    """[B, n_k, h_kv, d] -> [B, h_kv, d/16, n_k, 16]: chunk c = dims [8c, 8c+8) ++ [d/2+8c, d/2+8c+8)."""
+    B, n_k, h_kv, d = k_bshd.shape
+    kk = k_bshd.permute(0, 2, 1, 3)
+    lo = kk[..., : d // 2].reshape(B, h_kv, n_k, d // 16, 8)
+    hi = kk[..., d // 2:].reshape(B, h_kv, n_k, d // 16, 8)
+    return torch.cat([lo, hi], dim=-1).permute(0, 1, 3, 2, 4).contiguous()
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 64), (2, 37, 3, 128), (3, 1000, 2, 64)])
+def test_pack_bit_exact(shape):
+    note(f"pack {shape}")
+    k = W.random_bf16(shape, seed=sum(shape)).to(DEV)
+    kp = pack_kcache(k)
+    torch.cuda.synchronize()
+    ref = _ref_pack(k)
+    assert torch.equal(kp.view(torch.int16), ref.view(torch.int16))
+
+
+def _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed, theta=None):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((B, 1, h_q, d), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    th = torch.as_tensor(theta, dtype=torch.float64) if theta is not None else W.rope_theta(d, base)
+    q = W.rotate_half(q, torch.tensor([q_pos]), th)
+    k = W.rotate_half(k, torch.arange(0, n_k), th)
+    return q, k, v
+
+
+def _decode_parity(q4, k, v, q_pos, win, widths, label):
+    """q4 [B, 1, h_q, d] (oracle layout); every (b, head) row compared."""
+    note(f"decode {label} q={tuple(q4.shape)} k={tuple(k.shape)} q_pos={q_pos}")
+    qd = q4[:, 0].contiguous().to(DEV)
+    o, lse = gpu_decode(qd, k.to(DEV), v.to(DEV), q_pos, win)
+    o_ref, lse_ref, _ = oracle.attend(q4.cpu(), k.cpu(), v.cpu(), q_pos, widths)
+    return compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], label)
+
+
+CASES = [
+    # B, n_k, q_pos, h_q, h_kv, d, base, k
+    (1, 1, 1, 1, 1, 128, 1e4, 2.0),
+    (2, 300, 300, 6, 2, 128, 5e5, 2.0),
+    (3, 1000, 1000, 7, 1, 64, 1e6, 2.0),
+    (1, 2049, 5000, 8, 1, 128, 1e4, 2.0),       # query beyond the cache end
+    (1, 3000, 1500, 4, 2, 64, 1e4, 2.0),        # keys past the query are not causal
+    (2, 777, 777, 12, 1, 128, 1e4, 2.0),        # G = 12 in sub-groups of 6
+    (1, 4096, 4096, 16, 2, 128, 100.0, 2.0),    # saturated windows
+    (1, 513, 513, 2, 2, 64, 1e4, 0.05),         # tiny k: empty score sums
+    (1, 999, 999, 3, 1, 128, 1e4, math.inf),    # window off
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_decode_small(case):
+    B, n_k, q_pos, h_q, h_kv, d, base, kwin = case
+    q, k, v = _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed=hash(case) % 10000)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=q_pos + 1)
+    _decode_parity(q, k, v, q_pos, win, widths, f"small{case}")
+
+
+def test_decode_nonmonotone_table():
+    d = 128
+    rng = np.random.default_rng(8)
+    theta = rng.uniform(0.001, 2.0, d // 2)
+    theta[[0, 9]] = 0.0
+    q, k, v = _decode_inputs(2, 2500, 2500, 6, 3, d, 0.0, seed=4, theta=theta)
+    win, widths = windows_for(d, 1e4, 2.0, theta, n_ctx=2501)
+    _decode_parity(q, k, v, 2500, win, widths, "nonmonotone")
+
+
+@pytest.mark.parametrize("name", ["llama3b_decode_32k", "llama3b_decode_128k", "qwen7b1m_decode"])
+def test_decode_workload_all_rows(name):
+    wl = W.WORKLOADS[name]
+    note(f"generate {name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl)
+    q4 = inp["q"]
+    _decode_parity(q4, inp["k"], inp["v"], wl.q_pos0, win, widths, name)

@@ -1,0 +1,140 @@
+"""GPU parity of atf_prefill against the fp64 oracle on the same seeded inputs.
+
+Small shapes: every output element.  Full workload shapes (the launch
+configuration bench.py times): a stratified sample of rows recomputed one by one
+by the oracle, plus properties that hold at any size (determinism, chunked
+prefill equal to single-shot).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from conftest import gpu_available
+import oracle
+import workloads as W
+from parity import (compare, gpu_prefill, note, sample_rows, to_f64, windows_for,
+                    workload_window)
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
+
+DEV = "cuda"
+
+
+def _small_inputs(B, n_q, n_k, q0, h_q, h_kv, d, base, seed, theta=None, scale_k=1.0):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((B, n_q, h_q, d), generator=g).to(torch.bfloat16)
+    k = (torch.randn((B, n_k, h_kv, d), generator=g) * scale_k).to(torch.bfloat16)
+    v = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    th = torch.as_tensor(theta, dtype=torch.float64) if theta is not None else W.rope_theta(d, base)
+    q = W.rotate_half(q, torch.arange(q0, q0 + n_q), th)
+    k = W.rotate_half(k, torch.arange(0, n_k), th)
+    return q, k, v
+
+
+def _full_parity(q, k, v, q0, win, widths, label, scale=None):
+    note(f"prefill {label} shape q={tuple(q.shape)} k={tuple(k.shape)} q0={q0}")
+    o, lse = gpu_prefill(q.to(DEV), k.to(DEV), v.to(DEV), q0, win,
+                         0.0 if scale is None else scale)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, q0, widths, scale=scale)
+    return compare(to_f64(o), to_f64(lse), o_ref, lse_ref, label)
+
+
+CASES = [
+    # B, n_q, n_k, q0, h_q, h_kv, d, base, k
+    (1, 128, 128, 0, 1, 1, 64, 1e4, 2.0),
+    (1, 300, 300, 0, 6, 2, 128, 5e5, 2.0),
+    (2, 45, 45, 0, 4, 4, 64, 1e6, 2.0),           # partial wave, MHA
+    (1, 77, 267, 190, 7, 1, 64, 1e6, 2.0),        # chunk at the end of a longer context
+    (1, 200, 150, 0, 8, 1, 128, 1e4, 2.0),        # keys end before the last query
+    (1, 1, 1, 0, 2, 1, 128, 1e4, 2.0),            # one row, one key
+    (1, 257, 257, 0, 3, 3, 128, 100.0, 2.0),      # saturated: every window ends early
+    (1, 190, 190, 0, 2, 1, 64, 1e4, 0.05),        # tiny k: empty score sums
+    (1, 256, 256, 0, 2, 1, 128, 1e4, math.inf),   # window off
+    (1, 333, 500, 167, 16, 2, 64, 1e4, 1.0),      # G = 8, ragged tail
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_small_all_rows(case):
+    B, n_q, n_k, q0, h_q, h_kv, d, base, kwin = case
+    q, k, v = _small_inputs(B, n_q, n_k, q0, h_q, h_kv, d, base, seed=hash(case) % 10000)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=max(n_k, q0 + n_q))
+    _full_parity(q, k, v, q0, win, widths, f"small{case}")
+
+
+def test_prefill_llama3_effective_table_all_rows():
+    wl = W.WORKLOADS["llama3b_prefill_32k"]
+    inp = W.make_inputs(wl, n_k=700, n_q=700, q_pos0=0)
+    win, widths = workload_window(wl)
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, "llama3 700")
+
+
+def test_prefill_nonmonotone_table_and_position_free_pairs():
+    """Per-chunk min/max classification does not assume a monotone table."""
+    d = 128
+    rng = np.random.default_rng(5)
+    theta = rng.uniform(0.005, 3.0, d // 2)
+    theta[[3, 17, 40]] = 0.0  # position-free pairs: never pruned
+    q, k, v = _small_inputs(1, 260, 260, 0, 4, 2, d, 0.0, seed=9, theta=theta)
+    win, widths = windows_for(d, 1e4, 3.0, theta, n_ctx=260)
+    _full_parity(q, k, v, 0, win, widths, "nonmonotone")
+
+
+def test_prefill_custom_scale():
+    q, k, v = _small_inputs(1, 160, 160, 0, 2, 1, 64, 1e4, seed=3)
+    win, widths = windows_for(64, 1e4, 2.0, None, n_ctx=160)
+    _full_parity(q, k, v, 0, win, widths, "scale0.3", scale=0.3)
+
+
+def test_prefill_qwen_1k_workload_all_rows():
+    """The 1K Qwen2.5-0.5B-shaped workload, every row of every head."""
+    wl = W.WORKLOADS["qwen05b_prefill_1k"]
+    inp = W.make_inputs(wl)
+    win, widths = workload_window(wl)
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, wl.name)
+    # k = inf equals the oracle of ordinary causal attention
+    win_inf, widths_inf = workload_window(wl, k=math.inf)
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win_inf, widths_inf, wl.name + " k=inf")
+
+
+@pytest.mark.parametrize("name", ["qwen05b_prefill_8k", "qwen05b_prefill_32k",
+                                  "llama3b_prefill_32k", "llama3b_prefill_128k",
+                                  "qwen7b1m_prefill_chunk"])
+def test_prefill_workload_sampled_rows(name):
+    """Full-size workload in the benchmark's launch configuration; sampled rows."""
+    wl = W.WORKLOADS[name]
+    note(f"generate {name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl)
+    note(f"prefill {name}")
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], wl.q_pos0, win)
+    rows = sample_rows(wl.batch, wl.n_q, wl.h_q, 48, seed=wl.seed)
+    q_c, k_c, v_c = inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu()
+    o_ref, lse_ref, terms = oracle.attend(q_c, k_c, v_c, wl.q_pos0, widths, rows=rows)
+    og = torch.stack([o[b, i, h] for b, h, i in rows]).float().cpu().numpy()
+    lg = torch.stack([lse[b, h, i] for b, h, i in rows]).cpu().numpy()
+    compare(og, lg, o_ref, lse_ref, name)
+    # determinism: a second run is bit-identical
+    note(f"prefill {name} rerun")
+    o2, lse2 = gpu_prefill(inp["q"], inp["k"], inp["v"], wl.q_pos0, win)
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+
+
+def test_prefill_chunked_equals_single_shot():
+    """Prefill in chunks of 1024 rows (q_pos0 offsets, keys up to the chunk end)
+    is bit-identical to one call over all rows."""
+    wl = W.WORKLOADS["qwen05b_prefill_8k"]
+    inp = W.make_inputs(wl, device=DEV, n_q=4096, n_k=4096, q_pos0=0)
+    win, _ = workload_window(wl)
+    note("prefill chunked vs single")
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win)
+    for s in range(0, 4096, 1024):
+        qc = inp["q"][:, s:s + 1024].contiguous()
+        kc = inp["k"][:, :s + 1024].contiguous()
+        vc = inp["v"][:, :s + 1024].contiguous()
+        oc, lc = gpu_prefill(qc, kc, vc, s, win)
+        assert torch.equal(oc, o[:, s:s + 1024])
+        assert torch.equal(lc, lse[:, :, s:s + 1024])
