@@ -1,0 +1,281 @@
+"""Benchmark of the windowed-attention hot path on one MI355X.
+
+Workload: the Qwen2.5-7B-1M-shaped case -- a prefill of one 131072-row chunk
+(positions 917504 .. 1048575) against a 1,048,576-key causal context, plus a
+single-token decode at position 1,048,576 over the same cache; 28 query heads,
+4 KV heads, head_dim 128, RoPE base 1e7, k = 2, seeded N(0,1) bf16 inputs.
+
+One step = one windowed prefill call + one windowed decode call (all of the
+hot path: window table, tile classification, K/V staging, QK and PV MFMAs,
+boundary and causal masking, online softmax, epilogue, decode split + merge).
+The same kernels at an infinite window (k = +inf) are timed too, for the
+speedup the window buys.  Inputs are resident in HBM before timing starts.
+
+Prints ONE JSON line.  Effective TFLOP/s counts only the work the method must
+do: per query head 4*T + 2*d*C flops, T = retained (cell, pair) terms, C =
+causal cells (softmax not counted).  Decode GB/s counts 4 bytes per retained
+(token, pair) of K, all V rows (2*d bytes each), q and o.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+import torch  # noqa: E402
+
+METRIC = ("prefill ms + effective TFLOP/s vs full-window at 32K-128K; decode GB/s at 1M")
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--decode-iters", type=int, default=50)
+    ap.add_argument("--no-full-window", action="store_true",
+                    help="skip the k=inf reference timing")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=192,
+                    help="(row, head) pairs of the prefill chunk the oracle recomputes")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (for scaling rocprof byte counters)")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "launches": 3}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see DESIGN.md, 'How the path would shard').", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import paper_2608_02947_amd as atf
+    import workloads as W
+
+    dev = torch.device("cuda:0")
+    pf = W.WORKLOADS["qwen7b1m_prefill_chunk"]
+    dc = W.WORKLOADS["qwen7b1m_decode"]
+    d, B = pf.head_dim, pf.batch
+
+    # ---- inputs, resident in HBM
+    inp = W.make_inputs(pf, device=dev)
+    q, k, v = inp["q"], inp["k"], inp["v"]
+    gq = torch.Generator(device=dev)
+    gq.manual_seed(dc.seed + 17)
+    qd = torch.randn((dc.batch, 1, dc.h_q, d), generator=gq, device=dev).to(torch.bfloat16)
+    qd = W.rotate_half(qd, torch.tensor([dc.q_pos0]), W.rotation_theta(dc))[:, 0].contiguous()
+    kp = torch.empty((B, pf.h_kv, d // 16, pf.n_k, 16), dtype=torch.bfloat16, device=dev)
+    atf.atf_pack_kcache(k, kp)
+    vt = v.permute(0, 2, 1, 3).contiguous()
+    o = torch.empty_like(q)
+    lse = torch.empty((B, pf.h_q, pf.n_q), dtype=torch.float32, device=dev)
+    od = torch.empty_like(qd)
+    lsed = torch.empty((dc.batch, dc.h_q), dtype=torch.float32, device=dev)
+    ws = torch.empty(atf.atf_decode_workspace_bytes(dc.batch, dc.h_q, dc.h_kv, dc.n_k, d),
+                     dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+
+    win = atf.Window(d, pf.rope_base, pf.k)
+    win_off = atf.Window(d, pf.rope_base, math.inf)
+
+    # ---- algorithmic work
+    T, C = atf.atf_count_terms(win, pf.n_q, pf.q_pos0, pf.n_k)
+    T_full, _ = atf.atf_count_terms(win_off, pf.n_q, pf.q_pos0, pf.n_k)
+    flops_prefill = B * pf.h_q * (4 * T + 2 * d * C)
+    flops_prefill_full = B * pf.h_q * (4 * T_full + 2 * d * C)
+    Td, Cd = atf.atf_count_terms(win, 1, dc.q_pos0, dc.n_k)
+    Td_full, _ = atf.atf_count_terms(win_off, 1, dc.q_pos0, dc.n_k)
+    flops_decode = dc.batch * dc.h_q * (4 * Td + 2 * d * Cd)
+    bytes_decode = dc.batch * dc.h_kv * (4 * Td + 2 * d * Cd) + dc.batch * dc.h_q * d * 4
+    bytes_decode_full = dc.batch * dc.h_kv * (4 * Td_full + 2 * d * Cd) + dc.batch * dc.h_q * d * 4
+
+    stream = torch.cuda.current_stream()
+
+    def prefill(w):
+        atf.atf_prefill(q, k, v, o, lse, pf.q_pos0, w, stream=stream)
+
+    def decode(w):
+        atf.atf_decode(qd, kp, vt, od, lsed, dc.q_pos0, w, ws, stream=stream)
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    # ---- warmup
+    for _ in range(args.warmup):
+        prefill(win)
+        decode(win)
+    torch.cuda.synchronize()
+
+    # ---- timed steps (events on the stream the kernels run on)
+    t0, t1 = ev(), ev()
+    pre_ev, dec_ev = [], []
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for _ in range(args.steps):
+        a, b = ev(), ev()
+        a.record(stream)
+        prefill(win)
+        b.record(stream)
+        c, e = ev(), ev()
+        c.record(stream)
+        decode(win)
+        e.record(stream)
+        pre_ev.append((a, b))
+        dec_ev.append((c, e))
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t0.elapsed_time(t1) / args.steps
+    pre_ms = [a.elapsed_time(b) for a, b in pre_ev]
+    # decode alone: many back-to-back calls (its 1.45 GB of reads exceed the 256 MB MALL)
+    dec_ms = []
+    for _ in range(args.decode_iters):
+        a, b = ev(), ev()
+        a.record(stream)
+        decode(win)
+        b.record(stream)
+        dec_ms.append((a, b))
+    torch.cuda.synchronize()
+    dec_ms = [a.elapsed_time(b) for a, b in dec_ms]
+
+    full = None
+    if not args.no_full_window:
+        prefill(win_off)
+        torch.cuda.synchronize()
+        pf_full = []
+        for _ in range(args.steps):
+            a, b = ev(), ev()
+            a.record(stream)
+            prefill(win_off)
+            b.record(stream)
+            pf_full.append((a, b))
+        dfull = []
+        for _ in range(args.decode_iters):
+            a, b = ev(), ev()
+            a.record(stream)
+            decode(win_off)
+            b.record(stream)
+            dfull.append((a, b))
+        torch.cuda.synchronize()
+        full = {"prefill_ms": statistics.median(a.elapsed_time(b) for a, b in pf_full),
+                "decode_ms": statistics.median(a.elapsed_time(b) for a, b in dfull)}
+
+    pre_med = statistics.median(pre_ms)
+    pre_mean = statistics.fmean(pre_ms)
+    dec_med = statistics.median(dec_ms)
+    step_flops = flops_prefill + flops_decode
+    value = step_flops / (ms_step * 1e-3) / 1e12
+    achieved = flops_prefill / (pre_mean * 1e-3) / 1e12
+
+    prefill_info = {
+        "ms_median": round(pre_med, 3), "ms_min": round(min(pre_ms), 3),
+        "ms_max": round(max(pre_ms), 3),
+        "effective_tflops": round(flops_prefill / (pre_med * 1e-3) / 1e12, 1),
+        "frac_bf16_peak": round(flops_prefill / (pre_med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "retained_terms_per_head": T, "causal_cells_per_head": C,
+        "qk_pruned": round(1 - T / (C * d / 2), 4),
+        "ceiling_2_over_1_plus_s": round(flops_prefill_full / flops_prefill, 4),
+    }
+    decode_info = {
+        "ms_median": round(dec_med, 4), "ms_min": round(min(dec_ms), 4),
+        "GBps": round(bytes_decode / (dec_med * 1e-3) / 1e9, 1),
+        "frac_hbm_peak": round(bytes_decode / (dec_med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": bytes_decode, "retained_token_pairs_per_kv_head": Td,
+        "byte_ceiling_full_over_window": round(bytes_decode_full / bytes_decode, 4),
+    }
+    if full is not None:
+        prefill_info["full_window_ms"] = round(full["prefill_ms"], 3)
+        prefill_info["speedup_vs_full_window"] = round(full["prefill_ms"] / pre_med, 4)
+        prefill_info["full_window_dense_tflops"] = round(
+            flops_prefill_full / (full["prefill_ms"] * 1e-3) / 1e12, 1)
+        decode_info["full_window_ms"] = round(full["decode_ms"], 4)
+        decode_info["speedup_vs_full_window"] = round(full["decode_ms"] / dec_med, 4)
+        decode_info["full_window_GBps"] = round(
+            bytes_decode_full / (full["decode_ms"] * 1e-3) / 1e9, 1)
+
+    roofline = {"kernel": "prefill_kernel<128>", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "flops_per_launch": flops_prefill, "avg_launch_ms": round(pre_mean, 3)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(inp, pf, args.cpu_rows)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1), RoPE-rotated; stands in for LongBench-v2 documents)",
+        "config": {"workload": "Qwen2.5-7B-1M-shaped: prefill of a 131072-row chunk at "
+                               "positions 917504..1048575 over 1048576 keys + decode at 1048576",
+                   "batch": B, "n_q": pf.n_q, "q_pos0": pf.q_pos0, "n_k": pf.n_k,
+                   "h_q": pf.h_q, "h_kv": pf.h_kv, "head_dim": d, "rope_base": pf.rope_base,
+                   "k": pf.k, "parallelism": "single GPU"},
+        "prefill": prefill_info, "decode": decode_info, "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.machine()
+
+
+def cpu_baseline(inp, pf, n_rows):
+    """The fp64 oracle on a bounded sample of the same prefill chunk, on the host cores."""
+    import oracle
+    avail = len(os.sched_getaffinity(0))
+    cores = min(avail, int(os.environ.get("OMP_NUM_THREADS") or avail))
+    rng = np.random.default_rng(pf.seed)
+    rows = np.stack([np.zeros(n_rows, dtype=np.int64),
+                     rng.integers(0, pf.h_q, n_rows),
+                     rng.integers(0, pf.n_q, n_rows)], axis=1).astype(np.int64)
+    qc, kc, vc = inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu()
+    widths = oracle.window_widths(pf.head_dim, pf.rope_base, pf.k, n_ctx=pf.n_k)
+    t = time.perf_counter()
+    _, _, terms = oracle.attend(qc, kc, vc, pf.q_pos0, widths, rows=rows, threads=cores)
+    dt = time.perf_counter() - t
+    causal = np.minimum(pf.q_pos0 + rows[:, 2], pf.n_k - 1) + 1
+    flops = float(np.sum(4.0 * terms.astype(np.float64) + 2.0 * pf.head_dim * causal))
+    return {"value": float(f"{flops / dt / 1e12:.6g}"), "unit": "TFLOP/s", "cores": cores,
+            "kind": "oracle", "seconds": round(dt, 2), "cpu": cpu_model(),
+            "sample": f"{n_rows} random (query row, head) pairs of the 131072-row chunk, "
+                      f"each over its ~1M causal keys, fp64, OpenMP over rows"}
+
+
+if __name__ == "__main__":
+    main()
