@@ -52,7 +52,53 @@ def parse():
                     help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for scaling rocprof byte counters)")
+    ap.add_argument("--profile-workload", default=None,
+                    help="profiling driver: run only this workload's kernel (a name from "
+                         "workloads.WORKLOADS) --profile-iters times and print its timings")
+    ap.add_argument("--profile-iters", type=int, default=3)
+    ap.add_argument("--profile-kinf", action="store_true", help="profiling driver at k = +inf")
     return ap.parse_args()
+
+
+def profile_driver(name, iters, kinf):
+    """Run one workload's prefill or decode `iters` times (for rocprofv3 runs)."""
+    import paper_2608_02947_amd as atf
+    import workloads as W
+    wl = W.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    inp = W.make_inputs(wl, device=dev)
+    th = W.workload_theta(wl)
+    win = atf.Window(wl.head_dim, wl.rope_base, math.inf if kinf else wl.k,
+                     None if th is None else th.numpy())
+    stream = torch.cuda.current_stream()
+    d = wl.head_dim
+    if wl.kind == "prefill":
+        o = torch.empty_like(inp["q"])
+        lse = torch.empty((wl.batch, wl.h_q, wl.n_q), dtype=torch.float32, device=dev)
+        run = lambda: atf.atf_prefill(inp["q"], inp["k"], inp["v"], o, lse, wl.q_pos0, win,
+                                      stream=stream)
+    else:
+        kp = torch.empty((wl.batch, wl.h_kv, d // 16, wl.n_k, 16), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_kcache(inp["k"], kp)
+        vt = inp["v"].permute(0, 2, 1, 3).contiguous()
+        qd = inp["q"][:, 0].contiguous()
+        od = torch.empty_like(qd)
+        lsed = torch.empty((wl.batch, wl.h_q), dtype=torch.float32, device=dev)
+        ws = torch.empty(atf.atf_decode_workspace_bytes(wl.batch, wl.h_q, wl.h_kv, wl.n_k, d),
+                         dtype=torch.uint8, device=dev)
+        run = lambda: atf.atf_decode(qd, kp, vt, od, lsed, wl.q_pos0, win, ws, stream=stream)
+    ms = []
+    for _ in range(iters):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        run()
+        b.record(stream)
+        ms.append((a, b))
+    torch.cuda.synchronize()
+    print(json.dumps({"profile_workload": name, "k": "inf" if kinf else wl.k,
+                      "ms": [round(a.elapsed_time(b), 4) for a, b in ms]}))
 
 
 def copy_calibration():
@@ -74,6 +120,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.profile_workload:
+        profile_driver(args.profile_workload, args.profile_iters, args.profile_kinf)
         return
 
     import paper_2608_02947_amd as atf

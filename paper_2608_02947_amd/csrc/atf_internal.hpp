@@ -28,6 +28,7 @@ struct PrefillParams {
     uint16_t* o;         // [B][n_q][h_q][d]
     float* lse;          // [B][h_q][n_q]
     int32_t batch, n_q, n_k, q_pos0, h_q, h_kv, group;
+    int32_t pos_per_tile;  // query positions per workgroup (rows = positions x group)
     int32_t n_qtiles;
     float scale_log2;    // softmax scale * log2(e)
     WindowTable win;

@@ -124,17 +124,21 @@ def test_prefill_workload_sampled_rows(name):
 
 
 def test_prefill_chunked_equals_single_shot():
-    """Prefill in chunks of 1024 rows (q_pos0 offsets, keys up to the chunk end)
-    is bit-identical to one call over all rows."""
+    """Prefill in chunks (q_pos0 offsets, keys up to the chunk end) is bit-identical
+    to one call over all rows when every chunk boundary is a multiple of the
+    workgroup's position tile, floor(256 / G) positions (36 for G = 7)."""
     wl = W.WORKLOADS["qwen05b_prefill_8k"]
-    inp = W.make_inputs(wl, device=DEV, n_q=4096, n_k=4096, q_pos0=0)
+    tile = 256 // wl.group
+    chunk = tile * 28
+    n = 4 * chunk
+    inp = W.make_inputs(wl, device=DEV, n_q=n, n_k=n, q_pos0=0)
     win, _ = workload_window(wl)
     note("prefill chunked vs single")
     o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win)
-    for s in range(0, 4096, 1024):
-        qc = inp["q"][:, s:s + 1024].contiguous()
-        kc = inp["k"][:, :s + 1024].contiguous()
-        vc = inp["v"][:, :s + 1024].contiguous()
+    for s in range(0, n, chunk):
+        qc = inp["q"][:, s:s + chunk].contiguous()
+        kc = inp["k"][:, :s + chunk].contiguous()
+        vc = inp["v"][:, :s + chunk].contiguous()
         oc, lc = gpu_prefill(qc, kc, vc, s, win)
-        assert torch.equal(oc, o[:, s:s + 1024])
-        assert torch.equal(lc, lse[:, :, s:s + 1024])
+        assert torch.equal(oc, o[:, s:s + chunk])
+        assert torch.equal(lc, lse[:, :, s:s + chunk])
