@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--no-full-window", action="store_true",
                     help="skip the k=inf reference timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=192,
+    ap.add_argument("--cpu-rows", type=int, default=512,
                     help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for scaling rocprof byte counters)")
@@ -268,7 +268,7 @@ def main():
         decode_info["full_window_GBps"] = round(
             bytes_decode_full / (full["decode_ms"] * 1e-3) / 1e9, 1)
 
-    roofline = {"kernel": "prefill_kernel<128>", "bound": "mfma",
+    roofline = {"kernel": "prefill_kernel<128, true>", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
                 "flops_per_launch": flops_prefill, "avg_launch_ms": round(pre_mean, 3)}

@@ -128,7 +128,7 @@ __device__ __forceinline__ void load_to_lds(const uint16_t* g, uint16_t* lds_wav
 }
 
 template <int D, bool kWin>
-__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParams p) {
+__global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(const PrefillParams p) {
     using C = Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::kKTile];
     __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::kVTile];
@@ -189,11 +189,13 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
         }
     }
 
-    // chunks that some cell of the workgroup tile at keys [j0, j0 + 64) keeps
+    // chunks that some cell of the workgroup tile at keys [j0, j0 + 64) keeps, plus
+    // the last chunk: the first QK MFMA of a block always multiplies it (with the
+    // query dims of unkept pairs zeroed), so it must hold finite data
     auto tile_need = [&](int j0) -> uint32_t {
         if (!kWin) return (1u << C::kChunks) - 1u;
         const int zlo = max(0, pos_first - (j0 + kBN - 1));
-        uint32_t need = 0;
+        uint32_t need = 1u << (C::kChunks - 1);
 #pragma unroll
         for (int c = 0; c < C::kChunks; ++c)
             if (p.win.chunk_max[c] >= zlo) need |= 1u << c;
@@ -270,13 +272,19 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
         if (wave_active && wp_max >= j0) {
             const uint16_t* Kb = Ks[buf];
             const uint16_t* Vb = Vs[buf];
+            // ---- QK for both 32-key blocks of the tile (the matrix phase; the window's
+            // branches live here).  Block 0 always has a causal key; block 1 may not.
+            const bool live1 = wp_max >= j0 + 32 && j0 + 32 < p.n_k;
+            f32x16_t sacc[2];
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
+                if (kb == 1 && !live1) {
+                    sacc[1] = zero16();  // masked below
+                    continue;
+                }
                 const int jb = j0 + 32 * kb;
                 const int zhi = wp_max - jb;
-                if (zhi < 0 || jb >= p.n_k) continue;  // block entirely in the future or past n_k
-                const int zlo_raw = wp_min - (jb + 31);
-                const int zlo = max(0, zlo_raw);
+                const int zlo = max(0, wp_min - (jb + 31));
                 // every K fragment of the block is read before any branch so that the
                 // reads overlap; a chunk the block does not keep is never multiplied
                 const uint16_t* krow = Kb + k_off[kb];
@@ -284,11 +292,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
 #pragma unroll
                 for (int c = 0; c < C::kChunks; ++c)
                     kf[c] = *reinterpret_cast<const u32x4_t*>(krow + 8 * c);
-                f32x16_t sacc;
+                f32x16_t acc;
                 if (!kWin) {
-                    sacc = mfma(kf[C::kChunks - 1], qf[C::kChunks - 1], zero16());
+                    acc = mfma(kf[C::kChunks - 1], qf[C::kChunks - 1], zero16());
 #pragma unroll
-                    for (int c = C::kChunks - 2; c >= 0; --c) sacc = mfma(kf[c], qf[c], sacc);
+                    for (int c = C::kChunks - 2; c >= 0; --c) acc = mfma(kf[c], qf[c], acc);
                 } else {
                     // all pairs classified at once: lane r holds W_r; bit r of `full` = pair r
                     // kept in every cell of the block, of `keep` = kept in some cell
@@ -301,11 +309,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
                     for (int c = C::kChunks - 1; c >= 0; --c) {
                         const uint32_t fc = uint32_t(full >> (8 * c)) & 0xFFu;
                         if (c == C::kChunks - 1) {
-                            sacc = mfma(kf[c], keep_pairs(qf[c], fc), zero16());
+                            acc = mfma(kf[c], keep_pairs(qf[c], fc), zero16());
                         } else if (fc) {
                             u32x4_t qb = qf[c];
                             if (fc != 0xFFu) qb = keep_pairs(qb, fc);
-                            sacc = mfma(kf[c], qb, sacc);
+                            acc = mfma(kf[c], qb, acc);
                         }
                     }
                     // pairs whose window ends inside the block: one MFMA each, added where
@@ -327,45 +335,57 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
                             const int off = 8 * (v / 4) + (v % 4);
-                            sacc[v] += off >= thr ? t[v] : 0.f;
+                            acc[v] += off >= thr ? t[v] : 0.f;
                         }
                     }
                 }
-                // causal mask and key bound, only for blocks that reach the diagonal or n_k
-                if (zlo_raw < 0 || jb + 32 > p.n_k) {
+                sacc[kb] = acc;
+            }
+            // ---- causal mask and key bound, only in tiles that reach the diagonal or n_k
+            if (wp_min - (j0 + kBN - 1) < 0 || j0 + kBN > p.n_k) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    const int jb = j0 + 32 * kb;
                     const int kbound = p.n_k - jb - 4 * hh;
                     const int zbase = my_pos - jb - 4 * hh;
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         const int off = 8 * (v / 4) + (v % 4);
-                        if (off > zbase || off >= kbound) sacc[v] = -INFINITY;
+                        if (off > zbase || off >= kbound) sacc[kb][v] = -INFINITY;
                     }
                 }
-
-                // online softmax (lane = query row; the two lane halves hold disjoint keys)
-                float mx = -INFINITY;
+            }
+            // ---- online softmax over the tile (lane = query row; the two lane halves
+            // hold disjoint keys).  One rescale check per tile; below it the softmax and
+            // the PV products of both blocks are branch-free, so the PV matrix work of
+            // block 0 overlaps the exponentials of block 1.
+            float mx = -INFINITY;
 #pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[v]);
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const float cand = mx * sc;
-                if (__any(cand > m_run + kRescale)) {
-                    const float m_new = fmaxf(m_run, cand);
-                    const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
-                    m_run = m_new;
-                    l_run *= alpha;
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                    for (int i = 0; i < D / 32; ++i)
+                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float cand = mx * sc;
+            if (__any(cand > m_run + kRescale)) {
+                const float m_new = fmaxf(m_run, cand);
+                const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
+                m_run = m_new;
+                l_run *= alpha;
 #pragma unroll
-                        for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
-                }
-                const float m_use = m_run == -INFINITY ? 0.f : m_run;
+                for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
+            }
+            const float m_use = m_run == -INFINITY ? 0.f : m_run;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
                 u32x4_t pb[2];
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
                     for (int t = 0; t < 4; ++t) {
-                        const float a = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t], sc, -m_use));
-                        const float c2 = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t + 1], sc, -m_use));
+                        const float a = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t], sc, -m_use));
+                        const float c2 = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t + 1], sc, -m_use));
                         l_run += a;
                         l_run += c2;
                         bf16x2_t two;
@@ -374,7 +394,6 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
                         pb[ks][t] = __builtin_bit_cast(uint32_t, two);
                     }
                 }
-
                 // PV: V^T fragments by transposed LDS reads.  Lane group of 16: key rows
                 // 4 * hh + (l % 16) / 4 (8 rows further for elements 4..7), dims
                 // 16 * ((l / 16) % 2) + 4 * (l % 4) of each 32-dim block.
