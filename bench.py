@@ -81,13 +81,15 @@ def profile_driver(name, iters, kinf):
         kp = torch.empty((wl.batch, wl.h_kv, d // 16, wl.n_k, 16), dtype=torch.bfloat16,
                          device=dev)
         atf.atf_pack_kcache(inp["k"], kp)
-        vt = inp["v"].permute(0, 2, 1, 3).contiguous()
+        vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_vcache(inp["v"], vp)
         qd = inp["q"][:, 0].contiguous()
         od = torch.empty_like(qd)
         lsed = torch.empty((wl.batch, wl.h_q), dtype=torch.float32, device=dev)
         ws = torch.empty(atf.atf_decode_workspace_bytes(wl.batch, wl.h_q, wl.h_kv, wl.n_k, d),
                          dtype=torch.uint8, device=dev)
-        run = lambda: atf.atf_decode(qd, kp, vt, od, lsed, wl.q_pos0, win, ws, stream=stream)
+        run = lambda: atf.atf_decode(qd, kp, vp, od, lsed, wl.q_pos0, win, ws, stream=stream)
     ms = []
     for _ in range(iters):
         a = torch.cuda.Event(enable_timing=True)
@@ -142,7 +144,8 @@ def main():
     qd = W.rotate_half(qd, torch.tensor([dc.q_pos0]), W.rotation_theta(dc))[:, 0].contiguous()
     kp = torch.empty((B, pf.h_kv, d // 16, pf.n_k, 16), dtype=torch.bfloat16, device=dev)
     atf.atf_pack_kcache(k, kp)
-    vt = v.permute(0, 2, 1, 3).contiguous()
+    vp = torch.empty(atf.vcache_shape(B, pf.n_k, pf.h_kv, d), dtype=torch.bfloat16, device=dev)
+    atf.atf_pack_vcache(v, vp)
     o = torch.empty_like(q)
     lse = torch.empty((B, pf.h_q, pf.n_q), dtype=torch.float32, device=dev)
     od = torch.empty_like(qd)
@@ -171,7 +174,7 @@ def main():
         atf.atf_prefill(q, k, v, o, lse, pf.q_pos0, w, stream=stream)
 
     def decode(w):
-        atf.atf_decode(qd, kp, vt, od, lsed, dc.q_pos0, w, ws, stream=stream)
+        atf.atf_decode(qd, kp, vp, od, lsed, dc.q_pos0, w, ws, stream=stream)
 
     def ev():
         return torch.cuda.Event(enable_timing=True)

@@ -113,6 +113,22 @@ int32_t atf_kcache_chunk_pairs(int32_t head_dim);
 int atf_pack_kcache(const void *k_bshd, void *k_pcm, int32_t batch, int64_t n_k,
                     int32_t h_kv, int32_t head_dim, void *hip_stream);
 
+/* Bytes of the packed decode V cache for these sizes:
+ * batch * h_kv * ceil(n_k / 16) * 16 * head_dim * 2.  Returns 0 for invalid sizes. */
+size_t atf_vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_dim);
+
+/* Repack a value cache from [batch][n_k][h_kv][d] (bf16) to the decode layout
+ * [batch][h_kv][ceil(n_k/16)][d][16]: blocks of 16 tokens stored d-major, so that
+ * one 16-byte load gives the 8 tokens one lane of the PV matrix instruction
+ * multiplies.  Within a block, slot 8*h + e of a d-row holds token
+ * 8*(e/4) + 4*h + e%4 (h in {0,1}, e in 0..7), the token order of the score
+ * fragments; tokens past n_k are zero.  Pure data movement (bit-exact).
+ *   v_bshd  device, read;  v_pack  device, atf_vcache_bytes(...) bytes, written.
+ * Both 16-byte aligned and not overlapping.
+ * Errors: ATF_EINVAL, ATF_EUNSUPPORTED (d), ATF_EHIP. */
+int atf_pack_vcache(const void *v_bshd, void *v_pack, int32_t batch, int64_t n_k,
+                    int32_t h_kv, int32_t head_dim, void *hip_stream);
+
 /* Bytes of device workspace that atf_decode needs for these sizes (split-KV
  * partial softmax states).  Returns 0 for invalid sizes. */
 size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int64_t n_k,
@@ -126,14 +142,16 @@ size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int6
  * is read; pairs whose window ends inside that suffix are masked per token.
  *   q        bf16 [batch][h_q][d]                        (device, read)
  *   k_cache  bf16 pair-chunk-major, see atf_pack_kcache   (device, read)
- *   v_cache  bf16 [batch][h_kv][n_k][d]                   (device, read)
+ *   v_cache  bf16 packed 16-token blocks, see atf_pack_vcache (device, read)
  *   o        bf16 [batch][h_q][d]                         (device, written)
  *   lse      fp32 [batch][h_q]                            (device, written)
  *   workspace: device, >= atf_decode_workspace_bytes(batch, h_q, h_kv, n_k, d)
  *              bytes, 16-byte aligned, caller-owned; contents are scratch.
  * Errors: ATF_EINVAL (pointers, sizes, q_pos < 0, q_pos > 2^31 - 2, bad window or
- * scale), ATF_EUNSUPPORTED (d not 64/128, or h_q/h_kv > 8 and not a multiple
- * of a divisor <= 8), ATF_EWORKSPACE, ATF_EHIP. */
+ * scale), ATF_EUNSUPPORTED (d not 64/128), ATF_EWORKSPACE, ATF_EHIP.
+ * The query heads of one KV head are the columns of the matrix instructions
+ * (up to 32 per workgroup; larger groups are split over workgroups by their
+ * largest divisor <= 32).  Deterministic: equal inputs give equal bits. */
 int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o, float *lse,
                int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
                const atf_window *w, float softmax_scale,

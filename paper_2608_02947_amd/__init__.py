@@ -1,8 +1,8 @@
 """Python binding of libatf.so: per-RoPE-wavelength windowed causal attention on MI355X.
 
 Argument marshalling only.  Every step of prefill and decode runs in the HIP
-kernels of ``libatf.so`` (built from ``csrc/`` by ``python -m
-paper_2608_02947_amd.build``); torch supplies device memory and the current HIP
+kernels of ``libatf.so`` (built from ``csrc/`` by ``python
+paper_2608_02947_amd/build.py``); torch supplies device memory and the current HIP
 stream.  Importing this package loads the library and raises if it is missing:
 there is no fallback path.
 
@@ -11,6 +11,7 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_window_table`, :func:`atf_count_terms` -- host only.
 - :func:`atf_prefill` -- windowed prefill (chunked via ``q_pos0``).
 - :func:`atf_pack_kcache`, :func:`atf_kcache_chunk_pairs` -- decode K-cache layout.
+- :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- decode V-cache layout.
 - :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
 """
 from __future__ import annotations
@@ -47,7 +48,7 @@ class _CWindow(ctypes.Structure):
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(
-            f"{LIB_PATH} is missing: build it with `python -m paper_2608_02947_amd.build`")
+            f"{LIB_PATH} is missing: build it with `python paper_2608_02947_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
     i32, i64, f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float
@@ -58,6 +59,8 @@ def _load():
         "atf_prefill": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, W, f32, P]),
         "atf_kcache_chunk_pairs": (ctypes.c_int32, [i32]),
         "atf_pack_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
+        "atf_vcache_bytes": (ctypes.c_size_t, [i32, i64, i32, i32]),
+        "atf_pack_vcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
         "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
         "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, W, f32, P,
                                       ctypes.c_size_t, P]),
@@ -72,7 +75,8 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("atf_window_table", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
-            "atf_pack_kcache", "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
+            "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache",
+            "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
 
 
 def library():
@@ -186,19 +190,43 @@ def atf_pack_kcache(k_bshd, k_pcm, stream=None):
                                 _stream_ptr(stream)))
 
 
-def atf_decode(q, k_pcm, v_cache, o, lse, q_pos: int, window: Window, workspace,
+def atf_vcache_bytes(batch: int, n_k: int, h_kv: int, head_dim: int) -> int:
+    return int(_lib.atf_vcache_bytes(batch, n_k, h_kv, head_dim))
+
+
+def vcache_shape(batch: int, n_k: int, h_kv: int, head_dim: int):
+    """Shape of the packed V cache: [B, h_kv, ceil(n_k/16), d, 16]."""
+    return (batch, h_kv, (n_k + 15) // 16, head_dim, 16)
+
+
+def atf_pack_vcache(v_bshd, v_pack, stream=None):
+    """v_bshd [B, n_k, h_kv, d] -> v_pack [B, h_kv, ceil(n_k/16), d, 16] (bf16)."""
+    torch = _torch()
+    B, n_k, h_kv, d = v_bshd.shape
+    if tuple(v_pack.shape) != vcache_shape(B, n_k, h_kv, d):
+        raise ValueError("atf_pack_vcache: destination shape mismatch")
+    _check(_lib.atf_pack_vcache(_dev_ptr(v_bshd, torch.bfloat16, "v_bshd"),
+                                _dev_ptr(v_pack, torch.bfloat16, "v_pack"), B, n_k, h_kv, d,
+                                _stream_ptr(stream)))
+
+
+def atf_decode(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window, workspace,
                softmax_scale: float = 0.0, stream=None):
-    """q [B, h_q, d]; k_pcm pair-chunk-major; v_cache [B, h_kv, n_k, d]; o [B, h_q, d];
-    lse [B, h_q]; workspace: uint8 device tensor of atf_decode_workspace_bytes()."""
+    """q [B, h_q, d]; k_pcm [B, h_kv, d/16, n_k, 16]; v_pack [B, h_kv, ceil(n_k/16), d, 16];
+    o [B, h_q, d]; lse [B, h_q]; workspace: uint8 device tensor of
+    atf_decode_workspace_bytes()."""
     torch = _torch()
     B, h_q, d = q.shape
-    _, h_kv, n_k, _ = v_cache.shape
+    if k_pcm.dim() != 5:
+        raise ValueError("atf_decode: k_pcm must be [B, h_kv, d/16, n_k, 16]")
+    _, h_kv, _, n_k, _ = k_pcm.shape
     if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
-            k_pcm.numel() != v_cache.numel():
+            tuple(k_pcm.shape) != (B, h_kv, d // 16, n_k, 16) or \
+            tuple(v_pack.shape) != vcache_shape(B, n_k, h_kv, d):
         raise ValueError("atf_decode: inconsistent shapes")
     cw, keep = window.as_c()
     rc = _lib.atf_decode(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pcm, torch.bfloat16, "k"),
-                         _dev_ptr(v_cache, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+                         _dev_ptr(v_pack, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
                          _dev_ptr(lse, torch.float32, "lse"), B, n_k, q_pos, h_q, h_kv,
                          ctypes.byref(cw), float(softmax_scale),
                          _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),

@@ -1,6 +1,6 @@
 """Build libatf.so (gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2608_02947_amd.build
+Usage: python paper_2608_02947_amd/build.py
 Every HIP source is compiled for gfx950 only, with packed-FP32 instruction
 selection disabled, then linked into paper_2608_02947_amd/libatf.so.
 """

@@ -134,6 +134,7 @@ int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k) {
     int64_t s = (target_groups + int64_t(batch) * h_kv - 1) / (int64_t(batch) * h_kv);
     const int64_t max_s = (n_k + kDecodeTokenStep - 1) / kDecodeTokenStep;
     if (s > max_s) s = max_s;
+    if (s > kDecodeMaxSplits) s = kDecodeMaxSplits;
     if (s < 1) s = 1;
     return static_cast<int32_t>(s);
 }
@@ -230,23 +231,57 @@ int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse
     return ATF_OK;
 }
 
+namespace {
+int check_pack(const char* what, const void* src, void* dst, int32_t batch, int64_t n_k,
+               int32_t h_kv, int32_t head_dim, size_t dst_bytes) {
+    if (head_dim != 64 && head_dim != 128)
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built", what, head_dim);
+    if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit)
+        return fail(ATF_EINVAL, "%s: need batch >= 1, 1 <= n_k < 2^31, h_kv >= 1", what);
+    if (!src || !dst) return fail(ATF_EINVAL, "%s: NULL pointer", what);
+    if (!aligned(src, 16) || !aligned(dst, 16))
+        return fail(ATF_EINVAL, "%s: pointers must be 16-byte aligned", what);
+    const size_t src_bytes = size_t(batch) * size_t(n_k) * size_t(h_kv) * size_t(head_dim) * 2;
+    const char* a = static_cast<const char*>(src);
+    const char* b = static_cast<const char*>(dst);
+    if (a < b + dst_bytes && b < a + src_bytes)
+        return fail(ATF_EINVAL, "%s: buffers overlap", what);
+    return ATF_OK;
+}
+
+size_t vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_dim) {
+    return size_t(batch) * size_t(h_kv) * size_t((n_k + 15) / 16) * 16 * size_t(head_dim) * 2;
+}
+}  // namespace
+
 int atf_pack_kcache(const void* k_bshd, void* k_pcm, int32_t batch, int64_t n_k, int32_t h_kv,
                     int32_t head_dim, void* hip_stream) {
-    if (head_dim != 64 && head_dim != 128)
-        return fail(ATF_EUNSUPPORTED, "pack_kcache: head_dim %d not built", head_dim);
-    if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit)
-        return fail(ATF_EINVAL, "pack_kcache: need batch >= 1, 1 <= n_k < 2^31, h_kv >= 1");
-    if (!k_bshd || !k_pcm) return fail(ATF_EINVAL, "pack_kcache: NULL pointer");
-    if (!aligned(k_bshd, 16) || !aligned(k_pcm, 16))
-        return fail(ATF_EINVAL, "pack_kcache: pointers must be 16-byte aligned");
     const size_t bytes = size_t(batch) * size_t(n_k) * size_t(h_kv) * size_t(head_dim) * 2;
-    const char* a = static_cast<const char*>(k_bshd);
-    const char* b = static_cast<const char*>(k_pcm);
-    if (a < b + bytes && b < a + bytes) return fail(ATF_EINVAL, "pack_kcache: buffers overlap");
+    int rc = check_pack("pack_kcache", k_bshd, k_pcm, batch, n_k, h_kv, head_dim, bytes);
+    if (rc != ATF_OK) return rc;
     atf::PackParams p{static_cast<const uint16_t*>(k_bshd), static_cast<uint16_t*>(k_pcm), batch,
                       static_cast<int32_t>(n_k), h_kv};
     hipError_t e = atf::launch_pack_kcache(p, head_dim, static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return fail(ATF_EHIP, "pack_kcache: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
+}
+
+size_t atf_vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_dim) {
+    if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit || (head_dim != 64 && head_dim != 128))
+        return 0;
+    return vcache_bytes(batch, n_k, h_kv, head_dim);
+}
+
+int atf_pack_vcache(const void* v_bshd, void* v_pack, int32_t batch, int64_t n_k, int32_t h_kv,
+                    int32_t head_dim, void* hip_stream) {
+    int rc = check_pack("pack_vcache", v_bshd, v_pack, batch, n_k, h_kv, head_dim,
+                        (batch >= 1 && n_k >= 1 && h_kv >= 1 && n_k <= kPosLimit)
+                            ? vcache_bytes(batch, n_k, h_kv, head_dim) : 0);
+    if (rc != ATF_OK) return rc;
+    atf::PackParams p{static_cast<const uint16_t*>(v_bshd), static_cast<uint16_t*>(v_pack), batch,
+                      static_cast<int32_t>(n_k), h_kv};
+    hipError_t e = atf::launch_pack_vcache(p, head_dim, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "pack_vcache: launch failed: %s", hipGetErrorString(e));
     return ATF_OK;
 }
 
@@ -310,7 +345,7 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
     const int32_t group = h_q / h_kv;
     int32_t hpb = 1;
-    for (int32_t c = 8; c >= 1; --c)
+    for (int32_t c = atf::kDecodeMaxHeads; c >= 1; --c)
         if (group % c == 0) {
             hpb = c;
             break;
@@ -318,7 +353,7 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
     char* ws = static_cast<char*>(workspace);
     p.q = static_cast<const uint16_t*>(q);
     p.kpcm = static_cast<const uint16_t*>(k_cache);
-    p.v = static_cast<const uint16_t*>(v_cache);
+    p.vpk = static_cast<const uint16_t*>(v_cache);
     p.o = static_cast<uint16_t*>(o);
     p.lse = lse;
     p.ws_m = reinterpret_cast<float*>(ws + L.off_m);

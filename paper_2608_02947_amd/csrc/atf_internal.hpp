@@ -37,14 +37,14 @@ struct PrefillParams {
 struct DecodeParams {
     const uint16_t* q;       // [B][h_q][d]
     const uint16_t* kpcm;    // [B][h_kv][d/16][n_k][16]
-    const uint16_t* v;       // [B][h_kv][n_k][d]
+    const uint16_t* vpk;     // [B][h_kv][ceil(n_k/16)][d][16] (see atf_pack_vcache)
     uint16_t* o;             // [B][h_q][d]
     float* lse;              // [B][h_q]
     float* ws_m;             // [B][h_q][splits]   running max (log2 domain)
     float* ws_l;             // [B][h_q][splits]   normaliser
     float* ws_o;             // [B][h_q][splits][d] unnormalised output
     int32_t batch, n_k, q_pos, h_q, h_kv, group;
-    int32_t heads_per_block;  // query heads handled by one workgroup (divides group, <= 8)
+    int32_t heads_per_block;  // query heads handled by one workgroup (divides group, <= 32)
     int32_t n_valid;          // keys 0 .. n_valid - 1 are causal
     int32_t splits;
     int32_t split_tokens;     // tokens per split (multiple of the workgroup's token step)
@@ -54,7 +54,7 @@ struct DecodeParams {
 
 struct PackParams {
     const uint16_t* src;  // [B][n_k][h_kv][d]
-    uint16_t* dst;        // [B][h_kv][d/16][n_k][16]
+    uint16_t* dst;        // K: [B][h_kv][d/16][n_k][16]; V: [B][h_kv][ceil(n_k/16)][d][16]
     int32_t batch, n_k, h_kv;
 };
 
@@ -62,10 +62,15 @@ struct PackParams {
 hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan: number of KV splits per (batch, kv head) for these sizes.
 int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);
 // Tokens handled per decode workgroup iteration (the split granularity).
-constexpr int32_t kDecodeTokenStep = 256;
+constexpr int32_t kDecodeTokenStep = 128;
+// Largest split count the merge kernel accepts.
+constexpr int32_t kDecodeMaxSplits = 4096;
+// Query heads one decode workgroup handles at most (columns of its MFMA tiles).
+constexpr int32_t kDecodeMaxHeads = 32;
 
 }  // namespace atf

@@ -3,244 +3,334 @@
 // the split/merge decomposition is the one Sec. 5 describes), over a
 // pair-chunk-major K cache so that pruned pairs are never read from HBM.
 //
-// K cache layout [B][h_kv][d/16][n_k][16]: chunk c of a head is a contiguous
-// stream over tokens of 16 bf16 = dims [8c, 8c+8) then [d/2 + 8c, d/2 + 8c + 8).
-// With the query at position q_pos, token t sits at distance z = q_pos - t, and
-// chunk c is needed only for z <= max_{r in c} W_r: a contiguous suffix of the
-// stream.  Tokens with chunk_min < z <= chunk_max keep some pairs of the chunk;
-// the dropped pairs are zeroed per token before the dot product.
+// Caches (both produced from [B][n_k][h_kv][d] by the pack kernels below):
+//   K [B][h_kv][d/16][n_k][16]: chunk c of a head is a contiguous stream over
+//     tokens of 16 bf16 = dims [8c, 8c+8) then [d/2 + 8c, d/2 + 8c + 8).  With the
+//     query at position q_pos, token t sits at distance z = q_pos - t, and chunk c
+//     is needed only where z <= max_{r in c} W_r: a contiguous suffix of its
+//     stream.  32 tokens of one chunk are 1 KB of contiguous memory.
+//   V [B][h_kv][ceil(n_k/16)][d][16]: blocks of 16 tokens stored d-major, the 16
+//     tokens of a d-row in the order the PV matrix instruction consumes them
+//     (position 8h + e holds token 8*(e/4) + 4h + e%4), zero past n_k.
 //
-// Workgroup = 4 waves over one token split of one (batch, kv head, group of
-// query heads).  QK: lane = token (64 tokens per wave step), dot products in
-// fp32 against the pre-scaled query held in LDS.  PV: lanes re-map to
-// (token group, 8 output dims) so V rows stream as 16-byte loads; the per-token
-// probabilities pass through LDS.  The split writes (max, normaliser, output)
-// partials; decode_merge_kernel combines them.
+// The G query heads of one KV head are the columns of 32x32 MFMA tiles, so a
+// decode step is the prefill's arithmetic with "query rows" = heads:
+//   S^T[token][head] = K[token][dims] * Q^T[dims][head]   (A from the K stream)
+//   O^T[d][head]    += V^T[d][token] * P^T[token][head]   (A from the V blocks)
+// Every operand fragment is a 16-byte load straight from HBM into registers; no
+// LDS staging and no barrier in the streaming loop.  Each wave streams its own
+// 32-token blocks of the workgroup's split; the four waves' partial softmax
+// states are combined in LDS and written as the split's partial.
+//
+// Window: per 32-token block, all pairs are classified by two lane-parallel
+// compares and ballots (lane r holds W_r): pairs kept at every distance of the
+// block, and pairs kept at some distance.  Chunks with no kept pair are not
+// loaded.  Pairs whose window ends inside the block get one extra MFMA each,
+// added only to the tokens within their window.
 #include "atf_internal.hpp"
 
 namespace atf {
 namespace {
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float bf_lo(uint32_t x) { return __builtin_bit_cast(float, x << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t x) { return __builtin_bit_cast(float, x & 0xFFFF0000u); }
-__device__ __forceinline__ float bf_to_f(uint16_t x) { return __builtin_bit_cast(float, uint32_t(x) << 16); }
+constexpr int kWaves = 4;
+constexpr float kRescale = 8.0f;  // lazy-rescale threshold, log2 units
+
+__device__ __forceinline__ f32x16_t mfma(u32x4_t a, u32x4_t b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                   __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16_t zero16() {
+    f32x16_t z;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) z[v] = 0.f;
+    return z;
+}
+
+// Keep only the pairs whose bit is set in `mask` (bit e = pair 8c+e of the chunk).
+__device__ __forceinline__ u32x4_t keep_pairs(u32x4_t x, uint32_t mask) {
+    u32x4_t r;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const uint32_t m = ((mask >> (2 * t)) & 1u ? 0x0000FFFFu : 0u) |
+                           ((mask >> (2 * t + 1)) & 1u ? 0xFFFF0000u : 0u);
+        r[t] = x[t] & m;
+    }
+    return r;
+}
+
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-    return x;
-}
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
-    return x;
-}
-
-constexpr int kWaves = 4;
-
-template <int D, int NG>
-__global__ __launch_bounds__(256) void decode_split_kernel(const DecodeParams p) {
+template <int D>
+__global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const DecodeParams p) {
     constexpr int kChunks = D / 16;
     constexpr int kHalf = D / 2;
-    constexpr int LPT = D / 8;      // lanes per token in the PV phase (8 dims each)
-    constexpr int TPI = 64 / LPT;   // tokens per PV load row
-    constexpr int ROWS = 64 / TPI;  // PV load rows per 64 tokens
-
-    __shared__ float qs[NG][D];
-    __shared__ float ps[kWaves][NG][64];
-    __shared__ float red_m[kWaves][NG];
-    __shared__ float red_l[kWaves][NG];
-    __shared__ float red_o[kWaves][NG][D];
+    constexpr int kDB = D / 32;  // 32-dim blocks of the output
+    __shared__ float red_m[kWaves][32];
+    __shared__ float red_l[kWaves][32];
+    __shared__ float red_o[kDecodeMaxHeads][D + 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int col = lane & 31;  // head column
+    const int hh = lane >> 5;
     const int split = blockIdx.x;
-    const int subgroups = p.group / NG;
+    const int NH = p.heads_per_block;
+    const int subgroups = p.group / NH;
     const int g = blockIdx.y / subgroups;
     const int sub = blockIdx.y % subgroups;
     const int b = blockIdx.z;
-    const int hq0 = g * p.group + sub * NG;
-
-    for (int i = tid; i < NG * D; i += 256) {
-        const int h = i / D, x = i % D;
-        qs[h][x] = bf_to_f(p.q[(int64_t(b) * p.h_q + hq0 + h) * D + x]) * p.scale_log2;
-    }
-    __syncthreads();
+    const int hq0 = g * p.group + sub * NH;
+    const bool head_ok = col < NH;
 
     const int t_begin = split * p.split_tokens;
     const int t_end = min(p.n_valid, t_begin + p.split_tokens);
+    const int nblk16 = (p.n_k + 15) / 16;
 
     const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * int64_t(p.n_k) * 16;
-    const uint16_t* vbase = p.v + (int64_t(b) * p.h_kv + g) * int64_t(p.n_k) * D;
+    const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * int64_t(nblk16) * D * 16;
+    const int my_w = lane < kHalf ? p.win.W[lane] : -1;
 
-    float m[NG], lpart[NG], o[NG][8];
-#pragma unroll
-    for (int h = 0; h < NG; ++h) {
-        m[h] = -INFINITY;
-        lpart[h] = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = 0.f;
-    }
-
-    const int tg = lane / LPT;  // PV token group
-    const int ds = lane % LPT;  // PV dims 8*ds .. 8*ds+7
-
-    for (int tb = t_begin + 64 * wave; tb < t_end; tb += 64 * kWaves) {
-        // ---- QK: lane = token
-        const int t = tb + lane;
-        const bool valid = t < t_end;
-        const int z = p.q_pos - t;
-        const int zmin_wave = p.q_pos - min(tb + 63, t_end - 1);
-        float s[NG];
-#pragma unroll
-        for (int h = 0; h < NG; ++h) s[h] = 0.f;
+    // query fragments (B operand): head column `col`, dims of half hh of every chunk
+    u32x4_t qf[kChunks];
+    {
+        const uint16_t* qrow = p.q + (int64_t(b) * p.h_q + hq0 + (head_ok ? col : 0)) * D + hh * kHalf;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) {
-            const int cmax = p.win.chunk_max[c];
-            if (cmax < zmin_wave) continue;  // no token of this wave step keeps the chunk
-            if (valid && z <= cmax) {
-                const uint16_t* rec = kstream + (int64_t(c) * p.n_k + t) * 16;
-                u32x4_t klo = *reinterpret_cast<const u32x4_t*>(rec);
-                u32x4_t khi = *reinterpret_cast<const u32x4_t*>(rec + 8);
-                if (z > p.win.chunk_min[c]) {  // boundary token: drop pairs with W_r < z
-#pragma unroll
-                    for (int tt = 0; tt < 4; ++tt) {
-                        const uint32_t mk = (z <= p.win.W[8 * c + 2 * tt] ? 0x0000FFFFu : 0u) |
-                                            (z <= p.win.W[8 * c + 2 * tt + 1] ? 0xFFFF0000u : 0u);
-                        klo[tt] &= mk;
-                        khi[tt] &= mk;
-                    }
-                }
-                float kl[8], kh[8];
-#pragma unroll
-                for (int tt = 0; tt < 4; ++tt) {
-                    kl[2 * tt] = bf_lo(klo[tt]);
-                    kl[2 * tt + 1] = bf_hi(klo[tt]);
-                    kh[2 * tt] = bf_lo(khi[tt]);
-                    kh[2 * tt + 1] = bf_hi(khi[tt]);
-                }
-#pragma unroll
-                for (int h = 0; h < NG; ++h) {
-                    float acc = s[h];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        acc = __builtin_fmaf(qs[h][8 * c + e], kl[e], acc);
-                        acc = __builtin_fmaf(qs[h][kHalf + 8 * c + e], kh[e], acc);
-                    }
-                    s[h] = acc;
-                }
-            }
+            u32x4_t z = {0u, 0u, 0u, 0u};
+            if (head_ok) z = *reinterpret_cast<const u32x4_t*>(qrow + 8 * c);
+            qf[c] = z;
         }
-        // ---- online softmax over this wave step (scores already in the log2 domain)
-#pragma unroll
-        for (int h = 0; h < NG; ++h) {
-            const float sv = valid ? s[h] : -INFINITY;
-            const float m_new = fmaxf(m[h], wave_max(sv));  // finite: lane 0 is valid
-            const float alpha = exp2_fast(m[h] - m_new);
-            const float pr = exp2_fast(sv - m_new);
-            lpart[h] = lpart[h] * alpha + pr;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[h][e] *= alpha;
-            m[h] = m_new;
-            ps[wave][h][lane] = pr;
-        }
-        __builtin_amdgcn_wave_barrier();
-        // ---- PV: lanes = (token group, 8 dims)
-#pragma unroll 4
-        for (int r = 0; r < ROWS; ++r) {
-            const int tl = tg * ROWS + r;
-            const int tv = tb + tl;
-            if (tv < t_end) {
-                const u32x4_t vv =
-                    *reinterpret_cast<const u32x4_t*>(vbase + int64_t(tv) * D + 8 * ds);
-                float vf[8];
-#pragma unroll
-                for (int tt = 0; tt < 4; ++tt) {
-                    vf[2 * tt] = bf_lo(vv[tt]);
-                    vf[2 * tt + 1] = bf_hi(vv[tt]);
-                }
-#pragma unroll
-                for (int h = 0; h < NG; ++h) {
-                    const float pr = ps[wave][h][tl];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) o[h][e] = __builtin_fmaf(pr, vf[e], o[h][e]);
-                }
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
     }
 
-    // ---- reduce within the wave, then across waves
+    f32x16_t oacc[kDB];
 #pragma unroll
-    for (int h = 0; h < NG; ++h) {
-        const float l = wave_sum(lpart[h]);
+    for (int i = 0; i < kDB; ++i) oacc[i] = zero16();
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+    const float sc = p.scale_log2;
+
+    for (int t0 = t_begin + 32 * wave; t0 < t_end; t0 += 32 * kWaves) {
+        const int t_last = min(t0 + 31, t_end - 1);
+        const int zhi = p.q_pos - t0;
+        const int zlo = max(0, p.q_pos - t_last);
+        const uint64_t full = __ballot(my_w >= zhi);
+        const uint64_t keep = __ballot(my_w >= zlo);
+
+        // K fragments of the kept chunks (A operand: token t0 + col, dims of half hh);
+        // the last chunk is always fetched because the first MFMA multiplies it
+        const int tok = t0 + col;
+        const bool tok_ok = tok < t_end;
+        u32x4_t kf[kChunks];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            float x = o[h][e];
-#pragma unroll
-            for (int off = LPT; off < 64; off <<= 1) x += __shfl_xor(x, off);
-            o[h][e] = x;
+        for (int c = 0; c < kChunks; ++c) {
+            u32x4_t z = {0u, 0u, 0u, 0u};
+            const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
+            if (kept && tok_ok)
+                z = *reinterpret_cast<const u32x4_t*>(kstream + (int64_t(c) * p.n_k + tok) * 16 + 8 * hh);
+            kf[c] = z;
         }
-        if (lane == 0) {
-            red_m[wave][h] = m[h];
-            red_l[wave][h] = l;
-        }
-        if (lane < LPT) {
+        // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each 16-token group)
+        u32x4_t vf[2][kDB];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) red_o[wave][h][8 * ds + e] = o[h][e];
+        for (int ks = 0; ks < 2; ++ks) {
+            const int blk = t0 / 16 + ks;
+#pragma unroll
+            for (int i = 0; i < kDB; ++i) {
+                u32x4_t z = {0u, 0u, 0u, 0u};
+                if (blk < nblk16)
+                    z = *reinterpret_cast<const u32x4_t*>(vblocks + (int64_t(blk) * D + 32 * i + col) * 16 + 8 * hh);
+                vf[ks][i] = z;
+            }
         }
+
+        // QK (lowest frequencies first; one MFMA site per chunk)
+        f32x16_t sacc;
+#pragma unroll
+        for (int c = kChunks - 1; c >= 0; --c) {
+            const uint32_t fc = uint32_t(full >> (8 * c)) & 0xFFu;
+            if (c == kChunks - 1) {
+                sacc = mfma(kf[c], keep_pairs(qf[c], fc), zero16());
+            } else if (fc) {
+                u32x4_t qb = qf[c];
+                if (fc != 0xFFu) qb = keep_pairs(qb, fc);
+                sacc = mfma(kf[c], qb, sacc);
+            }
+        }
+        // pairs whose window ends inside the block (register v: token t0 + off(v) + 4 hh)
+        uint64_t part = keep & ~full;
+        while (part) {
+            const int r = __builtin_ctzll(part);
+            part &= part - 1;
+            const int c = r >> 3;
+            u32x4_t kfc = kf[0], qfc = qf[0];
+#pragma unroll
+            for (int cc = 1; cc < kChunks; ++cc)
+                if (cc == c) {
+                    kfc = kf[cc];
+                    qfc = qf[cc];
+                }
+            const f32x16_t t = mfma(kfc, keep_pairs(qfc, 1u << (r & 7)), zero16());
+            const int thr = p.q_pos - t0 - 4 * hh - p.win.W[r];  // keep iff off(v) >= thr
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int off = 8 * (v / 4) + (v % 4);
+                sacc[v] += off >= thr ? t[v] : 0.f;
+            }
+        }
+        // tokens past the split's end
+        if (t0 + 32 > t_end) {
+            const int bound = t_end - t0 - 4 * hh;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int off = 8 * (v / 4) + (v % 4);
+                if (off >= bound) sacc[v] = -INFINITY;
+            }
+        }
+
+        // online softmax per head column
+        float mx = -INFINITY;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float cand = mx * sc;
+        if (__any(cand > m_run + kRescale)) {
+            const float m_new = fmaxf(m_run, cand);
+            const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int i = 0; i < kDB; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        u32x4_t pb[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float a = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t], sc, -m_use));
+                const float c2 = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t + 1], sc, -m_use));
+                l_run += a;
+                l_run += c2;
+                bf16x2_t two;
+                two[0] = (__bf16)a;
+                two[1] = (__bf16)c2;
+                pb[ks][t] = __builtin_bit_cast(uint32_t, two);
+            }
+        }
+        // PV
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < kDB; ++i) oacc[i] = mfma(vf[ks][i], pb[ks], oacc[i]);
+    }
+
+    // ---- combine the four waves' states (in wave order, so the result is
+    // deterministic) and write the split's partial
+    const float l_lane = l_run + __shfl_xor(l_run, 32);
+    if (hh == 0) {
+        red_m[wave][col] = m_run;
+        red_l[wave][col] = l_lane;
     }
     __syncthreads();
-    for (int i = tid; i < NG * D; i += 256) {
-        const int h = i / D, x = i % D;
+    float m_all = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) m_all = fmaxf(m_all, red_m[w][col]);
+    const float f = m_run == -INFINITY ? 0.f : exp2_fast(m_run - m_all);
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+        if (wave == w && head_ok) {
+#pragma unroll
+            for (int i = 0; i < kDB; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    float& dst = red_o[col][32 * i + 8 * (v / 4) + 4 * hh + (v % 4)];
+                    dst = (w == 0 ? 0.f : dst) + oacc[i][v] * f;
+                }
+        }
+        __syncthreads();
+    }
+    for (int e = tid; e < NH * D; e += kWaves * 64) {
+        const int h = e / D, x = e % D;
         float M = -INFINITY;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) M = fmaxf(M, red_m[w][h]);
-        float L = 0.f, O = 0.f;
+        float L = 0.f;
         if (M != -INFINITY) {
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) {
-                const float f = exp2_fast(red_m[w][h] - M);  // 0 for an idle wave
-                L += red_l[w][h] * f;
-                O += red_o[w][h][x] * f;
-            }
+            for (int w = 0; w < kWaves; ++w)
+                if (red_m[w][h] != -INFINITY) L += red_l[w][h] * exp2_fast(red_m[w][h] - M);
         }
         const int64_t slot = (int64_t(b) * p.h_q + hq0 + h) * p.splits + split;
         if (x == 0) {
             p.ws_m[slot] = M;
             p.ws_l[slot] = L;
         }
-        p.ws_o[slot * D + x] = O;
+        p.ws_o[slot * D + x] = red_o[h][x];
     }
 }
 
+// Merge of the split partials of one (batch, head) and 32 output dims: 256 threads
+// = 8 split lanes x 32 dims.
 template <int D>
-__global__ __launch_bounds__(D) void decode_merge_kernel(const DecodeParams p) {
-    const int hq = blockIdx.x;
-    const int b = blockIdx.y;
-    const int x = threadIdx.x;
-    const int64_t base = (int64_t(b) * p.h_q + hq) * p.splits;
+__global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p) {
+    __shared__ float s_w[kDecodeMaxSplits];  // split weights exp2(m_s - M)
+    __shared__ float s_red[256];
+    const int bh = blockIdx.x;  // b * h_q + hq
+    const int d0 = 32 * blockIdx.y;
+    const int tid = threadIdx.x;
+    const int64_t base = int64_t(bh) * p.splits;
     float M = -INFINITY;
-    for (int s = 0; s < p.splits; ++s) M = fmaxf(M, p.ws_m[base + s]);
-    float L = 0.f, O = 0.f;
-    for (int s = 0; s < p.splits; ++s) {
-        const float ms = p.ws_m[base + s];
-        if (ms == -INFINITY) continue;  // split with no causal key
-        const float f = exp2_fast(ms - M);
-        L += p.ws_l[base + s] * f;
-        O += p.ws_o[(base + s) * D + x] * f;
+    for (int s = tid; s < p.splits; s += 256) M = fmaxf(M, p.ws_m[base + s]);
+    s_red[tid] = M;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (tid < off) s_red[tid] = fmaxf(s_red[tid], s_red[tid + off]);
+        __syncthreads();
     }
-    p.o[(int64_t(b) * p.h_q + hq) * D + x] = __builtin_bit_cast(uint16_t, (__bf16)(O / L));
-    if (x == 0) p.lse[int64_t(b) * p.h_q + hq] = M * 0.69314718055994531f + logf(L);
+    M = s_red[0];
+    __syncthreads();
+    float L = 0.f;
+    for (int s = tid; s < p.splits; s += 256) {
+        const float ms = p.ws_m[base + s];
+        const float w = ms == -INFINITY ? 0.f : exp2_fast(ms - M);  // split with no causal key
+        s_w[s] = w;
+        L += p.ws_l[base + s] * w;
+    }
+    s_red[tid] = L;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (tid < off) s_red[tid] += s_red[tid + off];
+        __syncthreads();
+    }
+    L = s_red[0];
+    __syncthreads();
+    const int x = tid & 31, sl = tid >> 5;
+    float O = 0.f;
+    for (int s = sl; s < p.splits; s += 8) O += s_w[s] * p.ws_o[(base + s) * D + d0 + x];
+    s_red[tid] = O;
+    __syncthreads();
+    if (tid < 32) {
+        float acc = 0.f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc += s_red[tid + 32 * k];
+        p.o[int64_t(bh) * D + d0 + x] = __builtin_bit_cast(uint16_t, (__bf16)(acc / L));
+        if (blockIdx.y == 0 && tid == 0) p.lse[bh] = M * 0.69314718055994531f + logf(L);
+    }
 }
 
 template <int D>
 __global__ __launch_bounds__(256) void pack_kcache_kernel(const PackParams p) {
     constexpr int kChunks = D / 16;
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
     const int64_t total = int64_t(p.batch) * p.n_k * p.h_kv * kChunks;
     for (int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x; idx < total;
          idx += int64_t(gridDim.x) * 256) {
@@ -251,59 +341,88 @@ __global__ __launch_bounds__(256) void pack_kcache_kernel(const PackParams p) {
         const int t = int(r % p.n_k);
         const int b = int(r / p.n_k);
         const uint16_t* src = p.src + ((int64_t(b) * p.n_k + t) * p.h_kv + g) * D;
-        const u32x4_t lo = *reinterpret_cast<const u32x4_t*>(src + 8 * c);
-        const u32x4_t hi = *reinterpret_cast<const u32x4_t*>(src + D / 2 + 8 * c);
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(src + 8 * c);
+        const u32x4 hi = *reinterpret_cast<const u32x4*>(src + D / 2 + 8 * c);
         uint16_t* dst = p.dst + (((int64_t(b) * p.h_kv + g) * kChunks + c) * p.n_k + t) * 16;
-        *reinterpret_cast<u32x4_t*>(dst) = lo;
-        *reinterpret_cast<u32x4_t*>(dst + 8) = hi;
+        *reinterpret_cast<u32x4*>(dst) = lo;
+        *reinterpret_cast<u32x4*>(dst + 8) = hi;
     }
 }
 
-template <int D, int NG>
-hipError_t launch_split(const DecodeParams& p, hipStream_t stream) {
-    const dim3 grid(unsigned(p.splits), unsigned(p.h_kv * (p.group / NG)), unsigned(p.batch));
-    hipLaunchKernelGGL((decode_split_kernel<D, NG>), grid, dim3(256), 0, stream, p);
-    return hipGetLastError();
+// V blocks: one thread per (batch, kv head, 16-token block, dim); position
+// 8h + e of the row holds token 8*(e/4) + 4h + e%4 of the block.
+template <int D>
+__global__ __launch_bounds__(256) void pack_vcache_kernel(const PackParams p) {
+    const int nblk = (p.n_k + 15) / 16;
+    const int64_t total = int64_t(p.batch) * p.h_kv * nblk * D;
+    for (int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x; idx < total;
+         idx += int64_t(gridDim.x) * 256) {
+        const int x = int(idx % D);
+        int64_t r = idx / D;
+        const int blk = int(r % nblk);
+        r /= nblk;
+        const int g = int(r % p.h_kv);
+        const int b = int(r / p.h_kv);
+        uint16_t row[16];
+#pragma unroll
+        for (int pos = 0; pos < 16; ++pos) {
+            const int h = pos >> 3, e = pos & 7;
+            const int t = 16 * blk + 8 * (e >> 2) + 4 * h + (e & 3);
+            row[pos] = t < p.n_k ? p.src[((int64_t(b) * p.n_k + t) * p.h_kv + g) * D + x] : uint16_t(0);
+        }
+        uint16_t* dst = p.dst + ((int64_t(b) * p.h_kv + g) * nblk + blk) * int64_t(D) * 16 + int64_t(x) * 16;
+#pragma unroll
+        for (int pos = 0; pos < 16; ++pos) dst[pos] = row[pos];
+    }
 }
 
 template <int D>
 hipError_t launch_decode_d(const DecodeParams& p, hipStream_t stream) {
-    hipError_t e;
-    switch (p.heads_per_block) {
-        case 1: e = launch_split<D, 1>(p, stream); break;
-        case 2: e = launch_split<D, 2>(p, stream); break;
-        case 3: e = launch_split<D, 3>(p, stream); break;
-        case 4: e = launch_split<D, 4>(p, stream); break;
-        case 5: e = launch_split<D, 5>(p, stream); break;
-        case 6: e = launch_split<D, 6>(p, stream); break;
-        case 7: e = launch_split<D, 7>(p, stream); break;
-        case 8: e = launch_split<D, 8>(p, stream); break;
-        default: return hipErrorInvalidValue;
-    }
+    const dim3 grid(unsigned(p.splits), unsigned(p.h_kv * (p.group / p.heads_per_block)),
+                    unsigned(p.batch));
+    hipLaunchKernelGGL(decode_split_kernel<D>, grid, dim3(kWaves * 64), 0, stream, p);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(unsigned(p.h_q), unsigned(p.batch)), dim3(D), 0,
-                       stream, p);
+    hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(unsigned(p.batch * p.h_q), unsigned(D / 32)),
+                       dim3(256), 0, stream, p);
     return hipGetLastError();
+}
+
+unsigned pack_blocks(int64_t total) {
+    int64_t blocks = (total + 255) / 256;
+    return unsigned(blocks > 65536 ? 65536 : blocks);
 }
 
 }  // namespace
 
 hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream) {
-    if (p.splits < 1 || p.group % p.heads_per_block != 0) return hipErrorInvalidValue;
-    if (int64_t(p.splits) * p.split_tokens < p.n_valid) return hipErrorInvalidValue;
+    if (p.splits < 1 || p.splits > kDecodeMaxSplits) return hipErrorInvalidValue;
+    if (p.heads_per_block < 1 || p.heads_per_block > kDecodeMaxHeads ||
+        p.group % p.heads_per_block != 0)
+        return hipErrorInvalidValue;
+    if (int64_t(p.splits) * p.split_tokens < p.n_valid || p.split_tokens % kDecodeTokenStep != 0)
+        return hipErrorInvalidValue;
     (void)hipGetLastError();
     return head_dim == 64 ? launch_decode_d<64>(p, stream) : launch_decode_d<128>(p, stream);
 }
 
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream) {
     const int64_t total = int64_t(p.batch) * p.n_k * p.h_kv * (head_dim / 16);
-    int64_t blocks = (total + 255) / 256;
-    if (blocks > 65536) blocks = 65536;
     (void)hipGetLastError();
     if (head_dim == 64)
-        hipLaunchKernelGGL(pack_kcache_kernel<64>, dim3(unsigned(blocks)), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL(pack_kcache_kernel<64>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
     else
-        hipLaunchKernelGGL(pack_kcache_kernel<128>, dim3(unsigned(blocks)), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL(pack_kcache_kernel<128>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream) {
+    const int64_t total = int64_t(p.batch) * p.h_kv * ((p.n_k + 15) / 16) * head_dim;
+    (void)hipGetLastError();
+    if (head_dim == 64)
+        hipLaunchKernelGGL(pack_vcache_kernel<64>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL(pack_vcache_kernel<128>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

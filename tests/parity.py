@@ -52,20 +52,28 @@ def pack_kcache(k_bshd):
     return kp
 
 
-def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vt=None):
-    """q [B, h_q, d]; caches given in BSHD are packed / transposed first."""
+def pack_vcache(v_bshd):
+    import paper_2608_02947_amd as atf
+    B, n_k, h_kv, d = v_bshd.shape
+    vp = torch.empty(atf.vcache_shape(B, n_k, h_kv, d), dtype=torch.bfloat16, device=v_bshd.device)
+    atf.atf_pack_vcache(v_bshd, vp)
+    return vp
+
+
+def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vp=None):
+    """q [B, h_q, d]; caches given in BSHD are packed by the library first."""
     import paper_2608_02947_amd as atf
     B, h_q, d = q.shape
     _, n_k, h_kv, _ = k_bshd.shape
     if kp is None:
         kp = pack_kcache(k_bshd)
-    if vt is None:
-        vt = v_bshd.permute(0, 2, 1, 3).contiguous()
+    if vp is None:
+        vp = pack_vcache(v_bshd)
     ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, n_k, d), dtype=torch.uint8,
                      device=q.device)
     o = torch.empty_like(q)
     lse = torch.empty((B, h_q), dtype=torch.float32, device=q.device)
-    atf.atf_decode(q, kp, vt, o, lse, q_pos, win, ws, scale)
+    atf.atf_decode(q, kp, vp, o, lse, q_pos, win, ws, scale)
     torch.cuda.synchronize()
     return o, lse
 

@@ -179,3 +179,19 @@ def test_pack_validation_before_launch():
     assert lib.atf_pack_kcache(16, 1 << 20, 0, 4, 1, 64, None) == atf.ATF_EINVAL
     assert atf.atf_kcache_chunk_pairs(128) == 8 and atf.atf_kcache_chunk_pairs(64) == 8
     assert atf.atf_kcache_chunk_pairs(32) == 0
+
+
+def test_vpack_validation_and_size():
+    lib = atf.library()
+    assert atf.atf_vcache_bytes(1, 17, 2, 64) == 1 * 2 * 2 * 16 * 64 * 2
+    assert atf.atf_vcache_bytes(3, 16, 1, 128) == 3 * 1 * 1 * 16 * 128 * 2
+    assert atf.atf_vcache_bytes(1, 0, 1, 64) == 0
+    assert atf.atf_vcache_bytes(1, 5, 1, 96) == 0
+    # destination overlapping the source (the packed size rounds n_k up to 16)
+    assert lib.atf_pack_vcache(1 << 20, (1 << 20) + 512, 1, 5, 1, 64, None) == atf.ATF_EINVAL
+    assert lib.atf_pack_vcache((1 << 20) + 1024, 1 << 20, 1, 5, 1, 64, None) == atf.ATF_EINVAL
+    assert lib.atf_pack_vcache(16, 1 << 20, 1, 4, 1, 48, None) == atf.ATF_EUNSUPPORTED
+    assert lib.atf_pack_vcache(None, 1 << 20, 1, 4, 1, 64, None) == atf.ATF_EINVAL
+    assert lib.atf_pack_vcache(24, 1 << 20, 1, 4, 1, 64, None) == atf.ATF_EINVAL  # alignment
+    assert lib.atf_pack_vcache(16, 1 << 20, 1, 4, 0, 64, None) == atf.ATF_EINVAL
+    assert atf.vcache_shape(2, 33, 4, 128) == (2, 4, 3, 128, 16)

@@ -1,7 +1,7 @@
-"""GPU parity of atf_pack_kcache and atf_decode against the oracle.
+"""GPU parity of atf_pack_kcache, atf_pack_vcache and atf_decode against the oracle.
 
-The K cache is packed by the library; the pack itself is checked bit-exactly
-against a torch re-indexing of the same tensor.  Decode outputs are compared
+The caches are packed by the library; each pack is checked bit-exactly against
+a torch re-indexing of the same tensor.  Decode outputs are compared
 for every (batch, query head) row, at small shapes and at the full workload
 shapes the benchmark times.
 """
@@ -14,7 +14,8 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import compare, gpu_decode, note, pack_kcache, to_f64, windows_for, workload_window
+from parity import (compare, gpu_decode, note, pack_kcache, pack_vcache, to_f64, windows_for,
+                    workload_window)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -39,6 +40,31 @@ def test_pack_bit_exact(shape):
     torch.cuda.synchronize()
     ref = _ref_pack(k)
     assert torch.equal(kp.view(torch.int16), ref.view(torch.int16))
+
+
+def _ref_vpack(v_bshd):
+    """[B, n_k, h_kv, d] -> [B, h_kv, ceil(n_k/16), d, 16]; slot 8h + e of a block's
+    d-row holds token 8*(e//4) + 4h + e%4 of the block, zero past n_k."""
+    B, n_k, h_kv, d = v_bshd.shape
+    nb = (n_k + 15) // 16
+    vv = torch.zeros((B, nb * 16, h_kv, d), dtype=v_bshd.dtype, device=v_bshd.device)
+    vv[:, :n_k] = v_bshd
+    blocks = vv.view(B, nb, 16, h_kv, d).permute(0, 3, 1, 4, 2)  # [B, h_kv, nb, d, 16 tokens]
+    order = torch.tensor([8 * (e // 4) + 4 * h + e % 4 for h in range(2) for e in range(8)],
+                         device=v_bshd.device)
+    return blocks[..., order].contiguous()
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 64), (2, 37, 3, 128), (3, 1000, 2, 64),
+                                   (1, 4096, 4, 128)])
+def test_vpack_bit_exact(shape):
+    note(f"vpack {shape}")
+    v = W.random_bf16(shape, seed=sum(shape) + 1).to(DEV)
+    vp = pack_vcache(v)
+    torch.cuda.synchronize()
+    ref = _ref_vpack(v)
+    assert vp.shape == ref.shape
+    assert torch.equal(vp.view(torch.int16), ref.view(torch.int16))
 
 
 def _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed, theta=None):
@@ -68,7 +94,9 @@ CASES = [
     (3, 1000, 1000, 7, 1, 64, 1e6, 2.0),
     (1, 2049, 5000, 8, 1, 128, 1e4, 2.0),       # query beyond the cache end
     (1, 3000, 1500, 4, 2, 64, 1e4, 2.0),        # keys past the query are not causal
-    (2, 777, 777, 12, 1, 128, 1e4, 2.0),        # G = 12 in sub-groups of 6
+    (2, 777, 777, 12, 1, 128, 1e4, 2.0),        # G = 12 in one workgroup
+    (1, 1500, 1500, 40, 1, 64, 1e4, 2.0),       # G = 40 in two sub-groups of 20
+    (1, 700, 700, 37, 1, 128, 1e4, 2.0),        # G = 37 (prime): one head per workgroup
     (1, 4096, 4096, 16, 2, 128, 100.0, 2.0),    # saturated windows
     (1, 513, 513, 2, 2, 64, 1e4, 0.05),         # tiny k: empty score sums
     (1, 999, 999, 3, 1, 128, 1e4, math.inf),    # window off
@@ -101,3 +129,15 @@ def test_decode_workload_all_rows(name):
     win, widths = workload_window(wl)
     q4 = inp["q"]
     _decode_parity(q4, inp["k"], inp["v"], wl.q_pos0, win, widths, name)
+
+
+def test_decode_custom_scale_and_determinism():
+    q, k, v = _decode_inputs(1, 3001, 3001, 8, 2, 128, 1e4, seed=11)
+    win, widths = windows_for(128, 1e4, 2.0, None, n_ctx=3002)
+    qd, kd, vd = q[:, 0].contiguous().to(DEV), k.to(DEV), v.to(DEV)
+    note("decode scale 0.2")
+    o, lse = gpu_decode(qd, kd, vd, 3001, win, scale=0.2)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, 3001, widths, scale=0.2)
+    compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], "scale0.2")
+    o2, lse2 = gpu_decode(qd, kd, vd, 3001, win, scale=0.2)
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
