@@ -30,6 +30,7 @@ struct PrefillParams {
     int32_t batch, n_q, n_k, q_pos0, h_q, h_kv, group;
     int32_t pos_per_tile;  // query positions per workgroup (rows = positions x group)
     int32_t n_qtiles;
+    int32_t mono;        // thresholds non-decreasing and the last chunk kept at every distance
     float scale_log2;    // softmax scale * log2(e)
     WindowTable win;
 };

@@ -6,15 +6,16 @@
 //   A workgroup of 8 waves owns 256 query rows that share one KV head: P = 256/G
 //   consecutive positions x the G query heads of the group (row f -> position
 //   f / G, head f % G), so every K/V tile staged in LDS serves 256 rows.  Each
-//   wave owns 32 rows (one MFMA row-block); two waves share a SIMD so one wave's
-//   softmax (VALU) overlaps the other's matrix work.  Key tiles of 64 are
-//   double-buffered in LDS and filled by global_load_lds_dwordx4 (global memory
-//   straight into LDS, no register staging) one tile ahead of the compute.
+//   wave owns 32 rows (one MFMA row-block); two waves share a SIMD.  Key tiles of
+//   64 rotate through three LDS buffers, filled by global_load_lds_dwordx4
+//   (global memory straight into LDS, no register staging) one tile ahead of the
+//   compute.
 //
-// LDS layout: K and V tiles are row-major [key][d] with padded rows, chosen so
-// that the K fragment reads (rows at one 16-byte segment) and the transposed V
-// reads (4 rows x 32 bytes per 16 lanes) hit distinct banks while every fragment
-// address is a per-lane base plus an immediate offset.
+// LDS layout: the K tile is segment-major, [16-byte segment s][key][8 bf16], so
+// one wave-wide direct load fills one segment for all 64 keys, and a chunk (two
+// segments, below) is loaded or skipped by one wave-uniform branch.  The V tile
+// is row-major [key][d] with rows padded to d + 32 bf16 so that the transposed
+// reads (4 rows x 32 bytes per 16 lanes) hit distinct banks.
 //
 // Matrix layout (v_mfma_f32_32x32x16_bf16, lane l, c = l % 32, h = l / 32)
 //   S^T[key][row] = K[key][dims] * Q^T[dims][row]: A = K fragment (key c, dims
@@ -27,16 +28,25 @@
 //   lane i gets column d0 + i of four consecutive key rows).
 //
 // Window as a K-slice (one K-step = one chunk of 8 rotary pairs = dims
-// [8c, 8c+8) and [d/2 + 8c, d/2 + 8c + 8)).  For each (wave, 32-key block) the
-// distances z of its cells span [zlo, zhi].  A chunk whose smallest threshold is
-// >= zhi is kept whole (one MFMA); a chunk whose largest threshold is < zlo is
-// skipped (not loaded into LDS when the whole tile skips it, never multiplied);
-// otherwise the chunk is a boundary chunk: its pairs kept in every cell go into
-// one MFMA with the other pairs' query dims zeroed, and each pair whose threshold
-// falls inside [zlo, zhi) gets one MFMA of its own whose product is added only
-// to the cells with z <= W_r.  Every cell sums exactly its kept pairs.  With the
-// window off (no threshold below the largest distance) the kernel is compiled
-// without any of this: every chunk is a full K-step.
+// [8c, 8c+8) and [d/2 + 8c, d/2 + 8c + 8)).  Whether pair r contributes to a cell
+// depends only on the cell's distance z (keep iff z <= W_r).
+//   Uniform tiles.  When no threshold falls inside the distance range of a wave's
+//   tile, every pair is either kept in all of its cells or in none.  With
+//   thresholds non-decreasing in r, the kept pairs are a suffix r >= rf, so the
+//   tile's QK is the chunks above rf / 8 in full plus chunk rf / 8 with the query
+//   dims of the pairs below rf zeroed.  That set stays the same for a run of
+//   consecutive tiles (until the next threshold enters the distance range), and
+//   each wave runs such a run in a loop compiled for its chunk count: straight
+//   matrix code with no per-tile branch.
+//   Other tiles (a threshold inside the range, or a table that is not monotone)
+//   take the general path: per 32-key block, two ballots classify all pairs at
+//   once (kept in every cell / in some cell); whole chunks go into one MFMA each
+//   with the query dims of pairs kept nowhere zeroed, and each pair whose
+//   threshold lies inside the block's range gets one MFMA of its own whose
+//   product is added only to the cells with z <= W_r.
+//   Every cell sums exactly its kept pairs.  K chunks that no cell of the
+//   workgroup's tile keeps are not loaded into LDS.  With the window off the
+//   kernel is compiled without any of this.
 //
 // Softmax: fp32 in the log2 domain.  The running max is raised only when a row's
 // tile max exceeds it by more than kRescale (log2 units); otherwise the stale
@@ -44,6 +54,8 @@
 // normaliser need no rescaling -- the result is the same softmax.  Row sums add
 // the fp32 probabilities; the PV MFMA consumes them rounded to bf16.
 #include "atf_internal.hpp"
+
+#include <type_traits>
 
 namespace atf {
 namespace {
@@ -54,34 +66,31 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef short s16x8_t __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
 constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kRows = kWaves * 32;  // query rows per workgroup
 constexpr int kBN = 64;             // keys per tile
+constexpr int kStages = 3;          // LDS buffers per K and V tile
 constexpr float kRescale = 8.0f;    // lazy-rescale threshold, log2 units
 
-// Row strides: K rows carry 16 bytes of padding, so 8 consecutive rows read at
-// one 16-byte segment fall on distinct banks; V rows are a multiple of 128 bytes
-// plus 64, so the four rows one transposed read touches start 64 bytes apart
-// modulo the 256-byte bank line.  Both tiles are whole kilobytes: a wave-wide
-// 16-byte direct load fills 1 KB of a tile, slot s = 64 * load + lane holding
-// (row s / slots-per-row, segment s % slots-per-row); slots past a row's data
-// are padding and receive a dummy load.
 template <int D>
 struct Cfg {
     static constexpr int kHalf = D / 2;
     static constexpr int kChunks = D / 16;
-    static constexpr int kSegs = D / 8;          // 16-byte data segments per row
-    static constexpr int kKStride = D + 8;       // bf16 per K row in LDS
-    static constexpr int kVStride = D + 32;      // bf16 per V row in LDS
-    static constexpr int kKSlots = kKStride / 8;
+    static constexpr int kSegs = D / 8;             // 16-byte segments per key row
+    static constexpr int kKTile = kSegs * kBN * 8;  // bf16; segment-major
+    static constexpr int kVStride = D + 32;         // bf16 per V row in LDS
     static constexpr int kVSlots = kVStride / 8;
-    static constexpr int kKTile = kBN * kKStride;  // bf16
     static constexpr int kVTile = kBN * kVStride;
-    static constexpr int kKLoads = kKTile / 512;   // wave-wide loads per tile
-    static constexpr int kVLoads = kVTile / 512;
-    static_assert(kKTile % 512 == 0 && kVTile % 512 == 0, "tiles must be whole kilobytes");
+    static constexpr int kKPerWave = kSegs / kWaves;  // K segments loaded per wave
+    static constexpr int kVLoads = kVTile / 512;      // wave-wide 1 KB loads per V tile
+    static constexpr int kVPer = (kVLoads + kWaves - 1) / kWaves;
+    static_assert(kSegs % kWaves == 0, "K segments must spread evenly over the waves");
+    static_assert(kVTile % 512 == 0, "V tile must be whole kilobytes");
 };
 
 __device__ __forceinline__ f32x16_t mfma(u32x4_t a, u32x4_t b, f32x16_t c) {
@@ -112,26 +121,48 @@ __device__ __forceinline__ u32x4_t keep_pairs(u32x4_t x, uint32_t mask) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
-typedef __attribute__((address_space(3))) char lds_char;
-
-// Transposed 4x4-block read of 16-bit elements from LDS (ds_read_b64_tr_b16).
-__device__ __forceinline__ s16x4_t lds_read_tr(const uint16_t* p) {
-    typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)((lds_char*)(p)));
+// LDS reads at a byte address.  Callers form addresses as (per-lane base below
+// 2^18) + (constant), so the compiler folds the constants into the
+// instructions' offset fields.
+__device__ __forceinline__ u32x4_t lds_read_b128(uint32_t byte_addr) {
+    return *(const lds_u32x4*)(uintptr_t)byte_addr;
+}
+// transposed 4x4-block read of 16-bit elements (ds_read_b64_tr_b16)
+__device__ __forceinline__ s16x4_t lds_read_tr(uint32_t byte_addr) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(uintptr_t)byte_addr);
+}
+// byte offset of the LDS buffer of a tile.  Passed through readfirstlane so the
+// compiler treats it as one opaque scalar per tile instead of re-deriving it in
+// every address (which defeats the offset-field folding above).
+__device__ __forceinline__ uint32_t stage_off(int tile, int buf_bytes) {
+    return uint32_t(__builtin_amdgcn_readfirstlane((tile % kStages) * buf_bytes));
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return uint32_t(reinterpret_cast<uintptr_t>((const lds_char*)p)) & 0x3FFFFu;
 }
 
-// 16 bytes per lane from global memory straight into LDS at lds_wave + 16 * lane
-// (lds_wave must be the same for every lane of the wave).
-__device__ __forceinline__ void load_to_lds(const uint16_t* g, uint16_t* lds_wave) {
-    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)((lds_char*)lds_wave),
-                                     16, 0, 0);
+// 16 bytes per lane from global memory straight into LDS: lane i reads base + off
+// (base wave-uniform) and its 16 bytes land at byte lds_wave + 16 * i (lds_wave
+// wave-uniform).  Issued as inline assembly so that the compiler does not make
+// LDS reads of other buffers wait for it; completion is awaited explicitly
+// (vm_wait) before the workgroup barrier that publishes the buffer.
+__device__ __forceinline__ void load_to_lds(const char* base, uint32_t off, uint32_t lds_wave) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :
+                 : "v"(off), "s"(base), "s"(lds_wave)
+                 : "memory", "m0");
 }
+// wait until this wave's vector memory loads have completed (vmcnt 0 only)
+__device__ __forceinline__ void vm_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+// workgroup barrier without a memory fence: every LDS read is consumed (waited
+// for) before it, and the direct-to-LDS loads are awaited with vm_wait
+__device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
 
 template <int D, bool kWin>
 __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(const PrefillParams p) {
     using C = Cfg<D>;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][C::kKTile];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[2][C::kVTile];
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[kStages][C::kKTile];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[kStages][C::kVTile];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -172,9 +203,9 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     // lane r holds the threshold of pair r (pairs past d/2 never count)
     const int my_w = lane < C::kHalf ? p.win.W[lane] : -1;
 
-    const int64_t kv_row_stride = int64_t(p.h_kv) * D;
-    const uint16_t* kbase = p.k + (int64_t(b) * p.n_k * p.h_kv + g) * D;
-    const uint16_t* vbase = p.v + (int64_t(b) * p.n_k * p.h_kv + g) * D;
+    const uint32_t row_bytes = uint32_t(p.h_kv) * D * 2;
+    const char* kbytes = reinterpret_cast<const char*>(p.k + (int64_t(b) * p.n_k * p.h_kv + g) * D);
+    const char* vbytes = reinterpret_cast<const char*>(p.v + (int64_t(b) * p.n_k * p.h_kv + g) * D);
 
     // query fragments (B operand): row `col`, dims of half hh of every chunk
     u32x4_t qf[C::kChunks];
@@ -189,10 +220,24 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
         }
     }
 
-    // chunks that some cell of the workgroup tile at keys [j0, j0 + 64) keeps, plus
-    // the last chunk: the first QK MFMA of a block always multiplies it (with the
-    // query dims of unkept pairs zeroed), so it must hold finite data
-    auto tile_need = [&](int j0) -> uint32_t {
+    // ---- global -> LDS staging of the tile at key j0 into buffer `buf`.
+    // K: wave w loads segments w, w + 8, ... (for d = 128 exactly the two halves
+    // of chunk w), lane i = key i, skipped when no cell of the workgroup tile keeps
+    // the segment's chunk; the last chunk is always loaded because the QK of a
+    // block always multiplies it.  V: wave w issues the tile's wave-wide loads
+    // w, w + 8, ...; slot s = 64 * load + lane holds (row s / slots-per-row,
+    // segment s % slots-per-row), padding slots re-read segment 0.  In a tile that
+    // crosses n_k, rows past it re-read the last key (finite values; masked).
+    const uint32_t ks_lds = lds_addr(&Ks[0][0]);
+    const uint32_t vs_lds = lds_addr(&Vs[0][0]);
+    uint32_t v_dma[C::kVPer];
+#pragma unroll
+    for (int t = 0; t < C::kVPer; ++t) {
+        const int s = 64 * (wave + kWaves * t) + lane;
+        const int seg = s % C::kVSlots;
+        v_dma[t] = uint32_t(s / C::kVSlots) * row_bytes + 16u * uint32_t(seg < C::kSegs ? seg : 0);
+    }
+    auto tile_need = [&](int j0) __attribute__((always_inline)) -> uint32_t {
         if (!kWin) return (1u << C::kChunks) - 1u;
         const int zlo = max(0, pos_first - (j0 + kBN - 1));
         uint32_t need = 1u << (C::kChunks - 1);
@@ -201,57 +246,42 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
             if (p.win.chunk_max[c] >= zlo) need |= 1u << c;
         return need;
     };
-    // issue the global -> LDS loads of the tile at key j0 into buffer `buf`; wave w
-    // issues the tile's wave-wide loads w, w + 8, ...  A lane's (row, segment) slot
-    // in each load is fixed, so its element offset within the tile is computed once;
-    // the tile base is wave-uniform.  In a tile that crosses n_k, rows past n_k
-    // re-read the last key (finite values; their scores are masked).
-    constexpr int kKPer = (C::kKLoads + kWaves - 1) / kWaves;
-    constexpr int kVPer = (C::kVLoads + kWaves - 1) / kWaves;
-    int k_row[kKPer], k_seg[kKPer], v_row_l[kVPer], v_seg[kVPer];
-#pragma unroll
-    for (int t = 0; t < kKPer; ++t) {
-        const int s = 64 * (wave + kWaves * t) + lane;
-        k_row[t] = s / C::kKSlots;
-        const int seg = s % C::kKSlots;
-        k_seg[t] = seg < C::kSegs ? seg : -1;  // -1: padding slot
-    }
-#pragma unroll
-    for (int t = 0; t < kVPer; ++t) {
-        const int s = 64 * (wave + kWaves * t) + lane;
-        v_row_l[t] = s / C::kVSlots;
-        const int seg = s % C::kVSlots;
-        v_seg[t] = seg < C::kSegs ? seg : 0;  // padding slots load a dummy
-    }
-    auto issue = [&](int j0, int buf) {
+    auto issue = [&](int j0, int buf) __attribute__((always_inline)) {
         const uint32_t need = tile_need(j0);
+        const char* kt = kbytes + int64_t(j0) * row_bytes;  // wave-uniform tile bases
+        const char* vt = vbytes + int64_t(j0) * row_bytes;
         const bool tail = j0 + kBN > p.n_k;
-        const uint16_t* kt = kbase + int64_t(j0) * kv_row_stride;
-        const uint16_t* vt = vbase + int64_t(j0) * kv_row_stride;
-        const int last = p.n_k - 1 - j0;  // last valid row of the tile
+        const uint32_t last = uint32_t(p.n_k - 1 - j0);
+        const uint32_t krow = (tail ? min(uint32_t(lane), last) : uint32_t(lane)) * row_bytes;
+        const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
-        for (int t = 0; t < kKPer; ++t) {
-            const int u = wave + kWaves * t;
-            if (u >= C::kKLoads) break;
-            const int seg = k_seg[t];
-            const int r = tail ? min(k_row[t], last) : k_row[t];
-            if (seg < 0 || ((need >> (seg % C::kChunks)) & 1u))
-                load_to_lds(kt + r * int(kv_row_stride) + 8 * (seg < 0 ? 0 : seg), &Ks[buf][512 * u]);
+        for (int t = 0; t < C::kKPerWave; ++t) {
+            const int s = wave + kWaves * t;
+            if ((need >> (s % C::kChunks)) & 1u) load_to_lds(kt, krow + 16u * s, kdst + 1024u * s);
         }
+        const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
 #pragma unroll
-        for (int t = 0; t < kVPer; ++t) {
+        for (int t = 0; t < C::kVPer; ++t) {
             const int u = wave + kWaves * t;
             if (u >= C::kVLoads) break;
-            const int r = tail ? min(v_row_l[t], last) : v_row_l[t];
-            load_to_lds(vt + r * int(kv_row_stride) + 8 * v_seg[t], &Vs[buf][512 * u]);
+            uint32_t off = v_dma[t];
+            if (tail) {
+                const int s = 64 * u + lane;
+                off = min(uint32_t(s / C::kVSlots), last) * row_bytes + (off % row_bytes);
+            }
+            load_to_lds(vt, off, vdst + 1024u * u);
         }
     };
 
-    // per-lane LDS fragment bases (buffer 0); fragment reads add immediate offsets
-    const int k_off[2] = {col * C::kKStride + hh * C::kHalf,
-                          (32 + col) * C::kKStride + hh * C::kHalf};
+    // per-lane LDS byte bases of the fragment reads (buffer 0, block 0)
+    //   K: chunk c, half hh = segment c + kChunks * hh, key col of the block
+    //   V: lane group of 16 reads key rows 4 * hh + (l % 16) / 4 (8 rows further
+    //      for elements 4..7), dims 16 * ((l / 16) % 2) + 4 * (l % 4) of each
+    //      32-dim block
+    const uint32_t k_lane = ks_lds + uint32_t((C::kChunks * hh * kBN + col) * 16);
     const int v_dsub = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
     const int v_row = 4 * hh + ((lane & 15) >> 2);
+    const uint32_t v_lane = vs_lds + uint32_t((v_row * C::kVStride + v_dsub) * 2);
 
     f32x16_t oacc[D / 32];
 #pragma unroll
@@ -259,160 +289,252 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     float m_run = -INFINITY;  // running (possibly stale) max, log2 domain
     float l_run = 0.f;        // normaliser over this lane's keys
     const float sc = p.scale_log2;
+    f32x16_t sacc[2];  // scores of the current tile (two 32-key blocks)
+    u32x4_t qb;        // query dims of chunk qb_rf / 8 with the pairs below qb_rf zeroed
+    int qb_rf = -1;
+
+    auto k_block = [&](int tile, int kb) __attribute__((always_inline)) -> uint32_t {
+        return k_lane + stage_off(tile, C::kKTile * 2) + uint32_t(kb * 32 * 16);
+    };
+
+    // ---- QK of a uniform tile: chunk CF with the boundary operand qb, then the
+    // whole chunks above it (for the window off: CF = 0, qb = qf[0])
+    auto qk_uniform = [&](int tile, auto cf_tag) __attribute__((always_inline)) {
+        constexpr int CF = decltype(cf_tag)::value;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const uint32_t kr = k_block(tile, kb);
+            u32x4_t kf[C::kChunks];
+#pragma unroll
+            for (int c = CF; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 1024u * c);
+            f32x16_t acc = mfma(kf[CF], qb, zero16());
+#pragma unroll
+            for (int c = CF + 1; c < C::kChunks; ++c) acc = mfma(kf[c], qf[c], acc);
+            sacc[kb] = acc;
+        }
+    };
+
+    // ---- QK of any tile (general path), per 32-key block
+    auto qk_general = [&](int tile) __attribute__((always_inline)) {
+        const int j0 = tile * kBN;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            const int jb = j0 + 32 * kb;
+            const uint32_t kr = k_block(tile, kb);
+            u32x4_t kf[C::kChunks];
+#pragma unroll
+            for (int c = 0; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 1024u * c);
+            const int zhi = wp_max - jb;
+            const int zlo = max(0, wp_min - (jb + 31));
+            // all pairs classified at once: lane r holds W_r; bit r of `full` = pair r
+            // kept in every cell of the block, of `keep` = kept in some cell
+            const uint64_t full = __ballot(my_w >= zhi);
+            const uint64_t keep = __ballot(my_w >= zlo);
+            // lowest frequencies (largest windows) first: the first MFMA always runs
+            // (pairs no cell keeps zeroed) and starts from a zero accumulator
+            f32x16_t acc;
+#pragma unroll
+            for (int c = C::kChunks - 1; c >= 0; --c) {
+                const uint32_t fc = uint32_t(full >> (8 * c)) & 0xFFu;
+                if (c == C::kChunks - 1) {
+                    acc = mfma(kf[c], keep_pairs(qf[c], fc), zero16());
+                } else if (fc) {
+                    u32x4_t q = qf[c];
+                    if (fc != 0xFFu) q = keep_pairs(q, fc);
+                    acc = mfma(kf[c], q, acc);
+                }
+            }
+            // pairs whose window ends inside the block: one MFMA each, added where
+            // z <= W_r (register v holds distance zbase - off(v): keep iff off(v) >= thr)
+            uint64_t part = keep & ~full;
+            while (part) {
+                const int r = __builtin_ctzll(part);
+                part &= part - 1;
+                const int c = r >> 3;
+                u32x4_t qc = qf[0];
+#pragma unroll
+                for (int cc = 1; cc < C::kChunks; ++cc)
+                    if (cc == c) qc = qf[cc];
+                const f32x16_t pr =
+                    mfma(lds_read_b128(kr + 1024u * c), keep_pairs(qc, 1u << (r & 7)), zero16());
+                const int thr = my_pos - jb - 4 * hh - p.win.W[r];
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = 8 * (v / 4) + (v % 4);
+                    acc[v] += off >= thr ? pr[v] : 0.f;
+                }
+            }
+            sacc[kb] = acc;
+        }
+    };
+
+    // ---- causal mask and key bound (only tiles that reach the diagonal or n_k),
+    // then the online softmax over the tile (lane = query row; the two lane halves
+    // hold disjoint keys), then PV.  One rescale check per tile; the exponentials
+    // are branch-free.
+    auto softmax_pv = [&](int tile) __attribute__((always_inline)) {
+        const int j0 = tile * kBN;
+        if (wp_min - (j0 + kBN - 1) < 0 || j0 + kBN > p.n_k) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb) {
+                const int jb = j0 + 32 * kb;
+                const int kbound = p.n_k - jb - 4 * hh;
+                const int zbase = my_pos - jb - 4 * hh;
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int off = 8 * (v / 4) + (v % 4);
+                    if (off > zbase || off >= kbound) sacc[kb][v] = -INFINITY;
+                }
+            }
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float cand = mx * sc;
+        if (__any(cand > m_run + kRescale)) {
+            const float m_new = fmaxf(m_run, cand);
+            const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
+            m_run = m_new;
+            l_run *= alpha;
+#pragma unroll
+            for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        const uint32_t vb = v_lane + stage_off(tile, C::kVTile * 2);
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            u32x4_t pb[2];
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float a = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t], sc, -m_use));
+                    const float c2 = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t + 1], sc, -m_use));
+                    l_run += a;
+                    l_run += c2;
+                    bf16x2_t two;
+                    two[0] = (__bf16)a;
+                    two[1] = (__bf16)c2;
+                    pb[ks][t] = __builtin_bit_cast(uint32_t, two);
+                }
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                for (int i = 0; i < D / 32; ++i) {
+                    const uint32_t o = uint32_t(((32 * kb + 16 * ks) * C::kVStride + 32 * i) * 2);
+                    const s16x4_t lo = lds_read_tr(vb + o);
+                    const s16x4_t hi = lds_read_tr(vb + o + 8 * C::kVStride * 2);
+                    const s16x8_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+                    oacc[i] = mfma(__builtin_bit_cast(u32x4_t, both), pb[ks], oacc[i]);
+                }
+        }
+    };
+
+    const int n_tiles = (key_end + kBN - 1) / kBN;
+    auto active = [&](int tile) __attribute__((always_inline)) { return wave_active && wp_max >= tile * kBN; };
+    // one tile: stage the next, compute this one (if the wave has rows there),
+    // await this wave's loads of the next tile, barrier
+    auto run_tile = [&](int u, auto&& qk) __attribute__((always_inline)) {
+        if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % kStages);
+        if (active(u)) {
+            qk(u);
+            softmax_pv(u);
+        }
+        vm_wait();
+        barrier();
+    };
 
     issue(0, 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    vm_wait();
+    barrier();
 
-    int buf = 0;
-    for (int j0 = 0; j0 < key_end; j0 += kBN, buf ^= 1) {
-        const bool has_next = j0 + kBN < key_end;
-        if (has_next) issue(j0 + kBN, buf ^ 1);
-
-        if (wave_active && wp_max >= j0) {
-            const uint16_t* Kb = Ks[buf];
-            const uint16_t* Vb = Vs[buf];
-            // ---- QK for both 32-key blocks of the tile (the matrix phase; the window's
-            // branches live here).  Block 0 always has a causal key; block 1 may not.
-            const bool live1 = wp_max >= j0 + 32 && j0 + 32 < p.n_k;
-            f32x16_t sacc[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                if (kb == 1 && !live1) {
-                    sacc[1] = zero16();  // masked below
-                    continue;
-                }
-                const int jb = j0 + 32 * kb;
-                const int zhi = wp_max - jb;
-                const int zlo = max(0, wp_min - (jb + 31));
-                // every K fragment of the block is read before any branch so that the
-                // reads overlap; a chunk the block does not keep is never multiplied
-                const uint16_t* krow = Kb + k_off[kb];
-                u32x4_t kf[C::kChunks];
-#pragma unroll
-                for (int c = 0; c < C::kChunks; ++c)
-                    kf[c] = *reinterpret_cast<const u32x4_t*>(krow + 8 * c);
-                f32x16_t acc;
-                if (!kWin) {
-                    acc = mfma(kf[C::kChunks - 1], qf[C::kChunks - 1], zero16());
-#pragma unroll
-                    for (int c = C::kChunks - 2; c >= 0; --c) acc = mfma(kf[c], qf[c], acc);
-                } else {
-                    // all pairs classified at once: lane r holds W_r; bit r of `full` = pair r
-                    // kept in every cell of the block, of `keep` = kept in some cell
-                    const uint64_t full = __ballot(my_w >= zhi);
-                    const uint64_t keep = __ballot(my_w >= zlo);
-                    // lowest frequencies (largest windows) first: the first MFMA always runs
-                    // (pairs no cell keeps zeroed) and starts from a zero accumulator.  Each
-                    // chunk has one MFMA site, so the scores are updated in place.
-#pragma unroll
-                    for (int c = C::kChunks - 1; c >= 0; --c) {
-                        const uint32_t fc = uint32_t(full >> (8 * c)) & 0xFFu;
-                        if (c == C::kChunks - 1) {
-                            acc = mfma(kf[c], keep_pairs(qf[c], fc), zero16());
-                        } else if (fc) {
-                            u32x4_t qb = qf[c];
-                            if (fc != 0xFFu) qb = keep_pairs(qb, fc);
-                            acc = mfma(kf[c], qb, acc);
-                        }
+    if constexpr (!kWin) {
+        // window off: every tile is the full contraction
+        qb = qf[0];
+        for (int u = 0; u < n_tiles; ++u)
+            run_tile(u, [&](int t) __attribute__((always_inline)) {
+                qk_uniform(t, std::integral_constant<int, 0>{});
+            });
+    } else {
+    // Each wave walks the tiles in runs; every tile ends with one barrier on every
+    // wave, whichever loop runs it.
+    constexpr int kGeneral = 64;  // mode of a general-path tile (chunk counts are 0..7)
+    int u = 0;
+    while (u < n_tiles) {
+        int mode, seg_end;
+        if (!active(u)) {
+            mode = -1;  // the wave's rows all precede this tile and every later one
+            seg_end = n_tiles;
+        } else {
+            mode = kGeneral;
+            seg_end = u + 1;
+            if (p.mono) {
+                const int zhi = wp_max - u * kBN;                      // largest distance of the tile
+                const int zlo = max(0, wp_min - (u * kBN + kBN - 1));  // smallest
+                const uint64_t full = __ballot(my_w >= zhi);
+                const uint64_t keep = __ballot(my_w >= zlo);
+                if (full == keep) {
+                    // uniform: kept pairs r >= rf (non-empty: the last chunk is kept at
+                    // every distance of the call).  The run lasts while the next
+                    // threshold below, W[rf - 1], stays under the tile's smallest
+                    // distance: wp_min - 64 u' - 63 > W[rf - 1].
+                    const int rf = __builtin_ctzll(full);
+                    seg_end = n_tiles;
+                    if (rf > 0) {
+                        const int wlow = p.win.W[rf - 1];
+                        const int64_t lim = (int64_t(wp_min) - kBN - wlow) / kBN + 1;
+                        seg_end = int(max(int64_t(u) + 1, min(lim, int64_t(n_tiles))));
                     }
-                    // pairs whose window ends inside the block: one MFMA each, added where
-                    // z <= W_r (register v holds distance zbase - off(v): keep iff off(v) >= thr)
-                    uint64_t part = keep & ~full;
-                    while (part) {
-                        const int r = __builtin_ctzll(part);
-                        part &= part - 1;
-                        const int c = r >> 3;
-                        u32x4_t kfc = kf[0], qfc = qf[0];
+                    mode = rf >> 3;
+                    if (rf != qb_rf) {
+                        qb_rf = rf;
+                        u32x4_t qs = qf[0];
 #pragma unroll
                         for (int cc = 1; cc < C::kChunks; ++cc)
-                            if (cc == c) {
-                                kfc = kf[cc];
-                                qfc = qf[cc];
-                            }
-                        const f32x16_t t = mfma(kfc, keep_pairs(qfc, 1u << (r & 7)), zero16());
-                        const int thr = my_pos - jb - 4 * hh - p.win.W[r];
-#pragma unroll
-                        for (int v = 0; v < 16; ++v) {
-                            const int off = 8 * (v / 4) + (v % 4);
-                            acc[v] += off >= thr ? t[v] : 0.f;
-                        }
-                    }
-                }
-                sacc[kb] = acc;
-            }
-            // ---- causal mask and key bound, only in tiles that reach the diagonal or n_k
-            if (wp_min - (j0 + kBN - 1) < 0 || j0 + kBN > p.n_k) {
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb) {
-                    const int jb = j0 + 32 * kb;
-                    const int kbound = p.n_k - jb - 4 * hh;
-                    const int zbase = my_pos - jb - 4 * hh;
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int off = 8 * (v / 4) + (v % 4);
-                        if (off > zbase || off >= kbound) sacc[kb][v] = -INFINITY;
-                    }
-                }
-            }
-            // ---- online softmax over the tile (lane = query row; the two lane halves
-            // hold disjoint keys).  One rescale check per tile; below it the softmax and
-            // the PV products of both blocks are branch-free, so the PV matrix work of
-            // block 0 overlaps the exponentials of block 1.
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float cand = mx * sc;
-            if (__any(cand > m_run + kRescale)) {
-                const float m_new = fmaxf(m_run, cand);
-                const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
-                m_run = m_new;
-                l_run *= alpha;
-#pragma unroll
-                for (int i = 0; i < D / 32; ++i)
-#pragma unroll
-                    for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
-            }
-            const float m_use = m_run == -INFINITY ? 0.f : m_run;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                u32x4_t pb[2];
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const float a = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t], sc, -m_use));
-                        const float c2 = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t + 1], sc, -m_use));
-                        l_run += a;
-                        l_run += c2;
-                        bf16x2_t two;
-                        two[0] = (__bf16)a;
-                        two[1] = (__bf16)c2;
-                        pb[ks][t] = __builtin_bit_cast(uint32_t, two);
-                    }
-                }
-                // PV: V^T fragments by transposed LDS reads.  Lane group of 16: key rows
-                // 4 * hh + (l % 16) / 4 (8 rows further for elements 4..7), dims
-                // 16 * ((l / 16) % 2) + 4 * (l % 4) of each 32-dim block.
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const uint16_t* vp = Vb + (32 * kb + 16 * ks + v_row) * C::kVStride + v_dsub;
-#pragma unroll
-                    for (int i = 0; i < D / 32; ++i) {
-                        const s16x4_t lo = lds_read_tr(vp + 32 * i);
-                        const s16x4_t hi = lds_read_tr(vp + 8 * C::kVStride + 32 * i);
-                        const s16x8_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                        oacc[i] = mfma(__builtin_bit_cast(u32x4_t, both), pb[ks], oacc[i]);
+                            if (cc == (rf >> 3)) qs = qf[cc];
+                        qb = keep_pairs(qs, (0xFFu << (rf & 7)) & 0xFFu);
                     }
                 }
             }
         }
-
-        __builtin_amdgcn_s_waitcnt(0);  // this thread's loads of the next tile have landed
-        __syncthreads();
+        switch (mode) {
+#define ATF_UNIFORM_RUN(CFV)                                                                    \
+    case CFV:                                                                                   \
+        if constexpr (CFV < C::kChunks) {                                                       \
+            for (; u < seg_end; ++u)                                                            \
+                run_tile(u, [&](int t) __attribute__((always_inline)) { qk_uniform(t, std::integral_constant<int, CFV>{}); }); \
+        } else { /* not reached: rf < d/2 - 8 */                                                \
+            run_tile(u, [&](int t) __attribute__((always_inline)) { qk_general(t); });                                         \
+            ++u;                                                                                \
+        }                                                                                       \
+        break;
+            ATF_UNIFORM_RUN(0)
+            ATF_UNIFORM_RUN(1)
+            ATF_UNIFORM_RUN(2)
+            ATF_UNIFORM_RUN(3)
+            ATF_UNIFORM_RUN(4)
+            ATF_UNIFORM_RUN(5)
+            ATF_UNIFORM_RUN(6)
+            ATF_UNIFORM_RUN(7)
+#undef ATF_UNIFORM_RUN
+            case kGeneral:
+                run_tile(u, [&](int t) __attribute__((always_inline)) { qk_general(t); });
+                ++u;
+                break;
+            default:  // idle: keep the barrier count
+                for (; u < seg_end; ++u) {
+                    if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % kStages);
+                    vm_wait();
+                    barrier();
+                }
+                break;
+        }
+    }
     }
 
     if (!wave_active) return;
@@ -454,11 +576,17 @@ hipError_t launch_prefill(const PrefillParams& p_in, int head_dim, hipStream_t s
     p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
     const int64_t blocks = int64_t(p.n_qtiles) * p.h_kv * p.batch;
     if (blocks <= 0 || blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-    // the window is off when no threshold is below the largest possible distance
+    // the window is off when no threshold is below the largest possible distance;
+    // the uniform-run path needs thresholds non-decreasing in r and the last chunk
+    // kept at every distance of the call
     const int64_t max_dist = int64_t(p.q_pos0) + p.n_q - 1;
     bool window_on = false;
     for (int r = 0; r < head_dim / 2; ++r)
         if (int64_t(p.win.W[r]) < max_dist) window_on = true;
+    bool mono = int64_t(p.win.W[head_dim / 2 - kChunkPairs]) >= max_dist;
+    for (int r = 1; r < head_dim / 2; ++r)
+        if (p.win.W[r] < p.win.W[r - 1]) mono = false;
+    p.mono = mono ? 1 : 0;
     (void)hipGetLastError();
     return head_dim == 64 ? launch_d<64>(p, unsigned(blocks), window_on, stream)
                           : launch_d<128>(p, unsigned(blocks), window_on, stream);
