@@ -75,7 +75,10 @@ def profile_driver(name, iters, kinf):
     if wl.kind == "prefill":
         o = torch.empty_like(inp["q"])
         lse = torch.empty((wl.batch, wl.h_q, wl.n_q), dtype=torch.float32, device=dev)
-        run = lambda: atf.atf_prefill(inp["q"], inp["k"], inp["v"], o, lse, wl.q_pos0, win,
+        kp = torch.empty(atf.kcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_kcache(inp["k"], kp)
+        run = lambda: atf.atf_prefill(inp["q"], kp, inp["v"], o, lse, wl.q_pos0, win,
                                       stream=stream)
     else:
         kp = torch.empty((wl.batch, wl.h_kv, d // 16, wl.n_k, 16), dtype=torch.bfloat16,
@@ -171,7 +174,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     def prefill(w):
-        atf.atf_prefill(q, k, v, o, lse, pf.q_pos0, w, stream=stream)
+        atf.atf_prefill(q, kp, v, o, lse, pf.q_pos0, w, stream=stream)
 
     def decode(w):
         atf.atf_decode(qd, kp, vp, od, lsed, dc.q_pos0, w, ws, stream=stream)

@@ -83,20 +83,27 @@ int atf_count_terms(const atf_window *w, int64_t n_q, int64_t q_pos0, int64_t n_
  * against n_k keys, tiled with an online softmax; the window is applied as a
  * per-tile slice of the QK contraction axis (Sec. 3.3): fully kept pair-chunks
  * are MFMA K-steps, fully pruned ones are neither loaded nor multiplied, and
- * pairs whose window ends inside the tile are masked per element.
- *   q   bf16 [batch][n_q][h_q][d]   rotated queries          (device, read)
- *   k   bf16 [batch][n_k][h_kv][d]  rotated keys             (device, read)
- *   v   bf16 [batch][n_k][h_kv][d]  values                   (device, read)
- *   o   bf16 [batch][n_q][h_q][d]   output, O/l rounded to nearest even (device, written)
- *   lse fp32 [batch][h_q][n_q]      natural-log sum of exp of the scaled scores (device, written)
+ * pairs whose window ends inside the tile are masked per element.  The keys are
+ * read from the pair-chunk-major K cache (the layout decode reads, produced by
+ * atf_pack_kcache), so a pruned chunk of a key is never read from HBM.
+ *   q        bf16 [batch][n_q][h_q][d]        rotated queries            (device, read)
+ *   k_cache  bf16 [batch][h_kv][d/16][cache_tokens][16]  rotated keys, pair-chunk-major,
+ *            see atf_pack_kcache; keys 0 .. n_k - 1 are read          (device, read)
+ *   v        bf16 [batch][cache_tokens][h_kv][d]  values; rows 0 .. n_k - 1 read (device, read)
+ *   o        bf16 [batch][n_q][h_q][d]        output, O/l rounded to nearest even (device, written)
+ *   lse      fp32 [batch][h_q][n_q]           natural-log sum of exp of the scaled scores (device, written)
+ * cache_tokens is the number of tokens each batch entry of the caches is
+ * allocated for (0 means n_k); a chunk of a longer prefill passes the positions of
+ * its rows (q_pos0) and the keys written so far (n_k) against the same caches.
  * Query head h uses key/value head h / (h_q / h_kv).  softmax_scale <= 0 selects
  * 1/sqrt(d).  n_q == 0 is a no-op.
  * Errors: ATF_EINVAL (NULL/misaligned pointer, batch < 1, n_q < 0, n_k < 1,
- * q_pos0 < 0, q_pos0 + n_q > 2^31 - 1, n_k > 2^31 - 1, h_q % h_kv != 0, bad window,
- * non-finite scale); ATF_EUNSUPPORTED (d not 64 or 128); ATF_EHIP. */
-int atf_prefill(const void *q, const void *k, const void *v, void *o, float *lse,
+ * q_pos0 < 0, q_pos0 + n_q > 2^31 - 1, n_k > 2^31 - 1, cache_tokens < n_k (when
+ * non-zero) or > 2^31 - 1, h_q % h_kv != 0, bad window, non-finite scale);
+ * ATF_EUNSUPPORTED (d not 64 or 128); ATF_EHIP. */
+int atf_prefill(const void *q, const void *k_cache, const void *v, void *o, float *lse,
                 int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
-                int32_t h_q, int32_t h_kv, const atf_window *w,
+                int32_t h_q, int32_t h_kv, int64_t cache_tokens, const atf_window *w,
                 float softmax_scale, void *hip_stream);
 
 /* Pair-chunk width C_p (rotary pairs per chunk) of the decode K cache.  One
@@ -140,21 +147,26 @@ size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int6
  * output) states that a second kernel merges (split-KV, Sec. 5).  For pair-chunk
  * c only the token suffix whose distance is within the chunk's largest window
  * is read; pairs whose window ends inside that suffix are masked per token.
- *   q        bf16 [batch][h_q][d]                        (device, read)
- *   k_cache  bf16 pair-chunk-major, see atf_pack_kcache   (device, read)
- *   v_cache  bf16 packed 16-token blocks, see atf_pack_vcache (device, read)
- *   o        bf16 [batch][h_q][d]                         (device, written)
- *   lse      fp32 [batch][h_q]                            (device, written)
+ *   q        bf16 [batch][h_q][d]                                   (device, read)
+ *   k_cache  bf16 [batch][h_kv][d/16][cache_tokens][16] pair-chunk-major,
+ *            see atf_pack_kcache                                     (device, read)
+ *   v_cache  bf16 [batch][h_kv][ceil(cache_tokens/16)][d][16] packed 16-token
+ *            blocks, see atf_pack_vcache                             (device, read)
+ *   o        bf16 [batch][h_q][d]                                   (device, written)
+ *   lse      fp32 [batch][h_q]                                      (device, written)
  *   workspace: device, >= atf_decode_workspace_bytes(batch, h_q, h_kv, n_k, d)
  *              bytes, 16-byte aligned, caller-owned; contents are scratch.
- * Errors: ATF_EINVAL (pointers, sizes, q_pos < 0, q_pos > 2^31 - 2, bad window or
- * scale), ATF_EUNSUPPORTED (d not 64/128), ATF_EWORKSPACE, ATF_EHIP.
+ * cache_tokens is the number of tokens each batch entry of the caches is
+ * allocated for (0 means n_k); only tokens below n_k are read.
+ * Errors: ATF_EINVAL (pointers, sizes, q_pos < 0, q_pos > 2^31 - 2, cache_tokens
+ * < n_k when non-zero, bad window or scale), ATF_EUNSUPPORTED (d not 64/128),
+ * ATF_EWORKSPACE, ATF_EHIP.
  * The query heads of one KV head are the columns of the matrix instructions
  * (up to 32 per workgroup; larger groups are split over workgroups by their
  * largest divisor <= 32).  Deterministic: equal inputs give equal bits. */
 int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o, float *lse,
                int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
-               const atf_window *w, float softmax_scale,
+               int64_t cache_tokens, const atf_window *w, float softmax_scale,
                void *workspace, size_t workspace_bytes, void *hip_stream);
 
 /* Message of the most recent failed call on this thread ("" if none). */

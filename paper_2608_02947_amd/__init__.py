@@ -56,13 +56,13 @@ def _load():
     sig = {
         "atf_window_table": (ctypes.c_int, [W, P]),
         "atf_count_terms": (ctypes.c_int, [W, i64, i64, i64, P, P]),
-        "atf_prefill": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, W, f32, P]),
+        "atf_prefill": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64, W, f32, P]),
         "atf_kcache_chunk_pairs": (ctypes.c_int32, [i32]),
         "atf_pack_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
         "atf_vcache_bytes": (ctypes.c_size_t, [i32, i64, i32, i32]),
         "atf_pack_vcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
         "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
-        "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, W, f32, P,
+        "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, f32, P,
                                       ctypes.c_size_t, P]),
         "atf_last_error": (ctypes.c_char_p, []),
     }
@@ -162,25 +162,36 @@ def _stream_ptr(stream):
     return s.cuda_stream
 
 
-def atf_prefill(q, k, v, o, lse, q_pos0: int, window: Window, softmax_scale: float = 0.0,
-                stream=None):
-    """q [B, n_q, h_q, d], k/v [B, n_k, h_kv, d], o like q (bf16); lse [B, h_q, n_q] fp32."""
+def kcache_shape(batch: int, cache_tokens: int, h_kv: int, head_dim: int):
+    """Shape of the pair-chunk-major K cache: [B, h_kv, d/16, cache_tokens, 16]."""
+    return (batch, h_kv, head_dim // 16, cache_tokens, 16)
+
+
+def atf_prefill(q, k_cache, v, o, lse, q_pos0: int, window: Window, softmax_scale: float = 0.0,
+                stream=None, n_k: Optional[int] = None):
+    """q [B, n_q, h_q, d] bf16; k_cache [B, h_kv, d/16, C, 16] pair-chunk-major (see
+    atf_pack_kcache); v [B, C, h_kv, d]; o like q; lse [B, h_q, n_q] fp32.  C is the
+    caches' token capacity; keys 0 .. n_k - 1 are used (n_k defaults to C)."""
     torch = _torch()
     B, n_q, h_q, d = q.shape
-    _, n_k, h_kv, _ = k.shape
-    if tuple(v.shape) != tuple(k.shape) or tuple(o.shape) != tuple(q.shape) or \
-            tuple(lse.shape) != (B, h_q, n_q) or k.shape[0] != B or k.shape[3] != d:
+    if k_cache.dim() != 5:
+        raise ValueError("atf_prefill: k_cache must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_cache.shape
+    n_k = cap if n_k is None else int(n_k)
+    if tuple(k_cache.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v.shape) != (B, cap, h_kv, d) or tuple(o.shape) != tuple(q.shape) or \
+            tuple(lse.shape) != (B, h_q, n_q):
         raise ValueError("atf_prefill: inconsistent shapes")
     cw, keep = window.as_c()
-    rc = _lib.atf_prefill(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k, torch.bfloat16, "k"),
+    rc = _lib.atf_prefill(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_cache, torch.bfloat16, "k"),
                           _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
                           _dev_ptr(lse, torch.float32, "lse"), B, n_q, n_k, q_pos0, h_q, h_kv,
-                          ctypes.byref(cw), float(softmax_scale), _stream_ptr(stream))
+                          cap, ctypes.byref(cw), float(softmax_scale), _stream_ptr(stream))
     _check(rc)
 
 
 def atf_pack_kcache(k_bshd, k_pcm, stream=None):
-    """k_bshd [B, n_k, h_kv, d] -> k_pcm [B, h_kv, d/16, n_k, 16] (bf16)."""
+    """k_bshd [B, C, h_kv, d] -> k_pcm [B, h_kv, d/16, C, 16] (bf16)."""
     torch = _torch()
     B, n_k, h_kv, d = k_bshd.shape
     if k_pcm.numel() != k_bshd.numel():
@@ -211,23 +222,25 @@ def atf_pack_vcache(v_bshd, v_pack, stream=None):
 
 
 def atf_decode(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window, workspace,
-               softmax_scale: float = 0.0, stream=None):
-    """q [B, h_q, d]; k_pcm [B, h_kv, d/16, n_k, 16]; v_pack [B, h_kv, ceil(n_k/16), d, 16];
+               softmax_scale: float = 0.0, stream=None, n_k: Optional[int] = None):
+    """q [B, h_q, d]; k_pcm [B, h_kv, d/16, C, 16]; v_pack [B, h_kv, ceil(C/16), d, 16];
     o [B, h_q, d]; lse [B, h_q]; workspace: uint8 device tensor of
-    atf_decode_workspace_bytes()."""
+    atf_decode_workspace_bytes().  C is the caches' token capacity; keys
+    0 .. n_k - 1 are used (n_k defaults to C)."""
     torch = _torch()
     B, h_q, d = q.shape
     if k_pcm.dim() != 5:
-        raise ValueError("atf_decode: k_pcm must be [B, h_kv, d/16, n_k, 16]")
-    _, h_kv, _, n_k, _ = k_pcm.shape
+        raise ValueError("atf_decode: k_pcm must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_pcm.shape
+    n_k = cap if n_k is None else int(n_k)
     if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
-            tuple(k_pcm.shape) != (B, h_kv, d // 16, n_k, 16) or \
-            tuple(v_pack.shape) != vcache_shape(B, n_k, h_kv, d):
+            tuple(k_pcm.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_pack.shape) != vcache_shape(B, cap, h_kv, d):
         raise ValueError("atf_decode: inconsistent shapes")
     cw, keep = window.as_c()
     rc = _lib.atf_decode(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pcm, torch.bfloat16, "k"),
                          _dev_ptr(v_pack, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
-                         _dev_ptr(lse, torch.float32, "lse"), B, n_k, q_pos, h_q, h_kv,
+                         _dev_ptr(lse, torch.float32, "lse"), B, n_k, q_pos, h_q, h_kv, cap,
                          ctypes.byref(cw), float(softmax_scale),
                          _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
                          _stream_ptr(stream))

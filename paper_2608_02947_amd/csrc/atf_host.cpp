@@ -188,7 +188,8 @@ int32_t atf_kcache_chunk_pairs(int32_t head_dim) {
 
 int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse,
                 int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
-                int32_t h_kv, const atf_window* w, float softmax_scale, void* hip_stream) {
+                int32_t h_kv, int64_t cache_tokens, const atf_window* w, float softmax_scale,
+                void* hip_stream) {
     if (w == nullptr) return fail(ATF_EINVAL, "prefill: NULL window");
     const int d = w->head_dim;
     if (d != 64 && d != 128)
@@ -202,6 +203,10 @@ int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse
         return fail(ATF_EUNSUPPORTED, "prefill: GQA ratio %d above 256 not built", h_q / h_kv);
     if (q_pos0 + n_q > kPosLimit || n_k > kPosLimit)
         return fail(ATF_EINVAL, "prefill: positions must stay below 2^31 - 1");
+    if (cache_tokens == 0) cache_tokens = n_k;
+    if (cache_tokens < n_k || cache_tokens > kPosLimit)
+        return fail(ATF_EINVAL, "prefill: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1",
+                    (long long)cache_tokens, (long long)n_k);
     if (!std::isfinite(softmax_scale))
         return fail(ATF_EINVAL, "prefill: softmax_scale must be finite");
     atf::PrefillParams p{};
@@ -221,6 +226,7 @@ int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse
     p.batch = batch;
     p.n_q = static_cast<int32_t>(n_q);
     p.n_k = static_cast<int32_t>(n_k);
+    p.cache_tokens = static_cast<int32_t>(cache_tokens);
     p.q_pos0 = static_cast<int32_t>(q_pos0);
     p.h_q = h_q;
     p.h_kv = h_kv;
@@ -314,7 +320,7 @@ size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int6
 
 int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
-               const atf_window* w, float softmax_scale, void* workspace,
+               int64_t cache_tokens, const atf_window* w, float softmax_scale, void* workspace,
                size_t workspace_bytes, void* hip_stream) {
     if (w == nullptr) return fail(ATF_EINVAL, "decode: NULL window");
     const int d = w->head_dim;
@@ -326,6 +332,10 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
         return fail(ATF_EINVAL, "decode: h_q %d not a multiple of h_kv %d", h_q, h_kv);
     if (q_pos >= kPosLimit || n_k > kPosLimit)
         return fail(ATF_EINVAL, "decode: positions must stay below 2^31 - 1");
+    if (cache_tokens == 0) cache_tokens = n_k;
+    if (cache_tokens < n_k || cache_tokens > kPosLimit)
+        return fail(ATF_EINVAL, "decode: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1",
+                    (long long)cache_tokens, (long long)n_k);
     if (!std::isfinite(softmax_scale))
         return fail(ATF_EINVAL, "decode: softmax_scale must be finite");
     atf::DecodeParams p{};
@@ -361,6 +371,7 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
     p.ws_o = reinterpret_cast<float*>(ws + L.off_o);
     p.batch = batch;
     p.n_k = static_cast<int32_t>(n_k);
+    p.cache_tokens = static_cast<int32_t>(cache_tokens);
     p.q_pos = static_cast<int32_t>(q_pos);
     p.h_q = h_q;
     p.h_kv = h_kv;

@@ -23,11 +23,12 @@ struct WindowTable {
 
 struct PrefillParams {
     const uint16_t* q;   // [B][n_q][h_q][d]
-    const uint16_t* k;   // [B][n_k][h_kv][d]
-    const uint16_t* v;   // [B][n_k][h_kv][d]
+    const uint16_t* k;   // [B][h_kv][d/16][cache_tokens][16] (pair-chunk-major)
+    const uint16_t* v;   // [B][cache_tokens][h_kv][d]
     uint16_t* o;         // [B][n_q][h_q][d]
     float* lse;          // [B][h_q][n_q]
     int32_t batch, n_q, n_k, q_pos0, h_q, h_kv, group;
+    int32_t cache_tokens;  // tokens each cache entry is allocated for (>= n_k)
     int32_t pos_per_tile;  // query positions per workgroup (rows = positions x group)
     int32_t n_qtiles;
     int32_t mono;        // thresholds non-decreasing and the last chunk kept at every distance
@@ -37,14 +38,15 @@ struct PrefillParams {
 
 struct DecodeParams {
     const uint16_t* q;       // [B][h_q][d]
-    const uint16_t* kpcm;    // [B][h_kv][d/16][n_k][16]
-    const uint16_t* vpk;     // [B][h_kv][ceil(n_k/16)][d][16] (see atf_pack_vcache)
+    const uint16_t* kpcm;    // [B][h_kv][d/16][cache_tokens][16]
+    const uint16_t* vpk;     // [B][h_kv][ceil(cache_tokens/16)][d][16] (see atf_pack_vcache)
     uint16_t* o;             // [B][h_q][d]
     float* lse;              // [B][h_q]
     float* ws_m;             // [B][h_q][splits]   running max (log2 domain)
     float* ws_l;             // [B][h_q][splits]   normaliser
     float* ws_o;             // [B][h_q][splits][d] unnormalised output
     int32_t batch, n_k, q_pos, h_q, h_kv, group;
+    int32_t cache_tokens;     // tokens each cache entry is allocated for (>= n_k)
     int32_t heads_per_block;  // query heads handled by one workgroup (divides group, <= 32)
     int32_t n_valid;          // keys 0 .. n_valid - 1 are causal
     int32_t splits;

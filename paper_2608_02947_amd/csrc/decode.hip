@@ -91,10 +91,9 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 
     const int t_begin = split * p.split_tokens;
     const int t_end = min(p.n_valid, t_begin + p.split_tokens);
-    const int nblk16 = (p.n_k + 15) / 16;
-
-    const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * int64_t(p.n_k) * 16;
-    const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * int64_t(nblk16) * D * 16;
+    const int64_t cap = p.cache_tokens;  // stream length of the caches
+    const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * cap * 16;
+    const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * ((cap + 15) / 16) * D * 16;
     const int my_w = lane < kHalf ? p.win.W[lane] : -1;
 
     // query fragments (B operand): head column `col`, dims of half hh of every chunk
@@ -133,10 +132,13 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             u32x4_t z = {0u, 0u, 0u, 0u};
             const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
             if (kept && tok_ok)
-                z = *reinterpret_cast<const u32x4_t*>(kstream + (int64_t(c) * p.n_k + tok) * 16 + 8 * hh);
+                z = *reinterpret_cast<const u32x4_t*>(kstream + (int64_t(c) * cap + tok) * 16 + 8 * hh);
             kf[c] = z;
         }
-        // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each 16-token group)
+        // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each
+        // 16-token group).  Blocks past n_k are not read; in the block holding
+        // token n_k the slots of later tokens are zeroed (the cache past n_k need
+        // not hold finite values, and their probabilities are 0).
         u32x4_t vf[2][kDB];
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
@@ -144,9 +146,21 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 #pragma unroll
             for (int i = 0; i < kDB; ++i) {
                 u32x4_t z = {0u, 0u, 0u, 0u};
-                if (blk < nblk16)
+                if (16 * blk < p.n_k)
                     z = *reinterpret_cast<const u32x4_t*>(vblocks + (int64_t(blk) * D + 32 * i + col) * 16 + 8 * hh);
                 vf[ks][i] = z;
+            }
+            if (16 * blk < p.n_k && 16 * blk + 16 > p.n_k) {
+                const int lim = p.n_k - 16 * blk - 4 * hh;  // slot e valid iff 8(e/4) + e%4 < lim
+#pragma unroll
+                for (int i = 0; i < kDB; ++i)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const int e0 = 2 * t, e1 = 2 * t + 1;
+                        const uint32_t m = (8 * (e0 / 4) + e0 % 4 < lim ? 0x0000FFFFu : 0u) |
+                                           (8 * (e1 / 4) + e1 % 4 < lim ? 0xFFFF0000u : 0u);
+                        vf[ks][i][t] &= m;
+                    }
             }
         }
 

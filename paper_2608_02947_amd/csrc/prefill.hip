@@ -11,11 +11,15 @@
 //   (global memory straight into LDS, no register staging) one tile ahead of the
 //   compute.
 //
-// LDS layout: the K tile is segment-major, [16-byte segment s][key][8 bf16], so
-// one wave-wide direct load fills one segment for all 64 keys, and a chunk (two
-// segments, below) is loaded or skipped by one wave-uniform branch.  The V tile
-// is row-major [key][d] with rows padded to d + 32 bf16 so that the transposed
-// reads (4 rows x 32 bytes per 16 lanes) hit distinct banks.
+// K comes from the pair-chunk-major cache (the decode layout): chunk c of a KV
+// head is a stream of 32 bytes per key (dims [8c, 8c+8) then [d/2+8c, d/2+8c+8)),
+// so one wave-wide direct load fetches one chunk of 32 keys as 1 KB of contiguous
+// memory, and a chunk that no cell of the tile keeps is skipped by one
+// wave-uniform branch -- its bytes are never read from HBM.  In LDS the K tile is
+// [chunk][32-key block][half][key][8 bf16]: a fragment read of 64 lanes covers
+// 1 KB without bank conflicts.  The V tile is row-major [key][d] with rows padded
+// to d + 32 bf16 so that the transposed reads (4 rows x 32 bytes per 16 lanes)
+// hit distinct banks.
 //
 // Matrix layout (v_mfma_f32_32x32x16_bf16, lane l, c = l % 32, h = l / 32)
 //   S^T[key][row] = K[key][dims] * Q^T[dims][row]: A = K fragment (key c, dims
@@ -81,15 +85,15 @@ template <int D>
 struct Cfg {
     static constexpr int kHalf = D / 2;
     static constexpr int kChunks = D / 16;
-    static constexpr int kSegs = D / 8;             // 16-byte segments per key row
-    static constexpr int kKTile = kSegs * kBN * 8;  // bf16; segment-major
+    static constexpr int kSegs = D / 8;             // 16-byte segments per V row
+    static constexpr int kKTile = kChunks * kBN * 16;  // bf16; [chunk][block][half][key][8]
     static constexpr int kVStride = D + 32;         // bf16 per V row in LDS
     static constexpr int kVSlots = kVStride / 8;
     static constexpr int kVTile = kBN * kVStride;
-    static constexpr int kKPerWave = kSegs / kWaves;  // K segments loaded per wave
+    static constexpr int kKPerWave = 2 * kChunks / kWaves;  // K (chunk, block) units per wave
     static constexpr int kVLoads = kVTile / 512;      // wave-wide 1 KB loads per V tile
     static constexpr int kVPer = (kVLoads + kWaves - 1) / kWaves;
-    static_assert(kSegs % kWaves == 0, "K segments must spread evenly over the waves");
+    static_assert((2 * kChunks) % kWaves == 0, "K units must spread evenly over the waves");
     static_assert(kVTile % 512 == 0, "V tile must be whole kilobytes");
 };
 
@@ -204,8 +208,12 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     const int my_w = lane < C::kHalf ? p.win.W[lane] : -1;
 
     const uint32_t row_bytes = uint32_t(p.h_kv) * D * 2;
-    const char* kbytes = reinterpret_cast<const char*>(p.k + (int64_t(b) * p.n_k * p.h_kv + g) * D);
-    const char* vbytes = reinterpret_cast<const char*>(p.v + (int64_t(b) * p.n_k * p.h_kv + g) * D);
+    // K: pair-chunk-major streams of cache_tokens keys, chunk c of this head =
+    // 32 bytes per key; V: rows of h_kv * d bf16
+    const int64_t chunk_bytes = int64_t(p.cache_tokens) * 32;
+    const char* kpcm = reinterpret_cast<const char*>(p.k) + (int64_t(b) * p.h_kv + g) * C::kChunks * chunk_bytes;
+    const uint32_t k_piece = uint32_t((lane & 31) * 32 + (lane >> 5) * 16);
+    const char* vbytes = reinterpret_cast<const char*>(p.v + (int64_t(b) * p.cache_tokens * p.h_kv + g) * D);
 
     // query fragments (B operand): row `col`, dims of half hh of every chunk
     u32x4_t qf[C::kChunks];
@@ -221,13 +229,15 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     }
 
     // ---- global -> LDS staging of the tile at key j0 into buffer `buf`.
-    // K: wave w loads segments w, w + 8, ... (for d = 128 exactly the two halves
-    // of chunk w), lane i = key i, skipped when no cell of the workgroup tile keeps
-    // the segment's chunk; the last chunk is always loaded because the QK of a
-    // block always multiplies it.  V: wave w issues the tile's wave-wide loads
-    // w, w + 8, ...; slot s = 64 * load + lane holds (row s / slots-per-row,
-    // segment s % slots-per-row), padding slots re-read segment 0.  In a tile that
-    // crosses n_k, rows past it re-read the last key (finite values; masked).
+    // K: the tile is 2 * kChunks units (chunk u / 2, 32-key block u % 2); wave w
+    // loads units w, w + 8, ...: lane i reads 16 bytes of key i % 32, half i / 32,
+    // so the wave's 1 KB of global memory is contiguous.  A unit whose chunk no
+    // cell of the workgroup tile keeps is skipped; the last chunk is always loaded
+    // because the QK of a block always multiplies it.  V: wave w issues the tile's
+    // wave-wide loads w, w + 8, ...; slot s = 64 * load + lane holds (row s /
+    // slots-per-row, segment s % slots-per-row), padding slots re-read segment 0.
+    // In a tile that crosses n_k, keys past it re-read the last key (finite
+    // values; their scores are masked).
     const uint32_t ks_lds = lds_addr(&Ks[0][0]);
     const uint32_t vs_lds = lds_addr(&Vs[0][0]);
     uint32_t v_dma[C::kVPer];
@@ -248,16 +258,21 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     };
     auto issue = [&](int j0, int buf) __attribute__((always_inline)) {
         const uint32_t need = tile_need(j0);
-        const char* kt = kbytes + int64_t(j0) * row_bytes;  // wave-uniform tile bases
-        const char* vt = vbytes + int64_t(j0) * row_bytes;
+        const char* vt = vbytes + int64_t(j0) * row_bytes;  // wave-uniform tile base
         const bool tail = j0 + kBN > p.n_k;
         const uint32_t last = uint32_t(p.n_k - 1 - j0);
-        const uint32_t krow = (tail ? min(uint32_t(lane), last) : uint32_t(lane)) * row_bytes;
         const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
         for (int t = 0; t < C::kKPerWave; ++t) {
-            const int s = wave + kWaves * t;
-            if ((need >> (s % C::kChunks)) & 1u) load_to_lds(kt, krow + 16u * s, kdst + 1024u * s);
+            const int u = wave + kWaves * t;  // unit = (chunk u / 2, 32-key block u % 2)
+            const int c = u >> 1;
+            if ((need >> c) & 1u) {
+                const int jb = min(j0 + 32 * (u & 1), p.n_k - 1);
+                uint32_t off = k_piece;
+                if (jb + 32 > p.n_k)
+                    off = min(uint32_t(lane & 31), uint32_t(p.n_k - 1 - jb)) * 32u + uint32_t(lane >> 5) * 16u;
+                load_to_lds(kpcm + c * chunk_bytes + int64_t(jb) * 32, off, kdst + 1024u * u);
+            }
         }
         const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
 #pragma unroll
@@ -274,11 +289,11 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     };
 
     // per-lane LDS byte bases of the fragment reads (buffer 0, block 0)
-    //   K: chunk c, half hh = segment c + kChunks * hh, key col of the block
+    //   K: unit (chunk c, block kb) at 1 KB * (2 c + kb), half hh, key col
     //   V: lane group of 16 reads key rows 4 * hh + (l % 16) / 4 (8 rows further
     //      for elements 4..7), dims 16 * ((l / 16) % 2) + 4 * (l % 4) of each
     //      32-dim block
-    const uint32_t k_lane = ks_lds + uint32_t((C::kChunks * hh * kBN + col) * 16);
+    const uint32_t k_lane = ks_lds + uint32_t(hh * 512 + col * 16);
     const int v_dsub = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
     const int v_row = 4 * hh + ((lane & 15) >> 2);
     const uint32_t v_lane = vs_lds + uint32_t((v_row * C::kVStride + v_dsub) * 2);
@@ -294,7 +309,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
     int qb_rf = -1;
 
     auto k_block = [&](int tile, int kb) __attribute__((always_inline)) -> uint32_t {
-        return k_lane + stage_off(tile, C::kKTile * 2) + uint32_t(kb * 32 * 16);
+        return k_lane + stage_off(tile, C::kKTile * 2) + uint32_t(kb * 1024);
     };
 
     // ---- QK of a uniform tile: chunk CF with the boundary operand qb, then the
@@ -306,7 +321,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
             const uint32_t kr = k_block(tile, kb);
             u32x4_t kf[C::kChunks];
 #pragma unroll
-            for (int c = CF; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 1024u * c);
+            for (int c = CF; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 2048u * c);
             f32x16_t acc = mfma(kf[CF], qb, zero16());
 #pragma unroll
             for (int c = CF + 1; c < C::kChunks; ++c) acc = mfma(kf[c], qf[c], acc);
@@ -323,7 +338,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
             const uint32_t kr = k_block(tile, kb);
             u32x4_t kf[C::kChunks];
 #pragma unroll
-            for (int c = 0; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 1024u * c);
+            for (int c = 0; c < C::kChunks; ++c) kf[c] = lds_read_b128(kr + 2048u * c);
             const int zhi = wp_max - jb;
             const int zlo = max(0, wp_min - (jb + 31));
             // all pairs classified at once: lane r holds W_r; bit r of `full` = pair r
@@ -356,7 +371,7 @@ __global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(cons
                 for (int cc = 1; cc < C::kChunks; ++cc)
                     if (cc == c) qc = qf[cc];
                 const f32x16_t pr =
-                    mfma(lds_read_b128(kr + 1024u * c), keep_pairs(qc, 1u << (r & 7)), zero16());
+                    mfma(lds_read_b128(kr + 2048u * c), keep_pairs(qc, 1u << (r & 7)), zero16());
                 const int thr = my_pos - jb - 4 * hh - p.win.W[r];
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {

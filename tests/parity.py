@@ -34,12 +34,16 @@ def windows_for(head_dim, rope_base, k, theta, n_ctx):
             oracle.window_widths(head_dim, rope_base, k, th, n_ctx=n_ctx))
 
 
-def gpu_prefill(q, k, v, q_pos0, win, scale=0.0):
+def gpu_prefill(q, k, v, q_pos0, win, scale=0.0, kp=None, n_k=None):
+    """q [B, n_q, h_q, d]; k, v [B, C, h_kv, d] (K is packed pair-chunk-major by the
+    library first unless kp is given); keys 0 .. n_k - 1 (default C) are used."""
     import paper_2608_02947_amd as atf
     B, n_q, h_q, d = q.shape
+    if kp is None:
+        kp = pack_kcache(k)
     o = torch.empty_like(q)
     lse = torch.empty((B, h_q, n_q), dtype=torch.float32, device=q.device)
-    atf.atf_prefill(q, k, v, o, lse, q_pos0, win, scale)
+    atf.atf_prefill(q, kp, v, o, lse, q_pos0, win, scale, n_k=n_k)
     torch.cuda.synchronize()
     return o, lse
 
@@ -60,20 +64,23 @@ def pack_vcache(v_bshd):
     return vp
 
 
-def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vp=None):
-    """q [B, h_q, d]; caches given in BSHD are packed by the library first."""
+def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vp=None, n_k=None):
+    """q [B, h_q, d]; caches given in BSHD [B, C, h_kv, d] are packed by the library
+    first; keys 0 .. n_k - 1 (default C) are used."""
     import paper_2608_02947_amd as atf
     B, h_q, d = q.shape
-    _, n_k, h_kv, _ = k_bshd.shape
+    _, cap, h_kv, _ = k_bshd.shape
     if kp is None:
         kp = pack_kcache(k_bshd)
     if vp is None:
         vp = pack_vcache(v_bshd)
+    if n_k is None:
+        n_k = cap
     ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, n_k, d), dtype=torch.uint8,
                      device=q.device)
     o = torch.empty_like(q)
     lse = torch.empty((B, h_q), dtype=torch.float32, device=q.device)
-    atf.atf_decode(q, kp, vp, o, lse, q_pos, win, ws, scale)
+    atf.atf_decode(q, kp, vp, o, lse, q_pos, win, ws, scale, n_k=n_k)
     torch.cuda.synchronize()
     return o, lse
 

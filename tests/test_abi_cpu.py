@@ -119,11 +119,12 @@ def test_window_validation():
 
 
 def _raw_prefill(lib, cw, **kw):
-    args = dict(q=16, k=16, v=16, o=16, lse=16, batch=1, n_q=4, n_k=4, q_pos0=0, h_q=2, h_kv=1)
+    args = dict(q=16, k=16, v=16, o=16, lse=16, batch=1, n_q=4, n_k=4, q_pos0=0, h_q=2, h_kv=1,
+                cache_tokens=0)
     args.update(kw)
     return lib.atf_prefill(args["q"], args["k"], args["v"], args["o"], args["lse"], args["batch"],
                            args["n_q"], args["n_k"], args["q_pos0"], args["h_q"], args["h_kv"],
-                           ctypes.byref(cw), 0.0, None)
+                           args["cache_tokens"], ctypes.byref(cw), 0.0, None)
 
 
 def test_prefill_validation_before_launch():
@@ -139,6 +140,8 @@ def test_prefill_validation_before_launch():
         (atf.Window(64, 1e4, 2.0), {"q": None}, atf.ATF_EINVAL),
         (atf.Window(64, 1e4, 2.0), {"o": 18}, atf.ATF_EINVAL),        # misaligned
         (atf.Window(64, 1e4, -1.0), {}, atf.ATF_EINVAL),
+        (atf.Window(64, 1e4, 2.0), {"cache_tokens": 3}, atf.ATF_EINVAL),   # below n_k
+        (atf.Window(64, 1e4, 2.0), {"cache_tokens": 2 ** 31}, atf.ATF_EINVAL),
     ]
     for win, kw, code in cases:
         cw, keep = win.as_c()
@@ -157,11 +160,11 @@ def test_decode_validation_before_launch():
     assert atf.atf_decode_workspace_bytes(8, 24, 8, 131072, 96) == 0
 
     def call(ws=16, ws_bytes=None, d=128, **kw):
-        a = dict(batch=8, n_k=131072, q_pos=131072, h_q=24, h_kv=8)
+        a = dict(batch=8, n_k=131072, q_pos=131072, h_q=24, h_kv=8, cache_tokens=0)
         a.update(kw)
         w, kp = atf.Window(d, 5e5, 2.0).as_c()
         return lib.atf_decode(16, 16, 16, 16, 16, a["batch"], a["n_k"], a["q_pos"], a["h_q"],
-                              a["h_kv"], ctypes.byref(w), 0.0, ws,
+                              a["h_kv"], a["cache_tokens"], ctypes.byref(w), 0.0, ws,
                               need - 1 if ws_bytes is None else ws_bytes, None)
     assert call() == atf.ATF_EWORKSPACE
     assert call(ws=None, ws_bytes=need) == atf.ATF_EWORKSPACE
@@ -169,6 +172,7 @@ def test_decode_validation_before_launch():
     assert call(q_pos=-1) == atf.ATF_EINVAL
     assert call(h_kv=5) == atf.ATF_EINVAL
     assert call(n_k=0) == atf.ATF_EINVAL
+    assert call(ws_bytes=need, cache_tokens=131071) == atf.ATF_EINVAL   # below n_k
 
 
 def test_pack_validation_before_launch():

@@ -141,3 +141,20 @@ def test_decode_custom_scale_and_determinism():
     compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], "scale0.2")
     o2, lse2 = gpu_decode(qd, kd, vd, 3001, win, scale=0.2)
     assert torch.equal(o, o2) and torch.equal(lse, lse2)
+
+
+def test_decode_cache_capacity_and_uninitialised_tail():
+    """Caches allocated for more tokens than written: tokens past n_k (NaN here,
+    including the rest of the 16-token block holding token n_k) are never used."""
+    B, n_k, cap, h_q, h_kv, d = 2, 1001, 1200, 8, 2, 128
+    q, k, v = _decode_inputs(B, n_k, n_k, h_q, h_kv, d, 1e4, seed=31)
+    win, widths = windows_for(d, 1e4, 2.0, None, n_ctx=n_k + 1)
+    kc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    vc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    kc[:, :n_k] = k
+    vc[:, :n_k] = v
+    note("decode cache capacity")
+    qd = q[:, 0].contiguous().to(DEV)
+    o, lse = gpu_decode(qd, kc.to(DEV), vc.to(DEV), n_k, win, n_k=n_k)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, n_k, widths)
+    compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], "capacity")

@@ -14,7 +14,7 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, gpu_prefill, note, sample_rows, to_f64, windows_for,
+from parity import (compare, gpu_prefill, note, pack_kcache, sample_rows, to_f64, windows_for,
                     workload_window)
 
 pytestmark = [pytest.mark.gpu,
@@ -124,9 +124,10 @@ def test_prefill_workload_sampled_rows(name):
 
 
 def test_prefill_chunked_equals_single_shot():
-    """Prefill in chunks (q_pos0 offsets, keys up to the chunk end) is bit-identical
-    to one call over all rows when every chunk boundary is a multiple of the
-    workgroup's position tile, floor(256 / G) positions (36 for G = 7)."""
+    """Prefill in chunks against one pair of caches allocated for the whole sequence
+    (q_pos0 offsets, n_k = keys written so far) is bit-identical to one call over
+    all rows when every chunk boundary is a multiple of the workgroup's position
+    tile, floor(256 / G) positions (36 for G = 7)."""
     wl = W.WORKLOADS["qwen05b_prefill_8k"]
     tile = 256 // wl.group
     chunk = tile * 28
@@ -134,11 +135,26 @@ def test_prefill_chunked_equals_single_shot():
     inp = W.make_inputs(wl, device=DEV, n_q=n, n_k=n, q_pos0=0)
     win, _ = workload_window(wl)
     note("prefill chunked vs single")
-    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win)
+    kp = pack_kcache(inp["k"])
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win, kp=kp)
     for s in range(0, n, chunk):
         qc = inp["q"][:, s:s + chunk].contiguous()
-        kc = inp["k"][:, :s + chunk].contiguous()
-        vc = inp["v"][:, :s + chunk].contiguous()
-        oc, lc = gpu_prefill(qc, kc, vc, s, win)
+        oc, lc = gpu_prefill(qc, inp["k"], inp["v"], s, win, kp=kp, n_k=s + chunk)
         assert torch.equal(oc, o[:, s:s + chunk])
         assert torch.equal(lc, lse[:, :, s:s + chunk])
+
+
+def test_prefill_cache_capacity_and_uninitialised_tail():
+    """Caches allocated for more tokens than written: keys past n_k (filled with NaN
+    here) are never used."""
+    B, n_q, n_k, cap, h_q, h_kv, d = 2, 150, 333, 400, 6, 2, 128
+    q, k, v = _small_inputs(B, n_q, n_k, n_k - n_q, h_q, h_kv, d, 1e4, seed=21)
+    win, widths = windows_for(d, 1e4, 2.0, None, n_ctx=n_k)
+    kc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    vc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    kc[:, :n_k] = k
+    vc[:, :n_k] = v
+    note("prefill cache capacity")
+    o, lse = gpu_prefill(q.to(DEV), kc.to(DEV), vc.to(DEV), n_k - n_q, win, n_k=n_k)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, n_k - n_q, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "capacity")
