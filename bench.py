@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-full-window", action="store_true",
                     help="skip the k=inf reference timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration table (the other workloads)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -115,6 +117,112 @@ def copy_calibration():
         b.copy_(a)
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes": n, "launches": 3}))
+
+
+PREFILL_CONFIGS = ["qwen05b_prefill_1k", "qwen05b_prefill_8k", "qwen05b_prefill_32k",
+                   "llama3b_prefill_32k", "llama3b_prefill_128k"]
+DECODE_CONFIGS = ["llama3b_decode_32k", "llama3b_decode_128k"]
+
+
+def _median_ms(fn, stream, warm, iters):
+    for _ in range(warm):
+        fn()
+    evs = []
+    for _ in range(iters):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        fn()
+        b.record(stream)
+        evs.append((a, b))
+    torch.cuda.synchronize()
+    return statistics.median(a.elapsed_time(b) for a, b in evs)
+
+
+def config_table(atf, W, dev, stream):
+    """ms, effective TFLOP/s (prefill) or GB/s (decode), fraction of the roofline and
+    speedup over the same kernel at k = +inf for each of the other configurations.
+    Llama tables: the effective-frequency window (default) and, as a second row,
+    the raw-base window, both on inputs rotated with the effective frequencies."""
+    out = {}
+    for name in PREFILL_CONFIGS:
+        wl = W.WORKLOADS[name]
+        d = wl.head_dim
+        inp = W.make_inputs(wl, device=dev)
+        kp = torch.empty(atf.kcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_kcache(inp["k"], kp)
+        o = torch.empty_like(inp["q"])
+        lse = torch.empty((wl.batch, wl.h_q, wl.n_q), dtype=torch.float32, device=dev)
+        th = W.workload_theta(wl)
+        tables = {"": None if th is None else th.numpy()}
+        if th is not None:
+            tables["raw_base"] = None
+        iters = 5 if wl.n_q * wl.h_q >= 1 << 21 else 20
+        off = atf.Window(d, wl.rope_base, math.inf)
+        run = lambda w: atf.atf_prefill(inp["q"], kp, inp["v"], o, lse, wl.q_pos0, w,
+                                        stream=stream)
+        t_off = _median_ms(lambda: run(off), stream, 2, iters)
+        for tag, table in tables.items():
+            win = atf.Window(d, wl.rope_base, wl.k, table)
+            T, C = atf.atf_count_terms(win, wl.n_q, wl.q_pos0, wl.n_k)
+            flops = wl.batch * wl.h_q * (4 * T + 2 * d * C)
+            t = _median_ms(lambda: run(win), stream, 2, iters)
+            tf = flops / (t * 1e-3) / 1e12
+            out[name + ("_" + tag if tag else "")] = {
+                "ms": round(t, 4), "effective_tflops": round(tf, 1),
+                "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                "full_window_ms": round(t_off, 4), "speedup_vs_full_window": round(t_off / t, 4),
+                "qk_pruned": round(1 - T / (C * d / 2), 4)}
+        del inp, kp, o, lse
+        torch.cuda.empty_cache()
+    for name in DECODE_CONFIGS:
+        wl = W.WORKLOADS[name]
+        d = wl.head_dim
+        inp = W.make_inputs(wl, device=dev)
+        per_set = 2 * wl.batch * wl.n_k * wl.h_kv * d * 2
+        nset = max(1, -(-(1 << 30) // per_set))  # cache sets rotated: >= 1 GiB in all
+        sets = []
+        for i in range(nset):
+            kp = torch.empty(atf.kcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                             device=dev)
+            vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                             device=dev)
+            atf.atf_pack_kcache(inp["k"], kp)
+            atf.atf_pack_vcache(inp["v"], vp)
+            sets.append((kp, vp))
+        del inp["k"], inp["v"]
+        qd = inp["q"][:, 0].contiguous()
+        od = torch.empty_like(qd)
+        lsed = torch.empty((wl.batch, wl.h_q), dtype=torch.float32, device=dev)
+        ws = torch.empty(atf.atf_decode_workspace_bytes(wl.batch, wl.h_q, wl.h_kv, wl.n_k, d),
+                         dtype=torch.uint8, device=dev)
+        th = W.workload_theta(wl)
+        tables = {"": None if th is None else th.numpy()}
+        if th is not None:
+            tables["raw_base"] = None
+        off = atf.Window(d, wl.rope_base, math.inf)
+        state = {"i": 0}
+
+        def run(w):
+            kp, vp = sets[state["i"] % nset]
+            state["i"] += 1
+            atf.atf_decode(qd, kp, vp, od, lsed, wl.q_pos0, w, ws, stream=stream)
+        t_off = _median_ms(lambda: run(off), stream, 3, 30)
+        R_off, Cd = atf.atf_count_terms(off, 1, wl.q_pos0, wl.n_k)
+        for tag, table in tables.items():
+            win = atf.Window(d, wl.rope_base, wl.k, table)
+            R, Cd = atf.atf_count_terms(win, 1, wl.q_pos0, wl.n_k)
+            nbytes = wl.batch * wl.h_kv * (4 * R + 2 * d * Cd) + wl.batch * wl.h_q * d * 4
+            t = _median_ms(lambda: run(win), stream, 3, 30)
+            gbs = nbytes / (t * 1e-3) / 1e9
+            out[name + ("_" + tag if tag else "")] = {
+                "ms": round(t, 4), "GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+                "algorithmic_bytes": nbytes, "full_window_ms": round(t_off, 4),
+                "speedup_vs_full_window": round(t_off / t, 4), "cache_sets": nset}
+        del sets, qd, od, lsed, ws
+        torch.cuda.empty_cache()
+    return out
 
 
 # HBM bytes moved by one launch of a kernel at the benchmark workload, from two
@@ -328,6 +436,9 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(inp, pf, args.cpu_rows)
+    del inp, q, k, v, kp, vp, o, lse
+    torch.cuda.empty_cache()
+    configs = None if args.no_configs else config_table(atf, W, dev, stream)
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
@@ -341,6 +452,7 @@ def main():
                    "k": pf.k, "parallelism": "single GPU"},
         "prefill": prefill_info, "decode": decode_info, "roofline": roofline,
         "cpu_baseline": cpu,
+        "configs": configs,
     }
     print(json.dumps(out))
 

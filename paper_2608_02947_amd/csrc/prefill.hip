@@ -162,8 +162,10 @@ __device__ __forceinline__ void vm_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); 
 // for) before it, and the direct-to-LDS loads are awaited with vm_wait
 __device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
 
+// Two waves per SIMD (one workgroup per CU): the windowed kernel's registers
+// exceed the 128 that four waves per SIMD would leave each wave, even at d = 64.
 template <int D, bool kWin>
-__global__ __launch_bounds__(kThreads, D == 64 ? 4 : 2) void prefill_kernel(const PrefillParams p) {
+__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParams p) {
     using C = Cfg<D>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[kStages][C::kKTile];
     __shared__ __attribute__((aligned(16))) uint16_t Vs[kStages][C::kVTile];
