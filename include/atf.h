@@ -100,7 +100,8 @@ int atf_count_terms(const atf_window *w, int64_t n_q, int64_t q_pos0, int64_t n_
  * Errors: ATF_EINVAL (NULL/misaligned pointer, batch < 1, n_q < 0, n_k < 1,
  * q_pos0 < 0, q_pos0 + n_q > 2^31 - 1, n_k > 2^31 - 1, cache_tokens < n_k (when
  * non-zero) or > 2^31 - 1, h_q % h_kv != 0, bad window, non-finite scale);
- * ATF_EUNSUPPORTED (d not 64 or 128); ATF_EHIP. */
+ * ATF_EUNSUPPORTED (d not 64 or 128, or h_q / h_kv above 128 at d = 64 or above 256 at
+ * d = 128: the query heads of one KV head share a workgroup's rows); ATF_EHIP. */
 int atf_prefill(const void *q, const void *k_cache, const void *v, void *o, float *lse,
                 int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
                 int32_t h_q, int32_t h_kv, int64_t cache_tokens, const atf_window *w,

@@ -199,8 +199,10 @@ int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse
                     "prefill: need batch >= 1, n_q >= 0, n_k >= 1, q_pos0 >= 0, heads >= 1");
     if (h_q % h_kv != 0)
         return fail(ATF_EINVAL, "prefill: h_q %d not a multiple of h_kv %d", h_q, h_kv);
-    if (h_q / h_kv > 256)
-        return fail(ATF_EUNSUPPORTED, "prefill: GQA ratio %d above 256 not built", h_q / h_kv);
+    const int max_group = d == 64 ? 128 : 256;  // query rows of one prefill workgroup
+    if (h_q / h_kv > max_group)
+        return fail(ATF_EUNSUPPORTED, "prefill: GQA ratio %d above %d not built for d = %d",
+                    h_q / h_kv, max_group, d);
     if (q_pos0 + n_q > kPosLimit || n_k > kPosLimit)
         return fail(ATF_EINVAL, "prefill: positions must stay below 2^31 - 1");
     if (cache_tokens == 0) cache_tokens = n_k;

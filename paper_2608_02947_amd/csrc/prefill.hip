@@ -3,13 +3,13 @@
 // as a per-tile slice of the QK contraction axis (Sec. 3.3).
 //
 // Work decomposition
-//   A workgroup of 8 waves owns 256 query rows that share one KV head: P = 256/G
+//   A workgroup of W waves owns 32 W query rows that share one KV head: P = 32W/G
 //   consecutive positions x the G query heads of the group (row f -> position
-//   f / G, head f % G), so every K/V tile staged in LDS serves 256 rows.  Each
-//   wave owns 32 rows (one MFMA row-block); two waves share a SIMD.  Key tiles of
-//   64 rotate through three LDS buffers, filled by global_load_lds_dwordx4
-//   (global memory straight into LDS, no register staging) one tile ahead of the
-//   compute.
+//   f / G, head f % G), so every K/V tile staged in LDS serves all of them.  Each
+//   wave owns 32 rows (one MFMA row-block).  W = 8 at d = 128 (two waves per
+//   SIMD), W = 4 at d = 64 (three workgroups per CU).  Key tiles of 64 rotate
+//   through LDS buffers filled by global_load_lds_dwordx4 (global memory straight
+//   into LDS, no register staging) one tile ahead of the compute.
 //
 // K comes from the pair-chunk-major cache (the decode layout): chunk c of a KV
 // head is a stream of 32 bytes per key (dims [8c, 8c+8) then [d/2+8c, d/2+8c+8)),
@@ -74,15 +74,20 @@ typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
-constexpr int kWaves = 8;
-constexpr int kThreads = kWaves * 64;
-constexpr int kRows = kWaves * 32;  // query rows per workgroup
-constexpr int kBN = 64;             // keys per tile
-constexpr int kStages = 3;          // LDS buffers per K and V tile
-constexpr float kRescale = 8.0f;    // lazy-rescale threshold, log2 units
+constexpr int kBN = 64;           // keys per tile
+constexpr float kRescale = 8.0f;  // lazy-rescale threshold, log2 units
 
-template <int D>
+// 8 waves (256 rows) per workgroup, two waves per SIMD, three LDS stages; the
+// windowed kernel at d = 64 instead runs 4 waves (128 rows) per workgroup with two
+// LDS stages, so that three workgroups share a CU at its ~160 VGPRs.
+template <int D, bool kWin>
 struct Cfg {
+    static constexpr bool kSmall = D == 64 && kWin;
+    static constexpr int kWaves = kSmall ? 4 : 8;
+    static constexpr int kThreads = kWaves * 64;
+    static constexpr int kRows = kWaves * 32;  // query rows per workgroup
+    static constexpr int kStages = kSmall ? 2 : 3;  // LDS buffers per K and V tile
+    static constexpr int kMinWavesPerSimd = kSmall ? 3 : 2;
     static constexpr int kHalf = D / 2;
     static constexpr int kChunks = D / 16;
     static constexpr int kSegs = D / 8;             // 16-byte segments per V row
@@ -138,6 +143,7 @@ __device__ __forceinline__ s16x4_t lds_read_tr(uint32_t byte_addr) {
 // byte offset of the LDS buffer of a tile.  Passed through readfirstlane so the
 // compiler treats it as one opaque scalar per tile instead of re-deriving it in
 // every address (which defeats the offset-field folding above).
+template <int kStages>
 __device__ __forceinline__ uint32_t stage_off(int tile, int buf_bytes) {
     return uint32_t(__builtin_amdgcn_readfirstlane((tile % kStages) * buf_bytes));
 }
@@ -165,10 +171,11 @@ __device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
 // Two waves per SIMD (one workgroup per CU): the windowed kernel's registers
 // exceed the 128 that four waves per SIMD would leave each wave, even at d = 64.
 template <int D, bool kWin>
-__global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParams p) {
-    using C = Cfg<D>;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[kStages][C::kKTile];
-    __shared__ __attribute__((aligned(16))) uint16_t Vs[kStages][C::kVTile];
+__global__ __launch_bounds__((Cfg<D, kWin>::kThreads), (Cfg<D, kWin>::kMinWavesPerSimd)) void
+prefill_kernel(const PrefillParams p) {
+    using C = Cfg<D, kWin>;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[C::kStages][C::kKTile];
+    __shared__ __attribute__((aligned(16))) uint16_t Vs[C::kStages][C::kVTile];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
     uint32_t v_dma[C::kVPer];
 #pragma unroll
     for (int t = 0; t < C::kVPer; ++t) {
-        const int s = 64 * (wave + kWaves * t) + lane;
+        const int s = 64 * (wave + C::kWaves * t) + lane;
         const int seg = s % C::kVSlots;
         v_dma[t] = uint32_t(s / C::kVSlots) * row_bytes + 16u * uint32_t(seg < C::kSegs ? seg : 0);
     }
@@ -266,7 +273,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
         const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
         for (int t = 0; t < C::kKPerWave; ++t) {
-            const int u = wave + kWaves * t;  // unit = (chunk u / 2, 32-key block u % 2)
+            const int u = wave + C::kWaves * t;  // unit = (chunk u / 2, 32-key block u % 2)
             const int c = u >> 1;
             if ((need >> c) & 1u) {
                 const int jb = min(j0 + 32 * (u & 1), p.n_k - 1);
@@ -279,7 +286,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
         const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
 #pragma unroll
         for (int t = 0; t < C::kVPer; ++t) {
-            const int u = wave + kWaves * t;
+            const int u = wave + C::kWaves * t;
             if (u >= C::kVLoads) break;
             uint32_t off = v_dma[t];
             if (tail) {
@@ -311,7 +318,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
     int qb_rf = -1;
 
     auto k_block = [&](int tile, int kb) __attribute__((always_inline)) -> uint32_t {
-        return k_lane + stage_off(tile, C::kKTile * 2) + uint32_t(kb * 1024);
+        return k_lane + stage_off<C::kStages>(tile, C::kKTile * 2) + uint32_t(kb * 1024);
     };
 
     // ---- QK of a uniform tile: chunk CF with the boundary operand qb, then the
@@ -422,7 +429,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
                 for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
         }
         const float m_use = m_run == -INFINITY ? 0.f : m_run;
-        const uint32_t vb = v_lane + stage_off(tile, C::kVTile * 2);
+        const uint32_t vb = v_lane + stage_off<C::kStages>(tile, C::kVTile * 2);
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             u32x4_t pb[2];
@@ -457,7 +464,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
     // one tile: stage the next, compute this one (if the wave has rows there),
     // await this wave's loads of the next tile, barrier
     auto run_tile = [&](int u, auto&& qk) __attribute__((always_inline)) {
-        if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % kStages);
+        if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
         if (active(u)) {
             qk(u);
             softmax_pv(u);
@@ -545,7 +552,7 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
                 break;
             default:  // idle: keep the barrier count
                 for (; u < seg_end; ++u) {
-                    if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % kStages);
+                    if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
                     vm_wait();
                     barrier();
                 }
@@ -578,9 +585,11 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_kernel(const PrefillParam
 template <int D>
 hipError_t launch_d(const PrefillParams& p, unsigned blocks, bool window_on, hipStream_t stream) {
     if (window_on)
-        hipLaunchKernelGGL((prefill_kernel<D, true>), dim3(blocks), dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL((prefill_kernel<D, true>), dim3(blocks), dim3(Cfg<D, true>::kThreads), 0,
+                           stream, p);
     else
-        hipLaunchKernelGGL((prefill_kernel<D, false>), dim3(blocks), dim3(kThreads), 0, stream, p);
+        hipLaunchKernelGGL((prefill_kernel<D, false>), dim3(blocks), dim3(Cfg<D, false>::kThreads),
+                           0, stream, p);
     return hipGetLastError();
 }
 
@@ -588,11 +597,6 @@ hipError_t launch_d(const PrefillParams& p, unsigned blocks, bool window_on, hip
 
 hipError_t launch_prefill(const PrefillParams& p_in, int head_dim, hipStream_t stream) {
     PrefillParams p = p_in;
-    if (p.group < 1 || p.group > kRows) return hipErrorInvalidValue;
-    p.pos_per_tile = kRows / p.group;
-    p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
-    const int64_t blocks = int64_t(p.n_qtiles) * p.h_kv * p.batch;
-    if (blocks <= 0 || blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     // the window is off when no threshold is below the largest possible distance;
     // the uniform-run path needs thresholds non-decreasing in r and the last chunk
     // kept at every distance of the call
@@ -604,6 +608,13 @@ hipError_t launch_prefill(const PrefillParams& p_in, int head_dim, hipStream_t s
     for (int r = 1; r < head_dim / 2; ++r)
         if (p.win.W[r] < p.win.W[r - 1]) mono = false;
     p.mono = mono ? 1 : 0;
+    const int rows = head_dim == 64 ? (window_on ? Cfg<64, true>::kRows : Cfg<64, false>::kRows)
+                                    : Cfg<128, true>::kRows;
+    if (p.group < 1 || p.group > rows) return hipErrorInvalidValue;
+    p.pos_per_tile = rows / p.group;
+    p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
+    const int64_t blocks = int64_t(p.n_qtiles) * p.h_kv * p.batch;
+    if (blocks <= 0 || blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
     (void)hipGetLastError();
     return head_dim == 64 ? launch_d<64>(p, unsigned(blocks), window_on, stream)
                           : launch_d<128>(p, unsigned(blocks), window_on, stream);

@@ -127,9 +127,10 @@ def test_prefill_chunked_equals_single_shot():
     """Prefill in chunks against one pair of caches allocated for the whole sequence
     (q_pos0 offsets, n_k = keys written so far) is bit-identical to one call over
     all rows when every chunk boundary is a multiple of the workgroup's position
-    tile, floor(256 / G) positions (36 for G = 7)."""
+    tile, floor(rows / G) positions (rows = 128 at d = 64, 256 at d = 128: 18 for
+    the d = 64, G = 7 workload used here)."""
     wl = W.WORKLOADS["qwen05b_prefill_8k"]
-    tile = 256 // wl.group
+    tile = (128 if wl.head_dim == 64 else 256) // wl.group
     chunk = tile * 28
     n = 4 * chunk
     inp = W.make_inputs(wl, device=DEV, n_q=n, n_k=n, q_pos0=0)
