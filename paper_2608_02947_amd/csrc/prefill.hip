@@ -608,8 +608,9 @@ hipError_t launch_prefill(const PrefillParams& p_in, int head_dim, hipStream_t s
     for (int r = 1; r < head_dim / 2; ++r)
         if (p.win.W[r] < p.win.W[r - 1]) mono = false;
     p.mono = mono ? 1 : 0;
-    const int rows = head_dim == 64 ? (window_on ? Cfg<64, true>::kRows : Cfg<64, false>::kRows)
-                                    : Cfg<128, true>::kRows;
+    const int rows = head_dim == 64
+                         ? (window_on ? Cfg<64, true>::kRows : Cfg<64, false>::kRows)
+                         : (window_on ? Cfg<128, true>::kRows : Cfg<128, false>::kRows);
     if (p.group < 1 || p.group > rows) return hipErrorInvalidValue;
     p.pos_per_tile = rows / p.group;
     p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
