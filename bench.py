@@ -234,8 +234,8 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "9ca18790552376311af808f7deca3b5e6c24ae3bc04f4e8862857048a980671d",
-        "fetch_kib": 79793422.94, "write_kib": 1020822.84,
+        "sha256": "c719073f8ef6a073e309e64a4a8c274446c720e171dd87838b0e2afa6c89a6d1",
+        "fetch_kib": 79793418.94, "write_kib": 1020823.06,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
