@@ -9,6 +9,9 @@ module only marshals numpy arrays into it:
 
 - :func:`window_widths` -- w_r = min(k * lambda_r, N), lambda_r = 2*pi/theta_r
   (Sec. 3.1 eq:lambda, Sec. 3.2 eq:window).
+- :func:`retention_profile` -- the per-pair retention k_r of App. A: constant,
+  k-arithmetic (the variable-k profile 16 -> 2 is one) or k-geometric.
+- :func:`family_widths` -- the window family of App. A eq:family.
 - :func:`scores` -- the windowed, scaled score matrix of one (batch, head)
   (Sec. 3.1 eq:pair with the keep rule of Sec. 3.2).
 - :func:`attend` -- windowed causal attention, plain two-pass softmax, for all
@@ -57,13 +60,14 @@ def _load():
         i64 = ctypes.c_int64
         dbl = ctypes.c_double
         lib.oracle_window_widths.argtypes = [i64, dbl, dbl, p, dbl, p]
+        lib.oracle_family_widths.argtypes = [i64, dbl, p, p, dbl, dbl, dbl, dbl, p]
         lib.oracle_scores.argtypes = [p, p, ctypes.c_int, i64, i64, i64, i64, i64, i64,
                                       i64, p, dbl, i64, i64, p]
         lib.oracle_attend.argtypes = [p, p, p, ctypes.c_int, i64, i64, i64, i64, i64, i64,
                                       i64, p, dbl, i64, p, p, p, p, ctypes.c_int]
         lib.oracle_count_terms.argtypes = [p, i64, i64, i64, i64, p, p]
-        for f in (lib.oracle_window_widths, lib.oracle_scores, lib.oracle_attend,
-                  lib.oracle_count_terms):
+        for f in (lib.oracle_window_widths, lib.oracle_family_widths, lib.oracle_scores,
+                  lib.oracle_attend, lib.oracle_count_terms):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -103,6 +107,47 @@ def window_widths(head_dim: int, rope_base: float, k: float, theta=None,
                                   _ptr(th) if th is not None else None, float(n_ctx), _ptr(w))
     if rc != 0:
         raise ValueError("oracle_window_widths: bad arguments")
+    return w
+
+
+def retention_profile(head_dim: int, kind: str, k_hi: float, k_lo: float = None) -> np.ndarray:
+    """Per-pair retention k_r, r = 0 (highest frequency) .. d/2 - 1 (App. A).
+
+    "constant": k_r = k_hi.  "arithmetic": k_r falls by the same amount per
+    pair, from k_hi at r = 0 to k_lo at r = d/2 - 1 (the variable-k profile of
+    the main text is k_hi = 16, k_lo = 2).  "geometric": k_r falls by the same
+    ratio per pair between the same end points.  With one pair, k_r = k_hi.
+    """
+    n = head_dim // 2
+    r = np.arange(n, dtype=np.float64)
+    if kind == "constant":
+        return np.full(n, float(k_hi))
+    span = max(n - 1, 1)
+    if kind == "arithmetic":
+        return k_hi - (k_hi - k_lo) * r / span
+    if kind == "geometric":
+        return k_hi * (k_lo / k_hi) ** (r / span)
+    raise ValueError(kind)
+
+
+def family_widths(head_dim: int, rope_base: float, k_profile, gamma: float = 1.0,
+                  a: float = 0.0, beta: float = 0.0, cap: float = math.inf,
+                  theta=None) -> np.ndarray:
+    """w_r = min(max(k_r lambda_r^gamma + a (r+1)/(d/2), beta), cap) (App. A eq:family);
+    a position-free pair (theta_r = 0) gets +inf."""
+    lib = _load()
+    kp = np.ascontiguousarray(np.broadcast_to(np.asarray(k_profile, dtype=np.float64),
+                                              (head_dim // 2,)))
+    th = None
+    if theta is not None:
+        th = np.ascontiguousarray(theta, dtype=np.float64)
+        assert th.shape == (head_dim // 2,)
+    w = np.empty(head_dim // 2, dtype=np.float64)
+    rc = lib.oracle_family_widths(head_dim, float(rope_base), _ptr(th) if th is not None else None,
+                                  _ptr(kp), float(gamma), float(a), float(beta), float(cap),
+                                  _ptr(w))
+    if rc != 0:
+        raise ValueError("oracle_family_widths: bad arguments")
     return w
 
 

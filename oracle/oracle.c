@@ -11,7 +11,9 @@
  *   - theta_r = B^(-2r/d) for pair r = 0..d/2-1, or a caller-supplied effective
  *     theta'_r (Sec. 3.1; Sec. 3.2 last paragraph for rope scaling).
  *   - wavelength lambda_r = 2*pi / theta_r (Sec. 3.1, eq:lambda).
- *   - window w_r = min(k * lambda_r, N) (Sec. 3.2, eq:window).
+ *   - window w_r = min(k * lambda_r, N) (Sec. 3.2, eq:window), or a member of
+ *     the window family w_r = min(max(k_r lambda_r^gamma + a(r+1)/(d/2), beta), W)
+ *     (App. A, eq:family).
  *   - the rotated score split into pair terms (Sec. 3.1, eq:pair): pair r of a
  *     rotate-half vector is dims (r, r + d/2), and its term is
  *     q[r]k[r] + q[r+d/2]k[r+d/2].  At cell (n, m), z = n - m, a pair term is
@@ -73,6 +75,46 @@ int oracle_window_widths(int64_t d, double base, double k, const double *theta,
         double lambda = two_pi / th; /* +inf when th == 0 */
         double kl = k * lambda;
         w_out[r] = kl < n_ctx ? kl : n_ctx;
+    }
+    return 0;
+}
+
+/*
+ * Window family (App. A, eq:family): for each pair r,
+ *   w_r = min( max( k_r * lambda_r^gamma + a * (r + 1) / (d/2), beta ), cap )
+ * with the retention profile k_r = k_prof[r], the wavelength exponent gamma, the
+ * additive term a (linear in r, no wavelength in it), the floor beta and the
+ * ceiling cap (the W of eq:family; +INFINITY for none).  The default window is
+ * k_r = k, gamma = 1, a = 0, beta = 0, cap = N.
+ * A position-free pair (theta_r == 0) has no wavelength: App. A treats it as
+ * the theta -> 0 limit that is never pruned, a knob apart from the family, so
+ * its width is +INFINITY whatever the other parameters are.
+ * Returns 0, or -1 on bad arguments or when a width is NaN.
+ */
+int oracle_family_widths(int64_t d, double base, const double *theta, const double *k_prof,
+                         double gamma, double a, double beta, double cap, double *w_out)
+{
+    if (d <= 0 || d % 2 != 0 || k_prof == NULL || w_out == NULL)
+        return -1;
+    const double two_pi = 2.0 * 3.14159265358979323846;
+    const double half = (double)(d / 2);
+    for (int64_t r = 0; r < d / 2; ++r) {
+        double th = theta ? theta[r] : pow(base, -2.0 * (double)r / (double)d);
+        if (!(th >= 0.0))
+            return -1;
+        if (th == 0.0) {
+            w_out[r] = INFINITY;
+            continue;
+        }
+        double lambda = two_pi / th;
+        double w = k_prof[r] * pow(lambda, gamma) + a * (double)(r + 1) / half;
+        if (w < beta)
+            w = beta;
+        if (w > cap)
+            w = cap;
+        if (isnan(w))
+            return -1;
+        w_out[r] = w;
     }
     return 0;
 }

@@ -292,10 +292,17 @@ def _pruned(oracle_lib, rec):
     f = kv(rec)
     d = int(f["d"])
     base = float(f["base"])
-    kwin = float(f["k"])
     N = int(f["N"])
     theta = W.llama3_theta(d, base).numpy() if rec[1] == "llama3b" else None
     qty = rec[5]
+    if "to" in f["k"]:  # k-arithmetic retention profile k_hi -> k_lo (App. A)
+        hi, lo = (float(x) for x in f["k"].split("to"))
+        assert qty == "pruned_prefill"
+        prof = oracle_lib.retention_profile(d, "arithmetic", hi, lo)
+        w = oracle_lib.family_widths(d, base, prof, cap=N, theta=theta)
+        T, C = oracle_lib.count_terms(w, N, 0, N)
+        return 100.0 * (1 - T / (C * d / 2))
+    kwin = float(f["k"])
     if qty == "pruned_prefill":
         w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
         T, C = oracle_lib.count_terms(w, N, 0, N)
@@ -413,3 +420,116 @@ def test_window_widths_basics(oracle_lib):
         oracle_lib.window_widths(8, 100.0, 0.0)
     with pytest.raises(ValueError):
         oracle_lib.window_widths(8, 100.0, float("nan"))
+
+
+# ----------------------------------------------------------------------------
+# window family of App. A (eq:family) and the retention profiles
+# ----------------------------------------------------------------------------
+def test_retention_profiles_follow_app_a(oracle_lib):
+    """Variable-k profile: 16 at the highest frequency (r = 0) down to 2 at the
+    lowest, falling by 14/(d/2 - 1) per pair; k-geometric: same end points, a
+    constant ratio; constant: k everywhere."""
+    for d in (64, 128):
+        n = d // 2
+        ka = oracle_lib.retention_profile(d, "arithmetic", 16.0, 2.0)
+        assert ka[0] == 16.0 and ka[-1] == pytest.approx(2.0, abs=1e-12)
+        np.testing.assert_allclose(np.diff(ka), -14.0 / (n - 1), rtol=1e-12)
+        kg = oracle_lib.retention_profile(d, "geometric", 16.0, 2.0)
+        assert kg[0] == 16.0 and kg[-1] == pytest.approx(2.0, rel=1e-12)
+        np.testing.assert_allclose(kg[1:] / kg[:-1], (2.0 / 16.0) ** (1.0 / (n - 1)), rtol=1e-12)
+        # the geometric profile falls faster at high frequencies
+        assert np.all(kg[1:-1] < ka[1:-1])
+        assert np.all(oracle_lib.retention_profile(d, "constant", 3.0) == 3.0)
+
+
+def test_family_default_point_is_the_default_window(oracle_lib):
+    """k_r = k, gamma = 1, a = 0, beta = 0, cap = N is eq:window (App. A)."""
+    for d, base, kwin, N in [(64, 1e6, 2.0, 32768), (128, 1e7, 2.0, 1 << 20), (8, 100.0, 1.0, 300)]:
+        wf = oracle_lib.family_widths(d, base, np.full(d // 2, kwin), cap=N)
+        wd = oracle_lib.window_widths(d, base, kwin, n_ctx=N)
+        np.testing.assert_array_equal(wf, wd)
+    th = W.llama3_theta(128, 5e5).numpy()
+    wf = oracle_lib.family_widths(128, 0.0, np.full(64, 2.0), cap=65536, theta=th)
+    np.testing.assert_array_equal(wf, oracle_lib.window_widths(128, 0.0, 2.0, th, n_ctx=65536))
+    # a position-free pair is never pruned, whatever the knobs (App. A)
+    wf = oracle_lib.family_widths(4, 0.0, [2.0, 0.0], gamma=0.5, beta=3.0, cap=10.0,
+                                  theta=np.array([1.0, 0.0]))
+    assert wf[1] == math.inf and wf[0] == pytest.approx(2.0 * math.sqrt(2 * math.pi))
+
+
+@pytest.mark.parametrize("gamma", [0.8, 1.3])
+@pytest.mark.parametrize("d,base", [(64, 1e6), (128, 5e5)])
+def test_family_gamma_acts_as_base_rescaling(oracle_lib, gamma, d, base):
+    """eq:gammasub: a gamma-window on base B is the default window on base B^gamma
+    with w_min = k (2 pi)^gamma, so eq:redprefill holds with ln B -> gamma ln B
+    (within the 1-2 point integral error of Sec. 4; 2 points allowed)."""
+    kwin = 2.0
+    wg = oracle_lib.family_widths(d, base, np.full(d // 2, kwin), gamma=gamma)
+    wd = oracle_lib.window_widths(d, base ** gamma, kwin * (2 * math.pi) ** (gamma - 1))
+    np.testing.assert_allclose(wg, wd, rtol=1e-13)
+    wmin = kwin * (2 * math.pi) ** gamma
+    for N in (32768, 131072):  # below saturation, N < k lambda_max^gamma
+        assert N < wg.max()
+        T, C = oracle_lib.count_terms(wg, N, 0, N)
+        exact = 1 - T / (C * d / 2)
+        closed = (math.log(N / wmin) - 1.5) / (gamma * math.log(base))
+        assert abs(exact - closed) < 0.02, (N, exact, closed)
+
+
+def test_family_linear_window_retention(oracle_lib):
+    """k_r = 0, a = W degenerates to the linear window w = W (r+1)/(d/2) (App. A,
+    App. C Step 4): one row of n keys retains 1 - n/(2W) of its terms for n <= W
+    and W/(2n) past it, up to O(1/d) (4/d allowed)."""
+    d, Wlin = 2048, 1000.0
+    w = oracle_lib.family_widths(d, 1e4, np.zeros(d // 2), a=Wlin)
+    np.testing.assert_allclose(w, Wlin * np.arange(1, d // 2 + 1) / (d // 2), rtol=1e-15)
+    for n in (100, 500, 1000, 2000, 8000):
+        T, C = oracle_lib.count_terms(w, 1, n - 1, n)
+        kept = T / (C * d / 2)
+        pred = 1 - n / (2 * Wlin) if n <= Wlin else Wlin / (2 * n)
+        assert abs(kept - pred) < 4.0 / d, (n, kept, pred)
+
+
+def test_family_sliding_window_counts_and_scores(oracle_lib):
+    """Every pair at one width S (k_r = 0, beta = cap = S): the sliding-window
+    special case of App. A.  Count = sum over rows of min(p + 1, S + 1) cells, times
+    d/2; scores are the full dot product for z <= S and an empty sum (0) beyond."""
+    d, S = 16, 37
+    w = oracle_lib.family_widths(d, 1e4, np.zeros(d // 2), beta=S, cap=S)
+    assert np.all(w == S)
+    for n_q, q0, n_k in [(300, 0, 300), (50, 400, 450), (10, 0, 5)]:
+        T, C = oracle_lib.count_terms(w, n_q, q0, n_k)
+        cells = sum(min(p + 1, n_k) - max(0, p - S) for p in range(q0, q0 + n_q)
+                    if max(0, p - S) <= min(p, n_k - 1))
+        assert T == cells * d // 2
+    rng = np.random.default_rng(17)
+    n = 90
+    q = bf16_grid(rng, (1, n, 1, d))
+    k = bf16_grid(rng, (1, n, 1, d))
+    s = oracle_lib.scores(q, k, 0, w)
+    full = q[0, :, 0] @ k[0, :, 0].T / math.sqrt(d)
+    z = np.arange(n)[:, None] - np.arange(n)[None, :]
+    want = np.where(z < 0, -np.inf, np.where(z > S, 0.0, full))
+    np.testing.assert_allclose(s, want, atol=1e-12)
+
+
+def test_family_floor_and_ceiling(oracle_lib):
+    """The floor beta keeps every pair at distances z <= beta (scores equal the full
+    dot product there); the ceiling cap prunes every pair past it (scores 0)."""
+    d, base, beta, cap = 16, 1e4, 30.0, 200.0
+    w = oracle_lib.family_widths(d, base, np.full(d // 2, 2.0), beta=beta, cap=cap)
+    wd = oracle_lib.window_widths(d, base, 2.0)
+    np.testing.assert_array_equal(w, np.minimum(np.maximum(wd, beta), cap))
+    assert w.min() == beta and w.max() == cap  # both clamps bind for this base
+    rng = np.random.default_rng(23)
+    n = 260
+    q = bf16_grid(rng, (1, n, 1, d))
+    k = bf16_grid(rng, (1, n, 1, d))
+    s = oracle_lib.scores(q, k, 0, w)
+    full = q[0, :, 0] @ k[0, :, 0].T / math.sqrt(d)
+    z = np.arange(n)[:, None] - np.arange(n)[None, :]
+    near = (z >= 0) & (z <= beta)
+    np.testing.assert_allclose(s[near], full[near], atol=1e-12)
+    assert np.all(s[z > cap] == 0.0)
+    with pytest.raises(ValueError):   # 0 * inf: the width is undefined
+        oracle_lib.family_widths(4, 10.0, [0.0, 1.0], gamma=1e6)
