@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-configuration table (the other workloads)")
+    ap.add_argument("--no-family", action="store_true",
+                    help="skip the window-family timings (variable-k profile, uniform k=64)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -122,6 +124,15 @@ def copy_calibration():
 PREFILL_CONFIGS = ["qwen05b_prefill_1k", "qwen05b_prefill_8k", "qwen05b_prefill_32k",
                    "llama3b_prefill_32k", "llama3b_prefill_128k"]
 DECODE_CONFIGS = ["llama3b_decode_32k", "llama3b_decode_128k"]
+# configurations also timed under the variable-k profile 16 -> 2 and uniform k = 64
+FAMILY_CONFIGS = ("qwen05b_prefill_32k", "llama3b_prefill_128k", "llama3b_decode_128k")
+
+
+def family_windows(atf, d, base, theta):
+    """The window-family members timed beside the default window (App. A)."""
+    return {"var16to2": atf.Window(d, base, 16.0, theta,
+                                   k_profile=atf.atf_retention_profile(d, "arithmetic", 16.0, 2.0)),
+            "k64": atf.Window(d, base, 64.0, theta)}
 
 
 def _median_ms(fn, stream, warm, iters):
@@ -143,7 +154,8 @@ def config_table(atf, W, dev, stream):
     """ms, effective TFLOP/s (prefill) or GB/s (decode), fraction of the roofline and
     speedup over the same kernel at k = +inf for each of the other configurations.
     Llama tables: the effective-frequency window (default) and, as a second row,
-    the raw-base window, both on inputs rotated with the effective frequencies."""
+    the raw-base window, both on inputs rotated with the effective frequencies.
+    FAMILY_CONFIGS add the variable-k profile 16 -> 2 and uniform k = 64."""
     out = {}
     for name in PREFILL_CONFIGS:
         wl = W.WORKLOADS[name]
@@ -163,8 +175,10 @@ def config_table(atf, W, dev, stream):
         run = lambda w: atf.atf_prefill(inp["q"], kp, inp["v"], o, lse, wl.q_pos0, w,
                                         stream=stream)
         t_off = _median_ms(lambda: run(off), stream, 2, iters)
-        for tag, table in tables.items():
-            win = atf.Window(d, wl.rope_base, wl.k, table)
+        wins = {tag: atf.Window(d, wl.rope_base, wl.k, table) for tag, table in tables.items()}
+        if name in FAMILY_CONFIGS:
+            wins.update(family_windows(atf, d, wl.rope_base, tables[""]))
+        for tag, win in wins.items():
             T, C = atf.atf_count_terms(win, wl.n_q, wl.q_pos0, wl.n_k)
             flops = wl.batch * wl.h_q * (4 * T + 2 * d * C)
             t = _median_ms(lambda: run(win), stream, 2, iters)
@@ -210,8 +224,10 @@ def config_table(atf, W, dev, stream):
             atf.atf_decode(qd, kp, vp, od, lsed, wl.q_pos0, w, ws, stream=stream)
         t_off = _median_ms(lambda: run(off), stream, 3, 30)
         R_off, Cd = atf.atf_count_terms(off, 1, wl.q_pos0, wl.n_k)
-        for tag, table in tables.items():
-            win = atf.Window(d, wl.rope_base, wl.k, table)
+        wins = {tag: atf.Window(d, wl.rope_base, wl.k, table) for tag, table in tables.items()}
+        if name in FAMILY_CONFIGS:
+            wins.update(family_windows(atf, d, wl.rope_base, tables[""]))
+        for tag, win in wins.items():
             R, Cd = atf.atf_count_terms(win, 1, wl.q_pos0, wl.n_k)
             nbytes = wl.batch * wl.h_kv * (4 * R + 2 * d * Cd) + wl.batch * wl.h_q * d * 4
             t = _median_ms(lambda: run(win), stream, 3, 30)
@@ -421,6 +437,27 @@ def main():
         decode_info["full_window_GBps"] = round(
             bytes_decode_full / (full["decode_ms"] * 1e-3) / 1e9, 1)
 
+    # ---- members of the window family of App. A on the same inputs: the variable-k
+    # profile 16 -> 2 and uniform k = 64 (tab:absbench)
+    family = None
+    if not args.no_family:
+        family = {}
+        for tag, fw in family_windows(atf, d, pf.rope_base, None).items():
+            Tf, Cf = atf.atf_count_terms(fw, pf.n_q, pf.q_pos0, pf.n_k)
+            fl = B * pf.h_q * (4 * Tf + 2 * d * Cf)
+            tp = _median_ms(lambda: prefill(fw), stream, 1, args.steps)
+            Rf, Cdf = atf.atf_count_terms(fw, 1, dc.q_pos0, dc.n_k)
+            nb = dc.batch * dc.h_kv * (4 * Rf + 2 * d * Cdf) + dc.batch * dc.h_q * d * 4
+            td = _median_ms(lambda: decode(fw), stream, 3, args.decode_iters)
+            family[tag] = {
+                "prefill_ms": round(tp, 3), "prefill_qk_pruned": round(1 - Tf / (Cf * d / 2), 4),
+                "prefill_effective_tflops": round(fl / (tp * 1e-3) / 1e12, 1),
+                "prefill_speedup_vs_full_window":
+                    None if full is None else round(full["prefill_ms"] / tp, 4),
+                "decode_ms": round(td, 4), "decode_GBps": round(nb / (td * 1e-3) / 1e9, 1),
+                "decode_speedup_vs_full_window":
+                    None if full is None else round(full["decode_ms"] / td, 4)}
+
     tr = recorded_traffic("prefill_kernel<128, true>")
     roofline = {"kernel": "prefill_kernel<128, true>", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
@@ -450,7 +487,8 @@ def main():
                    "batch": B, "n_q": pf.n_q, "q_pos0": pf.q_pos0, "n_k": pf.n_k,
                    "h_q": pf.h_q, "h_kv": pf.h_kv, "head_dim": d, "rope_base": pf.rope_base,
                    "k": pf.k, "parallelism": "single GPU"},
-        "prefill": prefill_info, "decode": decode_info, "roofline": roofline,
+        "prefill": prefill_info, "decode": decode_info, "window_family": family,
+        "roofline": roofline,
         "cpu_baseline": cpu,
         "configs": configs,
     }

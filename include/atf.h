@@ -52,22 +52,56 @@ enum {
 };
 
 /* Window parameters (Sec. 3.2: k is the only free parameter; the table follows
- * from the model's RoPE constants, or from its effective frequencies). */
+ * from the model's RoPE constants, or from its effective frequencies).
+ *
+ * With family != 0 the window is the member of the family of App. A (eq:family)
+ *     w_r = min(max(k_r * lambda_r^gamma + a * (r + 1) / (d/2), beta), cap)
+ * with k_r = k_profile[r] (or k for every pair when k_profile is NULL).  The
+ * default window is k_r = k, gamma = 1, a = 0, beta = 0, cap = +INFINITY, and a
+ * zero-initialised tail (family == 0) selects it whatever the other fields hold.
+ * Examples: the variable-k profile (atf_retention_profile, 16 -> 2); uniform
+ * k = 64; a ceiling cN (cap = c * N); the sliding window of width S (k_r = 0,
+ * beta = cap = S); the linear window (k_r = 0, a = W). */
 typedef struct atf_window {
     int32_t head_dim;        /* d; 64 or 128 for the GPU entry points, any even d >= 2 for the host ones */
     double rope_base;        /* B > 1; used only when inv_freq is NULL */
-    double k;                /* retained periods, > 0; +INFINITY turns the window off */
+    double k;                /* retained periods, > 0 (>= 0 with family != 0); +INFINITY turns
+                                the window off */
     const double *inv_freq;  /* optional HOST array [d/2] of effective theta'_r >= 0
                                 (e.g. llama3 rope_scaling); NULL => theta_r = B^(-2r/d).
-                                theta'_r == 0 is a position-free pair (never pruned). */
+                                theta'_r == 0 is a position-free pair (never pruned, in the
+                                family too: App. A treats it as a knob of its own). */
+    int32_t family;          /* 0: default window; else eq:family with the fields below */
+    const double *k_profile; /* optional HOST array [d/2] of k_r >= 0 (+INFINITY allowed);
+                                NULL => k for every pair */
+    double gamma;            /* wavelength exponent, finite */
+    double a;                /* additive width in tokens (times (r+1)/(d/2)), finite, >= 0 */
+    double beta;             /* floor in tokens, finite, >= 0 */
+    double cap;              /* ceiling in tokens, >= 0; +INFINITY for none */
 } atf_window;
 
-/* Window table (Sec. 3.2 eq:window with eq:lambda): W_out[r] = floor(k*2*pi/theta_r)
- * computed in fp64 and clamped to [0, 2^31 - 1] (the clamp is exact because
- * positions stay below 2^31 - 1).  W_out: host int32 array of d/2 entries.
- * Errors: ATF_EINVAL for a NULL pointer, odd or non-positive d, k <= 0 or NaN,
- * B <= 1 (without inv_freq), or a negative/NaN inv_freq entry. */
+/* Window table (Sec. 3.2 eq:window with eq:lambda, or App. A eq:family):
+ * W_out[r] = floor(w_r) computed in fp64 and clamped to [0, 2^31 - 1] (the clamp is
+ * exact because positions stay below 2^31 - 1, and w_r >= 0 always).  Pair r is kept
+ * at distance z iff z <= W_out[r].  W_out: host int32 array of d/2 entries.
+ * Errors: ATF_EINVAL for a NULL pointer, odd or non-positive d, k <= 0 or NaN
+ * (k < 0 with family), B <= 1 (without inv_freq), a negative/NaN inv_freq or
+ * k_profile entry, a non-finite gamma, a or beta, a negative a, beta or cap, or a
+ * width that evaluates to NaN (0 * inf). */
 int atf_window_table(const atf_window *w, int32_t *W_out);
+
+/* Retention profile k_r of App. A, r = 0 (highest frequency) .. d/2 - 1, into the
+ * HOST array k_out[d/2]:
+ *   ATF_PROFILE_CONSTANT    k_r = k_hi
+ *   ATF_PROFILE_ARITHMETIC  k_r falls by (k_hi - k_lo)/(d/2 - 1) per pair, k_hi -> k_lo
+ *                           (the variable-k profile: k_hi = 16, k_lo = 2)
+ *   ATF_PROFILE_GEOMETRIC   k_r falls by the ratio (k_lo/k_hi)^(1/(d/2 - 1)) per pair
+ * With one pair (d = 2) k_r = k_hi.  Errors: ATF_EINVAL for a NULL k_out, odd or
+ * non-positive d, an unknown kind, k_hi or k_lo negative or not finite, or
+ * (geometric) k_hi or k_lo == 0. */
+enum { ATF_PROFILE_CONSTANT = 0, ATF_PROFILE_ARITHMETIC = 1, ATF_PROFILE_GEOMETRIC = 2 };
+int atf_retention_profile(int32_t head_dim, int32_t kind, double k_hi, double k_lo,
+                          double *k_out);
 
 /* Retained inner-product terms of Sec. 4 for ONE (batch, query head): the number
  * of (causal cell, pair) terms kept by the window over query rows at positions

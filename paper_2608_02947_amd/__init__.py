@@ -8,7 +8,8 @@ there is no fallback path.
 
 The functions carry the C names of ``include/atf.h``:
 
-- :func:`atf_window_table`, :func:`atf_count_terms` -- host only.
+- :func:`atf_window_table`, :func:`atf_retention_profile`, :func:`atf_count_terms`
+  -- host only.
 - :func:`atf_prefill` -- windowed prefill (chunked via ``q_pos0``).
 - :func:`atf_pack_kcache`, :func:`atf_kcache_chunk_pairs` -- decode K-cache layout.
 - :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- decode V-cache layout.
@@ -42,7 +43,10 @@ class AtfError(RuntimeError):
 
 class _CWindow(ctypes.Structure):
     _fields_ = [("head_dim", ctypes.c_int32), ("rope_base", ctypes.c_double),
-                ("k", ctypes.c_double), ("inv_freq", ctypes.c_void_p)]
+                ("k", ctypes.c_double), ("inv_freq", ctypes.c_void_p),
+                ("family", ctypes.c_int32), ("k_profile", ctypes.c_void_p),
+                ("gamma", ctypes.c_double), ("a", ctypes.c_double),
+                ("beta", ctypes.c_double), ("cap", ctypes.c_double)]
 
 
 def _load():
@@ -55,6 +59,7 @@ def _load():
     W = ctypes.POINTER(_CWindow)
     sig = {
         "atf_window_table": (ctypes.c_int, [W, P]),
+        "atf_retention_profile": (ctypes.c_int, [i32, i32, ctypes.c_double, ctypes.c_double, P]),
         "atf_count_terms": (ctypes.c_int, [W, i64, i64, i64, P, P]),
         "atf_prefill": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64, W, f32, P]),
         "atf_kcache_chunk_pairs": (ctypes.c_int32, [i32]),
@@ -74,7 +79,7 @@ def _load():
 
 
 _lib = _load()
-EXPORTED = ("atf_window_table", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
+EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache",
             "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
 
@@ -93,21 +98,60 @@ def _check(rc: int):
         raise AtfError(rc, atf_last_error())
 
 
+ATF_PROFILE_CONSTANT = 0
+ATF_PROFILE_ARITHMETIC = 1
+ATF_PROFILE_GEOMETRIC = 2
+_PROFILE_KINDS = {"constant": ATF_PROFILE_CONSTANT, "arithmetic": ATF_PROFILE_ARITHMETIC,
+                  "geometric": ATF_PROFILE_GEOMETRIC}
+
+
 @dataclasses.dataclass
 class Window:
-    """atf_window: d, RoPE base B, retained periods k (+inf = off), optional theta'_r."""
+    """atf_window: d, RoPE base B, retained periods k (+inf = off), optional theta'_r.
+
+    Any of ``k_profile``, ``gamma``, ``a``, ``beta``, ``cap`` away from the default
+    window selects the window family of App. A (eq:family):
+    w_r = min(max(k_r lambda_r^gamma + a (r+1)/(d/2), beta), cap).
+    """
     head_dim: int
     rope_base: float
     k: float
     inv_freq: Optional[Sequence[float]] = None
+    k_profile: Optional[Sequence[float]] = None
+    gamma: float = 1.0
+    a: float = 0.0
+    beta: float = 0.0
+    cap: float = math.inf
+
+    @property
+    def family(self) -> bool:
+        return (self.k_profile is not None or self.gamma != 1.0 or self.a != 0.0
+                or self.beta != 0.0 or self.cap != math.inf)
 
     def as_c(self):
-        arr = None
-        if self.inv_freq is not None:
-            arr = np.ascontiguousarray(np.asarray(self.inv_freq, dtype=np.float64))
+        def arr(x):
+            if x is None:
+                return None
+            return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+        th, kp = arr(self.inv_freq), arr(self.k_profile)
+        for x, name in ((th, "inv_freq"), (kp, "k_profile")):
+            if x is not None and x.shape != (self.head_dim // 2,):
+                raise ValueError(f"{name} must hold head_dim/2 = {self.head_dim // 2} values")
         cw = _CWindow(int(self.head_dim), float(self.rope_base), float(self.k),
-                      arr.ctypes.data if arr is not None else None)
-        return cw, arr  # keep arr alive for the duration of the call
+                      th.ctypes.data if th is not None else None, int(self.family),
+                      kp.ctypes.data if kp is not None else None, float(self.gamma),
+                      float(self.a), float(self.beta), float(self.cap))
+        return cw, (th, kp)  # keep the arrays alive for the duration of the call
+
+
+def atf_retention_profile(head_dim: int, kind: str, k_hi: float, k_lo: float = 0.0) -> np.ndarray:
+    """k_r of App. A: "constant", "arithmetic" (variable-k: 16 -> 2) or "geometric"."""
+    if kind not in _PROFILE_KINDS:
+        raise ValueError(f"unknown profile kind {kind!r}")
+    out = np.zeros(head_dim // 2 if head_dim >= 2 else 1, dtype=np.float64)
+    _check(_lib.atf_retention_profile(head_dim, _PROFILE_KINDS[kind], float(k_hi), float(k_lo),
+                                      out.ctypes.data))
+    return out
 
 
 def atf_window_table(window: Window) -> np.ndarray:

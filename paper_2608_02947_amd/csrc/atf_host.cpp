@@ -31,19 +31,33 @@ constexpr int64_t kPosLimit = 2147483647;  // positions and thresholds are int32
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// W_r = floor(k * lambda_r), lambda_r = 2*pi/theta_r (eq:lambda, eq:window), in
-// fp64, clamped to [0, 2^31 - 1].  Works for any even d <= 2 * max_pairs.
+// W_r = floor(w_r), clamped to [0, 2^31 - 1], in fp64.  The default window is
+// w_r = k * lambda_r with lambda_r = 2*pi/theta_r (eq:lambda, eq:window); with
+// `family` set, w_r = min(max(k_r * lambda_r^gamma + a (r+1)/(d/2), beta), cap)
+// (App. A eq:family).  A position-free pair (theta_r == 0) is never pruned.
+// Works for any even d <= 2 * max_pairs.
 int window_thresholds(const atf_window* w, int32_t* out, int max_pairs) {
     if (w == nullptr || out == nullptr) return fail(ATF_EINVAL, "window: NULL pointer");
     const int d = w->head_dim;
     if (d < 2 || d % 2 != 0 || d / 2 > max_pairs)
         return fail(ATF_EINVAL, "window: head_dim %d must be even, >= 2 and <= %d", d,
                     2 * max_pairs);
-    if (!(w->k > 0.0))
-        return fail(ATF_EINVAL, "window: k must be > 0 (got %g)", w->k);
+    const bool fam = w->family != 0;
+    if (fam ? !(w->k >= 0.0) : !(w->k > 0.0))
+        return fail(ATF_EINVAL, "window: k must be %s (got %g)", fam ? ">= 0" : "> 0", w->k);
     if (w->inv_freq == nullptr && !(w->rope_base > 1.0 && std::isfinite(w->rope_base)))
         return fail(ATF_EINVAL, "window: rope_base must be finite and > 1 (got %g)",
                     w->rope_base);
+    if (fam) {
+        if (!std::isfinite(w->gamma))
+            return fail(ATF_EINVAL, "window: gamma must be finite (got %g)", w->gamma);
+        if (!(w->a >= 0.0) || !std::isfinite(w->a))
+            return fail(ATF_EINVAL, "window: a must be finite and >= 0 (got %g)", w->a);
+        if (!(w->beta >= 0.0) || !std::isfinite(w->beta))
+            return fail(ATF_EINVAL, "window: beta must be finite and >= 0 (got %g)", w->beta);
+        if (!(w->cap >= 0.0))
+            return fail(ATF_EINVAL, "window: cap must be >= 0 (got %g)", w->cap);
+    }
     const double two_pi = 6.283185307179586476925286766559;
     for (int r = 0; r < d / 2; ++r) {
         double theta;
@@ -55,9 +69,21 @@ int window_thresholds(const atf_window* w, int32_t* out, int max_pairs) {
         } else {
             theta = std::pow(w->rope_base, -2.0 * r / d);
         }
-        const double lambda = two_pi / theta;  // +inf for a position-free pair
-        const double kl = w->k * lambda;
-        double t = std::floor(kl);
+        double width;
+        if (theta == 0.0) {
+            width = HUGE_VAL;  // no wavelength: every distance keeps the pair
+        } else if (!fam) {
+            width = w->k * (two_pi / theta);
+        } else {
+            const double kr = w->k_profile ? w->k_profile[r] : w->k;
+            if (!(kr >= 0.0))
+                return fail(ATF_EINVAL, "window: k_profile[%d] = %g must be >= 0", r, kr);
+            width = kr * std::pow(two_pi / theta, w->gamma) + w->a * (r + 1) / (d / 2);
+            if (std::isnan(width))
+                return fail(ATF_EINVAL, "window: the width of pair %d is undefined (0 * inf)", r);
+            width = std::fmin(std::fmax(width, w->beta), w->cap);
+        }
+        double t = std::floor(width);
         if (!(t < static_cast<double>(kPosLimit))) t = static_cast<double>(kPosLimit);
         if (t < 0.0) t = 0.0;
         out[r] = static_cast<int32_t>(t);
@@ -147,6 +173,38 @@ const char* atf_last_error(void) { return g_last_error.c_str(); }
 
 int atf_window_table(const atf_window* w, int32_t* W_out) {
     return window_thresholds(w, W_out, 1 << 20);
+}
+
+int atf_retention_profile(int32_t head_dim, int32_t kind, double k_hi, double k_lo,
+                          double* k_out) {
+    if (k_out == nullptr) return fail(ATF_EINVAL, "retention_profile: NULL output");
+    if (head_dim < 2 || head_dim % 2 != 0)
+        return fail(ATF_EINVAL, "retention_profile: head_dim %d must be even and >= 2", head_dim);
+    if (!(k_hi >= 0.0) || !std::isfinite(k_hi) || !(k_lo >= 0.0) || !std::isfinite(k_lo))
+        return fail(ATF_EINVAL, "retention_profile: k_hi, k_lo must be finite and >= 0");
+    const int n = head_dim / 2;
+    const double span = n > 1 ? double(n - 1) : 1.0;
+    switch (kind) {
+        case ATF_PROFILE_CONSTANT:
+            for (int r = 0; r < n; ++r) k_out[r] = k_hi;
+            return ATF_OK;
+        case ATF_PROFILE_ARITHMETIC: {
+            const double step = (k_hi - k_lo) / span;
+            for (int r = 0; r < n; ++r) k_out[r] = k_hi - step * r;
+            if (n > 1) k_out[n - 1] = k_lo;
+            return ATF_OK;
+        }
+        case ATF_PROFILE_GEOMETRIC: {
+            if (!(k_hi > 0.0) || !(k_lo > 0.0))
+                return fail(ATF_EINVAL, "retention_profile: geometric needs k_hi, k_lo > 0");
+            const double lr = std::log(k_lo / k_hi) / span;
+            for (int r = 0; r < n; ++r) k_out[r] = k_hi * std::exp(lr * r);
+            if (n > 1) k_out[n - 1] = k_lo;
+            return ATF_OK;
+        }
+        default:
+            return fail(ATF_EINVAL, "retention_profile: unknown kind %d", kind);
+    }
 }
 
 int atf_count_terms(const atf_window* w, int64_t n_q, int64_t q_pos0, int64_t n_k,

@@ -34,6 +34,34 @@ def windows_for(head_dim, rope_base, k, theta, n_ctx):
             oracle.window_widths(head_dim, rope_base, k, th, n_ctx=n_ctx))
 
 
+# members of the window family of App. A (eq:family) used by the GPU tests:
+# name -> (profile (kind, k_hi, k_lo), gamma, a, beta, cap)
+FAMILIES = {
+    "var16to2": (("arithmetic", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "geo16to2": (("geometric", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "k64": (("constant", 64.0, 0.0), 1.0, 0.0, 0.0, math.inf),
+    "k2_floor40_cap180": (("constant", 2.0, 0.0), 1.0, 0.0, 40.0, 180.0),
+    "gamma0.8": (("constant", 2.0, 0.0), 0.8, 0.0, 0.0, math.inf),
+    "gamma1.25": (("constant", 2.0, 0.0), 1.25, 0.0, 0.0, math.inf),
+    "sliding100": (("constant", 0.0, 0.0), 1.0, 0.0, 100.0, 100.0),
+    "linear256": (("constant", 0.0, 0.0), 1.0, 256.0, 0.0, math.inf),
+}
+
+
+def family_windows_for(head_dim, rope_base, theta, family):
+    """(GPU window, oracle widths) of a window-family member, built independently
+    on each side (the library's profile and table, the oracle's profile and widths)."""
+    import paper_2608_02947_amd as atf
+    (kind, hi, lo), gamma, a, beta, cap = FAMILIES[family]
+    th = None if theta is None else np.asarray(theta, dtype=np.float64)
+    win = atf.Window(head_dim, rope_base, hi, th,
+                     k_profile=atf.atf_retention_profile(head_dim, kind, hi, lo),
+                     gamma=gamma, a=a, beta=beta, cap=cap)
+    widths = oracle.family_widths(head_dim, rope_base, oracle.retention_profile(head_dim, kind, hi, lo),
+                                  gamma=gamma, a=a, beta=beta, cap=cap, theta=th)
+    return win, widths
+
+
 def gpu_prefill(q, k, v, q_pos0, win, scale=0.0, kp=None, n_k=None):
     """q [B, n_q, h_q, d]; k, v [B, C, h_kv, d] (K is packed pair-chunk-major by the
     library first unless kp is given); keys 0 .. n_k - 1 (default C) are used."""
@@ -123,8 +151,11 @@ def sample_rows(batch, n_q, h_q, n_rows, seed, tile=128):
     return np.array(rows, dtype=np.int64)
 
 
-def workload_window(wl: W.Workload, k=None):
+def workload_window(wl: W.Workload, k=None, family=None):
     th = W.workload_theta(wl)
+    if family is not None:
+        return family_windows_for(wl.head_dim, wl.rope_base, None if th is None else th.numpy(),
+                                  family)
     return windows_for(wl.head_dim, wl.rope_base, wl.k if k is None else k,
                        None if th is None else th.numpy(),
                        n_ctx=max(wl.n_k, wl.q_pos0 + wl.n_q))

@@ -118,6 +118,92 @@ def test_window_validation():
     assert t[1] == 2 ** 31 - 1 and t[0] == math.floor(4 * math.pi)
 
 
+# window family of App. A: the library's table and counts against the oracle's
+# widths, built independently on each side
+FAMILY_CASES = {
+    # name: (d, base, theta-kind, profile (kind, hi, lo), gamma, a, beta, cap)
+    "var16to2_qwen05b": (64, 1e6, None, ("arithmetic", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "var16to2_qwen7b": (128, 1e7, None, ("arithmetic", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "var16to2_llama3": (128, 5e5, "llama3", ("arithmetic", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "geo16to2_qwen7b": (128, 1e7, None, ("geometric", 16.0, 2.0), 1.0, 0.0, 0.0, math.inf),
+    "k64_qwen7b": (128, 1e7, None, ("constant", 64.0, 0.0), 1.0, 0.0, 0.0, math.inf),
+    "cap_0.25N_32k": (64, 1e6, None, ("constant", 2.0, 0.0), 1.0, 0.0, 0.0, 8192.0),
+    "floor_and_cap": (128, 5e5, None, ("constant", 2.0, 0.0), 1.0, 0.0, 100.0, 50000.0),
+    "gamma_0.8": (128, 1e7, None, ("constant", 2.0, 0.0), 0.8, 0.0, 0.0, math.inf),
+    "gamma_1.25": (64, 1e6, None, ("constant", 2.0, 0.0), 1.25, 0.0, 0.0, math.inf),
+    "sliding_300": (64, 1e6, None, ("constant", 0.0, 0.0), 1.0, 0.0, 300.0, 300.0),
+    "linear_4096": (128, 1e7, None, ("constant", 0.0, 0.0), 1.0, 4096.0, 0.0, math.inf),
+    "additive_and_var": (64, 1e4, None, ("arithmetic", 8.0, 1.0), 1.0, 77.5, 0.0, math.inf),
+}
+
+
+def _family_pair(oracle_lib, case):
+    d, base, tk, (kind, hi, lo), gamma, a, beta, cap = FAMILY_CASES[case]
+    th = W.llama3_theta(d, base).numpy() if tk == "llama3" else None
+    prof = oracle_lib.retention_profile(d, kind, hi, lo)
+    widths = oracle_lib.family_widths(d, base, prof, gamma=gamma, a=a, beta=beta, cap=cap,
+                                      theta=th)
+    win = atf.Window(d, base, hi, th, k_profile=atf.atf_retention_profile(d, kind, hi, lo),
+                     gamma=gamma, a=a, beta=beta, cap=cap)
+    return win, widths
+
+
+@pytest.mark.parametrize("case", sorted(FAMILY_CASES))
+def test_family_table_and_counts_match_oracle(oracle_lib, case):
+    win, widths = _family_pair(oracle_lib, case)
+    got = atf.atf_window_table(win).astype(np.int64)
+    exp = np.minimum(np.floor(widths), 2 ** 31 - 1).astype(np.int64)
+    assert np.array_equal(got, exp)
+    for n_q, q0, n_k in [(16384, 0, 16384), (4096, 126976, 131072), (1, 1 << 20, 1 << 20),
+                         (300, 0, 200)]:
+        assert atf.atf_count_terms(win, n_q, q0, n_k) == oracle_lib.count_terms(widths, n_q, q0, n_k)
+
+
+@pytest.mark.parametrize("kind", ["constant", "arithmetic", "geometric"])
+@pytest.mark.parametrize("d", [2, 8, 64, 128])
+def test_retention_profile_matches_oracle(oracle_lib, kind, d):
+    got = atf.atf_retention_profile(d, kind, 16.0, 2.0)
+    np.testing.assert_allclose(got, oracle_lib.retention_profile(d, kind, 16.0, 2.0),
+                               rtol=1e-14, atol=0)
+
+
+def test_family_defaults_and_validation():
+    # the zero-initialised tail (family == 0) is the default window
+    cw, keep = atf.Window(64, 1e6, 2.0).as_c()
+    assert cw.family == 0 and not cw.k_profile and cw.gamma == 1.0
+    cw.gamma, cw.beta = 7.0, 1e9  # ignored while family == 0
+    t = np.zeros(32, dtype=np.int32)
+    assert atf.library().atf_window_table(ctypes.byref(cw), t.ctypes.data) == 0
+    assert np.array_equal(t, atf.atf_window_table(atf.Window(64, 1e6, 2.0)))
+    # the family at its default point equals the default window
+    same = atf.Window(64, 1e6, 2.0, k_profile=np.full(32, 2.0))
+    assert same.family
+    assert np.array_equal(atf.atf_window_table(same), t)
+    # k = 0 is allowed only in the family
+    assert np.all(atf.atf_window_table(atf.Window(8, 1e4, 0.0, beta=5.0)) == 5)
+    bad = [atf.Window(8, 1e4, 2.0, gamma=math.inf), atf.Window(8, 1e4, 2.0, gamma=math.nan),
+           atf.Window(8, 1e4, 2.0, a=-1.0), atf.Window(8, 1e4, 2.0, a=math.inf),
+           atf.Window(8, 1e4, 2.0, beta=-1.0), atf.Window(8, 1e4, 2.0, beta=math.inf),
+           atf.Window(8, 1e4, 2.0, cap=-1.0), atf.Window(8, 1e4, 2.0, cap=math.nan),
+           atf.Window(8, 1e4, -1.0, beta=1.0),
+           atf.Window(8, 1e4, 2.0, k_profile=[1.0, -1.0, 1.0, 1.0]),
+           atf.Window(8, 1e4, 2.0, k_profile=[1.0, math.nan, 1.0, 1.0]),
+           atf.Window(8, 1e4, 2.0, k_profile=[0.0, 1.0, 1.0, 1.0], gamma=1e6)]  # 0 * inf
+    for w in bad:
+        with pytest.raises(atf.AtfError) as e:
+            atf.atf_window_table(w)
+        assert e.value.code == atf.ATF_EINVAL and "window" in atf.atf_last_error()
+    with pytest.raises(ValueError):
+        atf.Window(8, 1e4, 2.0, k_profile=[1.0, 2.0]).as_c()
+    lib = atf.library()
+    out = np.zeros(4)
+    assert lib.atf_retention_profile(8, 9, 16.0, 2.0, out.ctypes.data) == atf.ATF_EINVAL
+    assert lib.atf_retention_profile(7, 1, 16.0, 2.0, out.ctypes.data) == atf.ATF_EINVAL
+    assert lib.atf_retention_profile(8, 2, 16.0, 0.0, out.ctypes.data) == atf.ATF_EINVAL
+    assert lib.atf_retention_profile(8, 1, -1.0, 2.0, out.ctypes.data) == atf.ATF_EINVAL
+    assert lib.atf_retention_profile(8, 1, 16.0, 2.0, None) == atf.ATF_EINVAL
+
+
 def _raw_prefill(lib, cw, **kw):
     args = dict(q=16, k=16, v=16, o=16, lse=16, batch=1, n_q=4, n_k=4, q_pos0=0, h_q=2, h_kv=1,
                 cache_tokens=0)

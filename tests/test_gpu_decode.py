@@ -14,8 +14,8 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, gpu_decode, note, pack_kcache, pack_vcache, to_f64, windows_for,
-                    workload_window)
+from parity import (compare, family_windows_for, gpu_decode, note, pack_kcache, pack_vcache,
+                    to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -119,6 +119,38 @@ def test_decode_nonmonotone_table():
     q, k, v = _decode_inputs(2, 2500, 2500, 6, 3, d, 0.0, seed=4, theta=theta)
     win, widths = windows_for(d, 1e4, 2.0, theta, n_ctx=2501)
     _decode_parity(q, k, v, 2500, win, widths, "nonmonotone")
+
+
+FAMILY_CASES = [
+    # family, B, n_k, q_pos, h_q, h_kv, d, base
+    ("var16to2", 2, 777, 777, 12, 1, 128, 1e4),
+    ("geo16to2", 1, 1500, 1500, 8, 1, 64, 1e6),
+    ("k64", 1, 3000, 3000, 6, 2, 128, 5e5),
+    ("k2_floor40_cap180", 1, 3000, 3000, 6, 2, 128, 5e5),
+    ("gamma1.25", 3, 1000, 1000, 7, 1, 64, 1e6),
+    ("sliding100", 1, 1500, 1500, 8, 1, 128, 1e4),   # every pair pruned past 100
+    ("linear256", 1, 2049, 2049, 4, 2, 64, 1e4),
+]
+
+
+@pytest.mark.parametrize("case", FAMILY_CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_decode_window_family(case):
+    """Members of the window family of App. A (eq:family)."""
+    fam, B, n_k, q_pos, h_q, h_kv, d, base = case
+    q, k, v = _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed=hash(case) % 10000)
+    win, widths = family_windows_for(d, base, None, fam)
+    _decode_parity(q, k, v, q_pos, win, widths, f"family{case}")
+
+
+@pytest.mark.parametrize("name,family", [("qwen7b1m_decode", "var16to2"),
+                                         ("qwen7b1m_decode", "k64"),
+                                         ("llama3b_decode_128k", "var16to2")])
+def test_decode_family_workload_all_rows(name, family):
+    wl = W.WORKLOADS[name]
+    note(f"generate {name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl, family=family)
+    _decode_parity(inp["q"], inp["k"], inp["v"], wl.q_pos0, win, widths, f"{name} {family}")
 
 
 @pytest.mark.parametrize("name", ["llama3b_decode_32k", "llama3b_decode_128k", "qwen7b1m_decode"])

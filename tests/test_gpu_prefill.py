@@ -14,8 +14,8 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, gpu_prefill, note, pack_kcache, sample_rows, to_f64, windows_for,
-                    workload_window)
+from parity import (compare, family_windows_for, gpu_prefill, note, pack_kcache, sample_rows,
+                    to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -98,6 +98,61 @@ def test_prefill_qwen_1k_workload_all_rows():
     # k = inf equals the oracle of ordinary causal attention
     win_inf, widths_inf = workload_window(wl, k=math.inf)
     _full_parity(inp["q"], inp["k"], inp["v"], 0, win_inf, widths_inf, wl.name + " k=inf")
+
+
+FAMILY_CASES = [
+    # family, B, n_q, n_k, q0, h_q, h_kv, d, base
+    ("var16to2", 2, 260, 260, 0, 4, 4, 64, 1e6),
+    ("geo16to2", 1, 300, 300, 0, 6, 2, 128, 5e5),
+    ("k64", 1, 333, 500, 167, 16, 2, 64, 1e4),
+    ("k2_floor40_cap180", 1, 333, 500, 167, 16, 2, 64, 1e4),   # floor and ceiling bind
+    ("gamma0.8", 1, 300, 300, 0, 6, 2, 128, 5e5),
+    ("gamma1.25", 1, 200, 450, 250, 8, 1, 128, 1e4),
+    ("sliding100", 1, 300, 300, 0, 4, 2, 128, 1e4),            # empty sums past 100
+    ("sliding100", 2, 190, 190, 0, 2, 1, 64, 1e4),
+    ("linear256", 1, 400, 400, 0, 2, 1, 128, 1e4),
+]
+
+
+@pytest.mark.parametrize("case", FAMILY_CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_window_family_all_rows(case):
+    """Members of the window family of App. A (eq:family): every output element."""
+    fam, B, n_q, n_k, q0, h_q, h_kv, d, base = case
+    q, k, v = _small_inputs(B, n_q, n_k, q0, h_q, h_kv, d, base, seed=hash(case) % 10000)
+    win, widths = family_windows_for(d, base, None, fam)
+    _full_parity(q, k, v, q0, win, widths, f"family{case}")
+
+
+def test_prefill_variable_k_workloads_all_rows():
+    """The variable-k profile 16 -> 2 on the 1K Qwen2.5-0.5B-shaped workload and on
+    700 rows of the Llama-3.2-3B shape (llama3-effective frequencies)."""
+    wl = W.WORKLOADS["qwen05b_prefill_1k"]
+    inp = W.make_inputs(wl)
+    win, widths = workload_window(wl, family="var16to2")
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, wl.name + " var16to2")
+    wl = W.WORKLOADS["llama3b_prefill_32k"]
+    inp = W.make_inputs(wl, n_k=700, n_q=700, q_pos0=0)
+    win, widths = workload_window(wl, family="var16to2")
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, "llama3 700 var16to2")
+
+
+@pytest.mark.parametrize("name,family", [("qwen05b_prefill_32k", "var16to2"),
+                                         ("qwen7b1m_prefill_chunk", "var16to2"),
+                                         ("llama3b_prefill_128k", "k64")])
+def test_prefill_family_workload_sampled_rows(name, family):
+    """Full-size workloads under a window-family member; sampled rows."""
+    wl = W.WORKLOADS[name]
+    note(f"generate {name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl, family=family)
+    note(f"prefill {name} {family}")
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], wl.q_pos0, win)
+    rows = sample_rows(wl.batch, wl.n_q, wl.h_q, 32, seed=wl.seed + 1)
+    q_c, k_c, v_c = inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu()
+    o_ref, lse_ref, _ = oracle.attend(q_c, k_c, v_c, wl.q_pos0, widths, rows=rows)
+    og = torch.stack([o[b, i, h] for b, h, i in rows]).float().cpu().numpy()
+    lg = torch.stack([lse[b, h, i] for b, h, i in rows]).cpu().numpy()
+    compare(og, lg, o_ref, lse_ref, f"{name} {family}")
 
 
 @pytest.mark.parametrize("name", ["qwen05b_prefill_8k", "qwen05b_prefill_32k",
