@@ -62,12 +62,13 @@ def _load():
         lib.oracle_window_widths.argtypes = [i64, dbl, dbl, p, dbl, p]
         lib.oracle_family_widths.argtypes = [i64, dbl, p, p, dbl, dbl, dbl, dbl, p]
         lib.oracle_scores.argtypes = [p, p, ctypes.c_int, i64, i64, i64, i64, i64, i64,
-                                      i64, p, dbl, i64, i64, p]
+                                      i64, p, i64, dbl, i64, i64, p]
         lib.oracle_attend.argtypes = [p, p, p, ctypes.c_int, i64, i64, i64, i64, i64, i64,
-                                      i64, p, dbl, i64, p, p, p, p, ctypes.c_int]
+                                      i64, p, i64, dbl, i64, p, p, p, p, ctypes.c_int]
         lib.oracle_count_terms.argtypes = [p, i64, i64, i64, i64, p, p]
+        lib.oracle_count_terms_by_distance.argtypes = [p, i64, i64, i64, i64, i64, p, p]
         for f in (lib.oracle_window_widths, lib.oracle_family_widths, lib.oracle_scores,
-                  lib.oracle_attend, lib.oracle_count_terms):
+                  lib.oracle_attend, lib.oracle_count_terms, lib.oracle_count_terms_by_distance):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -151,8 +152,10 @@ def family_widths(head_dim: int, rope_base: float, k_profile, gamma: float = 1.0
     return w
 
 
-def scores(q, k, q_pos0: int, widths, b: int = 0, hq: int = 0, scale=None) -> np.ndarray:
-    """Windowed scaled scores [n_q, n_k] of one (batch, query head); -inf above the diagonal."""
+def scores(q, k, q_pos0: int, widths, b: int = 0, hq: int = 0, scale=None,
+           atom: int = 0) -> np.ndarray:
+    """Windowed scaled scores [n_q, n_k] of one (batch, query head); -inf above the diagonal.
+    atom > 0: the rounded slice of Sec. 3.3 (kept slice rounded up to atom-pair steps)."""
     lib = _load()
     qa, dt = _as_input(q)
     ka, dt2 = _as_input(k)
@@ -163,7 +166,7 @@ def scores(q, k, q_pos0: int, widths, b: int = 0, hq: int = 0, scale=None) -> np
     sc = 1.0 / math.sqrt(d) if scale is None else float(scale)
     out = np.empty((n_q, n_k), dtype=np.float64)
     rc = lib.oracle_scores(_ptr(qa), _ptr(ka), dt, B, n_q, n_k, q_pos0, h_q, h_kv, d,
-                           _ptr(w), sc, b, hq, _ptr(out))
+                           _ptr(w), int(atom), sc, b, hq, _ptr(out))
     if rc != 0:
         raise ValueError("oracle_scores: bad arguments")
     return out
@@ -175,8 +178,12 @@ def all_rows(batch: int, n_q: int, h_q: int) -> np.ndarray:
     return np.stack([b.ravel(), h.ravel(), i.ravel()], axis=1).astype(np.int64)
 
 
-def attend(q, k, v, q_pos0: int, widths, scale=None, rows=None, threads: int = 0):
+def attend(q, k, v, q_pos0: int, widths, scale=None, rows=None, threads: int = 0,
+           atom: int = 0):
     """Windowed causal attention in fp64.
+
+    atom > 0 applies the rounded slice of Sec. 3.3: at each distance the kept
+    low-frequency slice is rounded up to a whole number of atom-pair K-steps.
 
     q [B, n_q, h_q, d], k/v [B, n_k, h_kv, d] (bf16 torch tensors, uint16 bf16
     bits, or float arrays).  ``rows`` is an (n, 3) array of (b, hq, i); None
@@ -201,7 +208,7 @@ def attend(q, k, v, q_pos0: int, widths, scale=None, rows=None, threads: int = 0
     lse = np.empty(n, dtype=np.float64)
     terms = np.empty(n, dtype=np.uint64)
     rc = lib.oracle_attend(_ptr(qa), _ptr(ka), _ptr(va), dt, B, n_q, n_k, q_pos0, h_q, h_kv, d,
-                           _ptr(w), sc, n, _ptr(r), _ptr(o), _ptr(lse), _ptr(terms),
+                           _ptr(w), int(atom), sc, n, _ptr(r), _ptr(o), _ptr(lse), _ptr(terms),
                            int(threads))
     if rc != 0:
         raise ValueError("oracle_attend: bad arguments")
@@ -212,13 +219,21 @@ def attend(q, k, v, q_pos0: int, widths, scale=None, rows=None, threads: int = 0
     return o, lse, terms
 
 
-def count_terms(widths, n_q: int, q_pos0: int, n_k: int):
-    """(retained terms, causal cells) of one (batch, query head), Sec. 4."""
+def count_terms(widths, n_q: int, q_pos0: int, n_k: int, atom: int = 0, by_distance=None):
+    """(retained terms, causal cells) of one (batch, query head), Sec. 4.
+
+    atom == 0: per pair and row in closed form.  atom > 0 (the rounded slice of
+    Sec. 3.3), or by_distance=True: summed over distances z with the pairs kept at z.
+    """
     lib = _load()
     w = np.ascontiguousarray(widths, dtype=np.float64)
     ret = np.zeros(1, dtype=np.uint64)
     cau = np.zeros(1, dtype=np.uint64)
-    rc = lib.oracle_count_terms(_ptr(w), w.shape[0], n_q, q_pos0, n_k, _ptr(ret), _ptr(cau))
+    if atom > 0 or by_distance:
+        rc = lib.oracle_count_terms_by_distance(_ptr(w), w.shape[0], int(atom), n_q, q_pos0,
+                                                n_k, _ptr(ret), _ptr(cau))
+    else:
+        rc = lib.oracle_count_terms(_ptr(w), w.shape[0], n_q, q_pos0, n_k, _ptr(ret), _ptr(cau))
     if rc != 0:
         raise ValueError("oracle_count_terms: bad arguments")
     return int(ret[0]), int(cau[0])

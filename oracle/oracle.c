@@ -20,6 +20,8 @@
  *     kept only when z <= w_r (Sec. 3.2); the kept terms are summed and scaled
  *     by 1/sqrt(d) (or a caller scale).  An empty sum is 0: tokens are never
  *     dropped, only terms.
+ *   - optionally the rounded slice of Sec. 3.3: at each distance the kept
+ *     low-frequency slice is rounded up to a whole number of MMA K-steps.
  *   - causal softmax over keys m <= n and the weighted sum of V rows, done as a
  *     plain two-pass softmax (max, then sum of exponentials); LSE = m + ln(l).
  *   - the retained-term count of Sec. 4: the number of kept (cell, pair)
@@ -120,26 +122,62 @@ int oracle_family_widths(int64_t d, double base, const double *theta, const doub
 }
 
 /*
+ * Pairs kept at distance z.  atom == 0: the window itself, pair r is kept iff
+ * z <= w_r (Sec. 3.2).  atom > 0: the rounded slice of Sec. 3.3: the pairs the
+ * window keeps form a slice on the low-frequency side (the largest r); its length
+ * n = #{r : z <= w_r} is rounded up to a whole number of K-steps of `atom` pairs,
+ * n' = min(h, atom * ceil(n / atom)), and the kept pairs are r >= h - n'.
+ * keep[r] receives 1 for a kept pair; returns the number kept.
+ */
+static int64_t kept_set(double z, const double *w, int64_t h, int64_t atom, unsigned char *keep)
+{
+    int64_t n = 0;
+    for (int64_t r = 0; r < h; ++r)
+        n += z <= w[r];
+    if (atom <= 0) {
+        for (int64_t r = 0; r < h; ++r)
+            keep[r] = z <= w[r];
+        return n;
+    }
+    int64_t nr = atom * ((n + atom - 1) / atom);
+    if (nr > h)
+        nr = h;
+    for (int64_t r = 0; r < h; ++r)
+        keep[r] = r >= h - nr;
+    return nr;
+}
+
+/* The rounded slice is defined for a window whose kept pairs are a suffix in r:
+ * widths non-decreasing in r. */
+static int widths_monotone(const double *w, int64_t h)
+{
+    for (int64_t r = 1; r < h; ++r)
+        if (!(w[r] >= w[r - 1]))
+            return 0;
+    return 1;
+}
+
+/*
  * Windowed score of one cell: (1/sqrt(d) or scale) * sum over kept pairs of
- * q[r]k[r] + q[r+h]k[r+h] (eq:pair with the keep rule of Sec. 3.2).
+ * q[r]k[r] + q[r+h]k[r+h] (eq:pair with the keep rule of Sec. 3.2, or the
+ * rounded slice of Sec. 3.3 when atom > 0).
  * qd holds the query row in fp64; krow points at the key row.
  * *kept receives the number of kept pairs.
  */
 static double cell_score(const double *qd, const void *k, int64_t krow_off, int kdt,
-                         int64_t d, double z, const double *w, double scale,
+                         int64_t d, double z, const double *w, int64_t atom, double scale,
                          int64_t *kept)
 {
     const int64_t h = d / 2;
+    unsigned char keep[512];
+    *kept = kept_set(z, w, h, atom, keep);
     double x = 0.0;
-    int64_t t = 0;
     for (int64_t r = 0; r < h; ++r) {
-        if (z <= w[r]) {
+        if (keep[r]) {
             x += qd[r] * load_elem(k, krow_off + r, kdt)
                + qd[r + h] * load_elem(k, krow_off + r + h, kdt);
-            ++t;
         }
     }
-    *kept = t;
     return x * scale;
 }
 
@@ -152,11 +190,11 @@ static double cell_score(const double *qd, const void *k, int64_t krow_off, int 
 int oracle_scores(const void *q, const void *k, int dtype,
                   int64_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
                   int64_t h_q, int64_t h_kv, int64_t d,
-                  const double *w, double scale, int64_t b, int64_t hq,
+                  const double *w, int64_t atom, double scale, int64_t b, int64_t hq,
                   double *s_out)
 {
     if (d <= 0 || d % 2 || h_kv <= 0 || h_q % h_kv || b < 0 || b >= batch ||
-        hq < 0 || hq >= h_q || d > 1024)
+        hq < 0 || hq >= h_q || d > 1024 || (atom > 0 && !widths_monotone(w, d / 2)))
         return -1;
     const int64_t g = hq / (h_q / h_kv);
     double qd[1024];
@@ -173,14 +211,14 @@ int oracle_scores(const void *q, const void *k, int dtype,
             int64_t kept;
             const int64_t koff = ((b * n_k + j) * h_kv + g) * d;
             s_out[i * n_k + j] = cell_score(qd, k, koff, dtype, d, (double)(p - j),
-                                            w, scale, &kept);
+                                            w, atom, scale, &kept);
         }
     }
     return 0;
 }
 
 /*
- * Windowed causal attention for a list of query rows.
+ * Windowed causal attention for a list of query rows (atom: see kept_set).
  *   rows: n_rows triples (b, hq, i); row i sits at position q_pos0 + i and
  *         attends keys j = 0 .. min(q_pos0 + i, n_k - 1).
  *   o_out [n_rows][d], lse_out [n_rows], terms_out [n_rows] (may be NULL).
@@ -189,13 +227,14 @@ int oracle_scores(const void *q, const void *k, int dtype,
 int oracle_attend(const void *q, const void *k, const void *v, int dtype,
                   int64_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
                   int64_t h_q, int64_t h_kv, int64_t d,
-                  const double *w, double scale,
+                  const double *w, int64_t atom, double scale,
                   int64_t n_rows, const int64_t *rows,
                   double *o_out, double *lse_out, uint64_t *terms_out,
                   int n_threads)
 {
     if (d <= 0 || d % 2 || d > 1024 || h_kv <= 0 || h_q % h_kv || n_k <= 0 ||
-        q_pos0 < 0 || rows == NULL || o_out == NULL || lse_out == NULL)
+        q_pos0 < 0 || rows == NULL || o_out == NULL || lse_out == NULL ||
+        (atom > 0 && !widths_monotone(w, d / 2)))
         return -1;
     for (int64_t t = 0; t < n_rows; ++t) {
         const int64_t b = rows[3 * t], hq = rows[3 * t + 1], i = rows[3 * t + 2];
@@ -234,7 +273,8 @@ int oracle_attend(const void *q, const void *k, const void *v, int dtype,
             for (int64_t j = 0; j <= last; ++j) {
                 int64_t kept;
                 const int64_t koff = ((b * n_k + j) * h_kv + g) * d;
-                s[j] = cell_score(qd, k, koff, dtype, d, (double)(p - j), w, scale, &kept);
+                s[j] = cell_score(qd, k, koff, dtype, d, (double)(p - j), w, atom, scale,
+                                  &kept);
                 kept_total += (uint64_t)kept;
                 if (s[j] > m)
                     m = s[j];
@@ -269,6 +309,41 @@ int oracle_attend(const void *q, const void *k, const void *v, int dtype,
  * with p - j <= w_r, i.e. j >= p - floor(w_r); their number is the length of
  * that integer interval.  *causal_out is the number of causal cells.
  */
+int oracle_count_terms(const double *w, int64_t n_pairs, int64_t n_q, int64_t q_pos0,
+                       int64_t n_k, uint64_t *retained_out, uint64_t *causal_out);
+
+/*
+ * The same count with the keep rule of kept_set (atom > 0: the rounded slice of
+ * Sec. 3.3), summed by distance: the cells at distance z are the rows p in
+ * [max(q_pos0, z), min(q_pos0 + n_q - 1, z + n_k - 1)] (key j = p - z must lie in
+ * [0, n_k - 1]), and each keeps kept_set(z) pairs.
+ */
+int oracle_count_terms_by_distance(const double *w, int64_t n_pairs, int64_t atom,
+                                   int64_t n_q, int64_t q_pos0, int64_t n_k,
+                                   uint64_t *retained_out, uint64_t *causal_out)
+{
+    if (n_pairs <= 0 || n_pairs > 512 || n_q < 0 || q_pos0 < 0 || n_k < 0 ||
+        retained_out == NULL || causal_out == NULL ||
+        (atom > 0 && !widths_monotone(w, n_pairs)))
+        return -1;
+    const int64_t p0 = q_pos0, p1 = q_pos0 + n_q - 1;
+    uint64_t retained = 0, causal = 0;
+#pragma omp parallel for reduction(+ : retained, causal) schedule(static)
+    for (int64_t z = 0; z <= p1; ++z) {
+        const int64_t lo = p0 > z ? p0 : z;
+        const int64_t hi = p1 < z + n_k - 1 ? p1 : z + n_k - 1;
+        if (hi < lo)
+            continue;
+        unsigned char keep[512];
+        const int64_t kept = kept_set((double)z, w, n_pairs, atom, keep);
+        causal += (uint64_t)(hi - lo + 1);
+        retained += (uint64_t)(hi - lo + 1) * (uint64_t)kept;
+    }
+    *retained_out = retained;
+    *causal_out = causal;
+    return 0;
+}
+
 int oracle_count_terms(const double *w, int64_t n_pairs, int64_t n_q, int64_t q_pos0,
                        int64_t n_k, uint64_t *retained_out, uint64_t *causal_out)
 {

@@ -294,7 +294,7 @@ def _pruned(oracle_lib, rec):
     base = float(f["base"])
     N = int(f["N"])
     theta = W.llama3_theta(d, base).numpy() if rec[1] == "llama3b" else None
-    qty = rec[5]
+    qty = next(x for x in rec[2:] if "=" not in x)  # the quantity's name
     if "to" in f["k"]:  # k-arithmetic retention profile k_hi -> k_lo (App. A)
         hi, lo = (float(x) for x in f["k"].split("to"))
         assert qty == "pruned_prefill"
@@ -303,6 +303,14 @@ def _pruned(oracle_lib, rec):
         T, C = oracle_lib.count_terms(w, N, 0, N)
         return 100.0 * (1 - T / (C * d / 2))
     kwin = float(f["k"])
+    if "atom" in f:  # the rounded slice of Sec. 3.3
+        w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
+        T, C = oracle_lib.count_terms(w, N, 0, N, atom=int(f["atom"]))
+        s = T / (C * d / 2)
+        if qty == "ceiling":
+            return 2.0 / (1.0 + s)
+        assert qty == "pruned_prefill"
+        return 100.0 * (1 - s)
     if qty == "pruned_prefill":
         w = oracle_lib.window_widths(d, base, kwin, theta, n_ctx=N)
         T, C = oracle_lib.count_terms(w, N, 0, N)
@@ -533,3 +541,75 @@ def test_family_floor_and_ceiling(oracle_lib):
     assert np.all(s[z > cap] == 0.0)
     with pytest.raises(ValueError):   # 0 * inf: the width is undefined
         oracle_lib.family_widths(4, 10.0, [0.0, 1.0], gamma=1e6)
+
+
+# ----------------------------------------------------------------------------
+# rounded slice of Sec. 3.3 (kept low-frequency slice rounded up to MMA K-steps)
+# ----------------------------------------------------------------------------
+def test_rounded_slice_exact_window_misses_the_printed_ceilings(oracle_lib):
+    """tab:c2e2e and the abstract's 57 % fit the rounded slice, not the exact window."""
+    w = oracle_lib.window_widths(128, 1e7, 2.0)
+    for N, ceil_printed in [(262144, 1.31), (524288, 1.35), (1048576, 1.40)]:
+        T, C = oracle_lib.count_terms(w, N, 0, N)
+        s = T / (C * 64)
+        assert 2 / (1 + s) - ceil_printed > 0.04
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_rounded_slice_atom1_is_the_window_and_counts_agree(oracle_lib, seed):
+    """atom = 1 rounds nothing; the by-distance count equals the per-pair closed form
+    and brute force; rounded counts are at least the exact ones."""
+    rng = np.random.default_rng(100 + seed)
+    h = int(rng.integers(1, 20))
+    w = np.sort(rng.uniform(-1, 60, h))
+    n_q, q0, n_k = int(rng.integers(0, 40)), int(rng.integers(0, 50)), int(rng.integers(0, 70))
+    exact = oracle_lib.count_terms(w, n_q, q0, n_k)
+    assert oracle_lib.count_terms(w, n_q, q0, n_k, by_distance=True) == exact
+    assert oracle_lib.count_terms(w, n_q, q0, n_k, atom=1) == exact
+    assert exact == brute_force_count(w, n_q, q0, n_k)
+    for atom in (2, 3, 8):
+        Tr, Cr = oracle_lib.count_terms(w, n_q, q0, n_k, atom=atom)
+        assert Cr == exact[1] and Tr >= exact[0]
+        # brute force of the rounding rule, cell by cell
+        T = 0
+        for i in range(n_q):
+            p = q0 + i
+            for j in range(min(p, n_k - 1) + 1):
+                n = int(np.sum(p - j <= w))
+                T += min(h, atom * -(-n // atom))
+        assert Tr == T
+
+
+def test_rounded_slice_scores(oracle_lib):
+    """Scores under the rounded slice: with one atom spanning every pair, a cell keeps
+    all pairs as soon as the window keeps one (full dot product) and none otherwise (0);
+    with 8-pair atoms the kept set is the lowest-frequency 8*ceil(n/8) pairs, a superset
+    of the window's, and equals it where the widths are constant over each atom."""
+    rng = np.random.default_rng(31)
+    d, n = 32, 120
+    h = d // 2
+    q = bf16_grid(rng, (1, n, 1, d))
+    k = bf16_grid(rng, (1, n, 1, d))
+    w = oracle_lib.window_widths(d, 30.0, 1.0)  # widths 6 .. ~100: every count occurs
+    full = q[0, :, 0] @ k[0, :, 0].T / math.sqrt(d)
+    z = np.arange(n)[:, None] - np.arange(n)[None, :]
+    s_all = oracle_lib.scores(q, k, 0, w, atom=h)
+    any_kept = z <= w.max()
+    want = np.where(z < 0, -np.inf, np.where(any_kept, full, 0.0))
+    np.testing.assert_allclose(s_all, want, atol=1e-12)
+    # 8-pair atoms, against the sum over the kept suffix written per cell
+    s8 = oracle_lib.scores(q, k, 0, w, atom=8)
+    for i in range(0, n, 7):
+        for j in range(0, i + 1, 5):
+            cnt = int(np.sum(i - j <= w))
+            r0 = h - min(h, 8 * -(-cnt // 8))
+            x = sum(q[0, i, 0, r] * k[0, j, 0, r] + q[0, i, 0, r + h] * k[0, j, 0, r + h]
+                    for r in range(r0, h))
+            assert s8[i, j] == pytest.approx(x / math.sqrt(d), abs=1e-12)
+    # widths constant over each 8-pair atom: rounding changes nothing
+    wc = np.repeat(np.array([5.0, 40.0]), 8)
+    np.testing.assert_array_equal(oracle_lib.scores(q, k, 0, wc, atom=8),
+                                  oracle_lib.scores(q, k, 0, wc))
+    # the rounded slice needs a window whose kept pairs are a low-frequency suffix
+    with pytest.raises(ValueError):
+        oracle_lib.scores(q, k, 0, w[::-1].copy(), atom=8)
