@@ -51,7 +51,7 @@ def parse():
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the per-configuration table (the other workloads)")
     ap.add_argument("--no-family", action="store_true",
-                    help="skip the window-family timings (variable-k profile, uniform k=64)")
+                    help="skip the other windows (variable-k profile, uniform k=64, rounded slice)")
     ap.add_argument("--cpu-rows", type=int, default=512,
                     help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -124,15 +124,18 @@ def copy_calibration():
 PREFILL_CONFIGS = ["qwen05b_prefill_1k", "qwen05b_prefill_8k", "qwen05b_prefill_32k",
                    "llama3b_prefill_32k", "llama3b_prefill_128k"]
 DECODE_CONFIGS = ["llama3b_decode_32k", "llama3b_decode_128k"]
-# configurations also timed under the variable-k profile 16 -> 2 and uniform k = 64
+# configurations also timed under the variable-k profile 16 -> 2, uniform k = 64 and
+# the rounded slice
 FAMILY_CONFIGS = ("qwen05b_prefill_32k", "llama3b_prefill_128k", "llama3b_decode_128k")
 
 
-def family_windows(atf, d, base, theta):
-    """The window-family members timed beside the default window (App. A)."""
+def family_windows(atf, d, base, theta, k=2.0):
+    """Windows timed beside the default one: two members of the window family of
+    App. A, and the default window with the rounded slice of Sec. 3.3 (8-pair steps)."""
     return {"var16to2": atf.Window(d, base, 16.0, theta,
                                    k_profile=atf.atf_retention_profile(d, "arithmetic", 16.0, 2.0)),
-            "k64": atf.Window(d, base, 64.0, theta)}
+            "k64": atf.Window(d, base, 64.0, theta),
+            "rounded8": atf.Window(d, base, k, theta, slice_pairs=8)}
 
 
 def _median_ms(fn, stream, warm, iters):
@@ -177,7 +180,7 @@ def config_table(atf, W, dev, stream):
         t_off = _median_ms(lambda: run(off), stream, 2, iters)
         wins = {tag: atf.Window(d, wl.rope_base, wl.k, table) for tag, table in tables.items()}
         if name in FAMILY_CONFIGS:
-            wins.update(family_windows(atf, d, wl.rope_base, tables[""]))
+            wins.update(family_windows(atf, d, wl.rope_base, tables[""], wl.k))
         for tag, win in wins.items():
             T, C = atf.atf_count_terms(win, wl.n_q, wl.q_pos0, wl.n_k)
             flops = wl.batch * wl.h_q * (4 * T + 2 * d * C)
@@ -226,7 +229,7 @@ def config_table(atf, W, dev, stream):
         R_off, Cd = atf.atf_count_terms(off, 1, wl.q_pos0, wl.n_k)
         wins = {tag: atf.Window(d, wl.rope_base, wl.k, table) for tag, table in tables.items()}
         if name in FAMILY_CONFIGS:
-            wins.update(family_windows(atf, d, wl.rope_base, tables[""]))
+            wins.update(family_windows(atf, d, wl.rope_base, tables[""], wl.k))
         for tag, win in wins.items():
             R, Cd = atf.atf_count_terms(win, 1, wl.q_pos0, wl.n_k)
             nbytes = wl.batch * wl.h_kv * (4 * R + 2 * d * Cd) + wl.batch * wl.h_q * d * 4
@@ -437,12 +440,12 @@ def main():
         decode_info["full_window_GBps"] = round(
             bytes_decode_full / (full["decode_ms"] * 1e-3) / 1e9, 1)
 
-    # ---- members of the window family of App. A on the same inputs: the variable-k
-    # profile 16 -> 2 and uniform k = 64 (tab:absbench)
+    # ---- other windows on the same inputs: the variable-k profile 16 -> 2 and uniform
+    # k = 64 (App. A, tab:absbench), and the rounded slice (Sec. 3.3, tab:c2e2e)
     family = None
     if not args.no_family:
         family = {}
-        for tag, fw in family_windows(atf, d, pf.rope_base, None).items():
+        for tag, fw in family_windows(atf, d, pf.rope_base, None, pf.k).items():
             Tf, Cf = atf.atf_count_terms(fw, pf.n_q, pf.q_pos0, pf.n_k)
             fl = B * pf.h_q * (4 * Tf + 2 * d * Cf)
             tp = _median_ms(lambda: prefill(fw), stream, 1, args.steps)
@@ -487,7 +490,7 @@ def main():
                    "batch": B, "n_q": pf.n_q, "q_pos0": pf.q_pos0, "n_k": pf.n_k,
                    "h_q": pf.h_q, "h_kv": pf.h_kv, "head_dim": d, "rope_base": pf.rope_base,
                    "k": pf.k, "parallelism": "single GPU"},
-        "prefill": prefill_info, "decode": decode_info, "window_family": family,
+        "prefill": prefill_info, "decode": decode_info, "window_variants": family,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "configs": configs,

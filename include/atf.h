@@ -57,8 +57,9 @@ enum {
  * With family != 0 the window is the member of the family of App. A (eq:family)
  *     w_r = min(max(k_r * lambda_r^gamma + a * (r + 1) / (d/2), beta), cap)
  * with k_r = k_profile[r] (or k for every pair when k_profile is NULL).  The
- * default window is k_r = k, gamma = 1, a = 0, beta = 0, cap = +INFINITY, and a
- * zero-initialised tail (family == 0) selects it whatever the other fields hold.
+ * default window is k_r = k, gamma = 1, a = 0, beta = 0, cap = +INFINITY, and
+ * family == 0 selects it whatever k_profile, gamma, a, beta and cap hold.  A
+ * zero-initialised tail (family == 0, slice_pairs == 0) is the exact default window.
  * Examples: the variable-k profile (atf_retention_profile, 16 -> 2); uniform
  * k = 64; a ceiling cN (cap = c * N); the sliding window of width S (k_r = 0,
  * beta = cap = S); the linear window (k_r = 0, a = W). */
@@ -78,16 +79,25 @@ typedef struct atf_window {
     double a;                /* additive width in tokens (times (r+1)/(d/2)), finite, >= 0 */
     double beta;             /* floor in tokens, finite, >= 0 */
     double cap;              /* ceiling in tokens, >= 0; +INFINITY for none */
+    int32_t slice_pairs;     /* 0 or 1: the exact window.  s > 1: the rounded slice of Sec. 3.3:
+                                at each distance the kept pairs, a low-frequency slice, are
+                                rounded up to a whole number of s-pair steps counted from the
+                                lowest frequency (s = 8: 16-element MMA K-steps); needs a table
+                                non-decreasing in r.  Read with family == 0 too. */
 } atf_window;
 
 /* Window table (Sec. 3.2 eq:window with eq:lambda, or App. A eq:family):
  * W_out[r] = floor(w_r) computed in fp64 and clamped to [0, 2^31 - 1] (the clamp is
  * exact because positions stay below 2^31 - 1, and w_r >= 0 always).  Pair r is kept
- * at distance z iff z <= W_out[r].  W_out: host int32 array of d/2 entries.
+ * at distance z iff z <= W_out[r].  With slice_pairs = s > 1 the rounded slice keeps
+ * pair r exactly where the window keeps the top pair of its s-pair step (steps counted
+ * down from r = d/2 - 1), so W_out[r] is that pair's threshold.
+ * W_out: host int32 array of d/2 entries.
  * Errors: ATF_EINVAL for a NULL pointer, odd or non-positive d, k <= 0 or NaN
  * (k < 0 with family), B <= 1 (without inv_freq), a negative/NaN inv_freq or
- * k_profile entry, a non-finite gamma, a or beta, a negative a, beta or cap, or a
- * width that evaluates to NaN (0 * inf). */
+ * k_profile entry, a non-finite gamma, a or beta, a negative a, beta or cap, a
+ * width that evaluates to NaN (0 * inf), slice_pairs < 0 or > d/2, or slice_pairs > 1
+ * with a table that decreases somewhere in r. */
 int atf_window_table(const atf_window *w, int32_t *W_out);
 
 /* Retention profile k_r of App. A, r = 0 (highest frequency) .. d/2 - 1, into the

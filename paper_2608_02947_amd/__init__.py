@@ -46,7 +46,8 @@ class _CWindow(ctypes.Structure):
                 ("k", ctypes.c_double), ("inv_freq", ctypes.c_void_p),
                 ("family", ctypes.c_int32), ("k_profile", ctypes.c_void_p),
                 ("gamma", ctypes.c_double), ("a", ctypes.c_double),
-                ("beta", ctypes.c_double), ("cap", ctypes.c_double)]
+                ("beta", ctypes.c_double), ("cap", ctypes.c_double),
+                ("slice_pairs", ctypes.c_int32)]
 
 
 def _load():
@@ -112,6 +113,8 @@ class Window:
     Any of ``k_profile``, ``gamma``, ``a``, ``beta``, ``cap`` away from the default
     window selects the window family of App. A (eq:family):
     w_r = min(max(k_r lambda_r^gamma + a (r+1)/(d/2), beta), cap).
+    ``slice_pairs`` = 8 selects the rounded slice of Sec. 3.3 (the kept low-frequency
+    slice rounded up to 16-element MMA K-steps at each distance); 0 is the exact window.
     """
     head_dim: int
     rope_base: float
@@ -122,6 +125,7 @@ class Window:
     a: float = 0.0
     beta: float = 0.0
     cap: float = math.inf
+    slice_pairs: int = 0
 
     @property
     def family(self) -> bool:
@@ -140,7 +144,8 @@ class Window:
         cw = _CWindow(int(self.head_dim), float(self.rope_base), float(self.k),
                       th.ctypes.data if th is not None else None, int(self.family),
                       kp.ctypes.data if kp is not None else None, float(self.gamma),
-                      float(self.a), float(self.beta), float(self.cap))
+                      float(self.a), float(self.beta), float(self.cap),
+                      int(self.slice_pairs))
         return cw, (th, kp)  # keep the arrays alive for the duration of the call
 
 

@@ -88,6 +88,20 @@ int window_thresholds(const atf_window* w, int32_t* out, int max_pairs) {
         if (t < 0.0) t = 0.0;
         out[r] = static_cast<int32_t>(t);
     }
+    // Rounded slice (Sec. 3.3): at distance z the window keeps the suffix r >= rf(z)
+    // of a non-decreasing table; rounding its length up to whole s-pair steps counted
+    // from r = h - 1 keeps pair r iff the top pair of r's step is kept.
+    const int h = d / 2, sp = w->slice_pairs;
+    if (sp < 0 || sp > h)
+        return fail(ATF_EINVAL, "window: slice_pairs %d must be in [0, d/2 = %d]", sp, h);
+    if (sp > 1) {
+        for (int r = 1; r < h; ++r)
+            if (out[r] < out[r - 1])
+                return fail(ATF_EINVAL,
+                            "window: the rounded slice needs a table non-decreasing in r "
+                            "(W[%d] = %d < W[%d] = %d)", r, out[r], r - 1, out[r - 1]);
+        for (int r = 0; r < h; ++r) out[r] = out[h - 1 - sp * ((h - 1 - r) / sp)];
+    }
     return ATF_OK;
 }
 

@@ -177,12 +177,15 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                 sacc = mfma(kf[c], qb, sacc);
             }
         }
-        // pairs whose window ends inside the block (register v: token t0 + off(v) + 4 hh)
+        // pairs whose window ends inside the block (register v: token t0 + off(v) + 4 hh),
+        // grouped by chunk and threshold: one MFMA per group
         uint64_t part = keep & ~full;
         while (part) {
             const int r = __builtin_ctzll(part);
-            part &= part - 1;
             const int c = r >> 3;
+            const int wr = p.win.W[r];
+            const uint64_t grp = __ballot(my_w == wr) & part & (0xFFull << (8 * c));
+            part &= ~grp;
             u32x4_t kfc = kf[0], qfc = qf[0];
 #pragma unroll
             for (int cc = 1; cc < kChunks; ++cc)
@@ -190,8 +193,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                     kfc = kf[cc];
                     qfc = qf[cc];
                 }
-            const f32x16_t t = mfma(kfc, keep_pairs(qfc, 1u << (r & 7)), zero16());
-            const int thr = p.q_pos - t0 - 4 * hh - p.win.W[r];  // keep iff off(v) >= thr
+            const f32x16_t t = mfma(kfc, keep_pairs(qfc, uint32_t(grp >> (8 * c))), zero16());
+            const int thr = p.q_pos - t0 - 4 * hh - wr;  // keep iff off(v) >= thr
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int off = 8 * (v / 4) + (v % 4);

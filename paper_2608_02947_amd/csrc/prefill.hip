@@ -368,20 +368,24 @@ prefill_kernel(const PrefillParams p) {
                     acc = mfma(kf[c], q, acc);
                 }
             }
-            // pairs whose window ends inside the block: one MFMA each, added where
-            // z <= W_r (register v holds distance zbase - off(v): keep iff off(v) >= thr)
+            // pairs whose window ends inside the block, grouped by chunk and threshold:
+            // one MFMA per group, added where z <= W_r (register v holds distance
+            // zbase - off(v): keep iff off(v) >= thr).  A table whose chunks share one
+            // threshold (the rounded slice) needs one MFMA per partial chunk.
             uint64_t part = keep & ~full;
             while (part) {
                 const int r = __builtin_ctzll(part);
-                part &= part - 1;
                 const int c = r >> 3;
+                const int wr = p.win.W[r];
+                const uint64_t grp = __ballot(my_w == wr) & part & (0xFFull << (8 * c));
+                part &= ~grp;
                 u32x4_t qc = qf[0];
 #pragma unroll
                 for (int cc = 1; cc < C::kChunks; ++cc)
                     if (cc == c) qc = qf[cc];
-                const f32x16_t pr =
-                    mfma(lds_read_b128(kr + 2048u * c), keep_pairs(qc, 1u << (r & 7)), zero16());
-                const int thr = my_pos - jb - 4 * hh - p.win.W[r];
+                const f32x16_t pr = mfma(lds_read_b128(kr + 2048u * c),
+                                         keep_pairs(qc, uint32_t(grp >> (8 * c))), zero16());
+                const int thr = my_pos - jb - 4 * hh - wr;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int off = 8 * (v / 4) + (v % 4);

@@ -26,11 +26,13 @@ def note(msg: str):
     sys.stdout.flush()
 
 
-def windows_for(head_dim, rope_base, k, theta, n_ctx):
-    """(GPU window, oracle widths) built independently on each side."""
+def windows_for(head_dim, rope_base, k, theta, n_ctx, slice_pairs=0):
+    """(GPU window, oracle widths) built independently on each side.  slice_pairs > 1
+    selects the rounded slice on the GPU side; the oracle applies its own rounding
+    rule when called with atom=slice_pairs."""
     import paper_2608_02947_amd as atf
     th = None if theta is None else np.asarray(theta, dtype=np.float64)
-    return (atf.Window(head_dim, rope_base, k, th),
+    return (atf.Window(head_dim, rope_base, k, th, slice_pairs=slice_pairs),
             oracle.window_widths(head_dim, rope_base, k, th, n_ctx=n_ctx))
 
 
@@ -151,11 +153,11 @@ def sample_rows(batch, n_q, h_q, n_rows, seed, tile=128):
     return np.array(rows, dtype=np.int64)
 
 
-def workload_window(wl: W.Workload, k=None, family=None):
+def workload_window(wl: W.Workload, k=None, family=None, slice_pairs=0):
     th = W.workload_theta(wl)
     if family is not None:
         return family_windows_for(wl.head_dim, wl.rope_base, None if th is None else th.numpy(),
                                   family)
     return windows_for(wl.head_dim, wl.rope_base, wl.k if k is None else k,
                        None if th is None else th.numpy(),
-                       n_ctx=max(wl.n_k, wl.q_pos0 + wl.n_q))
+                       n_ctx=max(wl.n_k, wl.q_pos0 + wl.n_q), slice_pairs=slice_pairs)

@@ -204,6 +204,49 @@ def test_family_defaults_and_validation():
     assert lib.atf_retention_profile(8, 1, 16.0, 2.0, None) == atf.ATF_EINVAL
 
 
+# the rounded slice of Sec. 3.3: the library's table/counts against the oracle's
+# cell-by-cell rounding rule summed by distance
+@pytest.mark.parametrize("name", ["qwen05b_prefill_32k", "llama3b_prefill_128k",
+                                  "qwen7b1m_prefill_chunk", "qwen7b1m_decode"])
+@pytest.mark.parametrize("sp", [2, 3, 8, 16])
+def test_rounded_slice_counts_match_oracle(oracle_lib, name, sp):
+    wl = W.WORKLOADS[name]
+    th = W.workload_theta(wl)
+    th_np = th.numpy() if th is not None else None
+    win = atf.Window(wl.head_dim, wl.rope_base, wl.k, th_np, slice_pairs=sp)
+    widths = oracle_lib.window_widths(wl.head_dim, wl.rope_base, wl.k, th_np)
+    n_q = min(wl.n_q, 4096)   # the by-distance sum walks every distance up to the last row
+    q0 = wl.q_pos0 + wl.n_q - n_q
+    got = atf.atf_count_terms(win, n_q, q0, wl.n_k)
+    assert got == oracle_lib.count_terms(widths, n_q, q0, wl.n_k, atom=sp)
+    # rounding only adds terms
+    assert got[0] >= atf.atf_count_terms(atf.Window(wl.head_dim, wl.rope_base, wl.k, th_np),
+                                         n_q, q0, wl.n_k)[0]
+
+
+def test_rounded_slice_table_and_validation(oracle_lib):
+    t = atf.atf_window_table(atf.Window(128, 1e7, 2.0, slice_pairs=8))
+    exact = atf.atf_window_table(atf.Window(128, 1e7, 2.0))
+    # each 8-pair step takes the threshold of its lowest-frequency pair
+    assert np.array_equal(t, np.repeat(exact[7::8], 8))
+    assert np.array_equal(atf.atf_window_table(atf.Window(128, 1e7, 2.0, slice_pairs=1)), exact)
+    # steps counted from the lowest frequency: with 3-pair steps on 4 pairs, {0} {1,2,3}
+    t3 = atf.atf_window_table(atf.Window(8, 100.0, 2.0, slice_pairs=3))
+    e3 = atf.atf_window_table(atf.Window(8, 100.0, 2.0))
+    assert list(t3) == [e3[0], e3[3], e3[3], e3[3]]
+    # the variable-k profile keeps a non-decreasing table: allowed
+    var = atf.Window(64, 1e6, 16.0, k_profile=atf.atf_retention_profile(64, "arithmetic", 16, 2),
+                     slice_pairs=8)
+    atf.atf_window_table(var)
+    bad = [atf.Window(8, 1e4, 2.0, slice_pairs=-1), atf.Window(8, 1e4, 2.0, slice_pairs=5),
+           atf.Window(8, 1e4, 2.0, [1.0, 0.5, 2.0, 0.1], slice_pairs=2),   # decreasing widths
+           atf.Window(64, 1e4, 1e6, gamma=-1.0, slice_pairs=8)]
+    for w in bad:
+        with pytest.raises(atf.AtfError) as e:
+            atf.atf_window_table(w)
+        assert e.value.code == atf.ATF_EINVAL and "window" in atf.atf_last_error()
+
+
 def _raw_prefill(lib, cw, **kw):
     args = dict(q=16, k=16, v=16, o=16, lse=16, batch=1, n_q=4, n_k=4, q_pos0=0, h_q=2, h_kv=1,
                 cache_tokens=0)

@@ -78,12 +78,12 @@ def _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed, theta=None):
     return q, k, v
 
 
-def _decode_parity(q4, k, v, q_pos, win, widths, label):
+def _decode_parity(q4, k, v, q_pos, win, widths, label, atom=0):
     """q4 [B, 1, h_q, d] (oracle layout); every (b, head) row compared."""
     note(f"decode {label} q={tuple(q4.shape)} k={tuple(k.shape)} q_pos={q_pos}")
     qd = q4[:, 0].contiguous().to(DEV)
     o, lse = gpu_decode(qd, k.to(DEV), v.to(DEV), q_pos, win)
-    o_ref, lse_ref, _ = oracle.attend(q4.cpu(), k.cpu(), v.cpu(), q_pos, widths)
+    o_ref, lse_ref, _ = oracle.attend(q4.cpu(), k.cpu(), v.cpu(), q_pos, widths, atom=atom)
     return compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], label)
 
 
@@ -151,6 +151,28 @@ def test_decode_family_workload_all_rows(name, family):
     inp = W.make_inputs(wl, device=DEV)
     win, widths = workload_window(wl, family=family)
     _decode_parity(inp["q"], inp["k"], inp["v"], wl.q_pos0, win, widths, f"{name} {family}")
+
+
+@pytest.mark.parametrize("case", [(2, 777, 777, 12, 1, 128, 1e4, 2.0),
+                                  (1, 1500, 1500, 40, 1, 64, 1e4, 2.0),
+                                  (1, 4096, 4096, 16, 2, 128, 100.0, 2.0)],
+                         ids=lambda c: "x".join(str(x) for x in c))
+def test_decode_rounded_slice(case):
+    """The rounded slice of Sec. 3.3 (8-pair K-steps) against the oracle's rounding rule."""
+    B, n_k, q_pos, h_q, h_kv, d, base, kwin = case
+    q, k, v = _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed=hash(case) % 10000 + 1)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=q_pos + 1, slice_pairs=8)
+    _decode_parity(q, k, v, q_pos, win, widths, f"rounded{case}", atom=8)
+
+
+@pytest.mark.parametrize("name", ["qwen7b1m_decode", "llama3b_decode_128k"])
+def test_decode_rounded_slice_workloads(name):
+    wl = W.WORKLOADS[name]
+    note(f"generate {name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl, slice_pairs=8)
+    _decode_parity(inp["q"], inp["k"], inp["v"], wl.q_pos0, win, widths, f"{name} rounded",
+                   atom=8)
 
 
 @pytest.mark.parametrize("name", ["llama3b_decode_32k", "llama3b_decode_128k", "qwen7b1m_decode"])

@@ -34,11 +34,11 @@ def _small_inputs(B, n_q, n_k, q0, h_q, h_kv, d, base, seed, theta=None, scale_k
     return q, k, v
 
 
-def _full_parity(q, k, v, q0, win, widths, label, scale=None):
+def _full_parity(q, k, v, q0, win, widths, label, scale=None, atom=0):
     note(f"prefill {label} shape q={tuple(q.shape)} k={tuple(k.shape)} q0={q0}")
     o, lse = gpu_prefill(q.to(DEV), k.to(DEV), v.to(DEV), q0, win,
                          0.0 if scale is None else scale)
-    o_ref, lse_ref, _ = oracle.attend(q, k, v, q0, widths, scale=scale)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, q0, widths, scale=scale, atom=atom)
     return compare(to_f64(o), to_f64(lse), o_ref, lse_ref, label)
 
 
@@ -153,6 +153,49 @@ def test_prefill_family_workload_sampled_rows(name, family):
     og = torch.stack([o[b, i, h] for b, h, i in rows]).float().cpu().numpy()
     lg = torch.stack([lse[b, h, i] for b, h, i in rows]).cpu().numpy()
     compare(og, lg, o_ref, lse_ref, f"{name} {family}")
+
+
+ROUNDED_CASES = [
+    # B, n_q, n_k, q0, h_q, h_kv, d, base, k
+    (1, 300, 300, 0, 6, 2, 128, 5e5, 2.0),
+    (2, 260, 260, 0, 4, 4, 64, 1e6, 2.0),
+    (1, 333, 500, 167, 16, 2, 64, 1e4, 1.0),      # G = 8, ragged tail
+    (1, 257, 257, 0, 3, 3, 128, 100.0, 2.0),      # saturated: empty sums
+]
+
+
+@pytest.mark.parametrize("case", ROUNDED_CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_rounded_slice_all_rows(case):
+    """The rounded slice of Sec. 3.3 (8-pair K-steps) against the oracle's rounding rule."""
+    B, n_q, n_k, q0, h_q, h_kv, d, base, kwin = case
+    q, k, v = _small_inputs(B, n_q, n_k, q0, h_q, h_kv, d, base, seed=hash(case) % 10000 + 1)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=max(n_k, q0 + n_q), slice_pairs=8)
+    _full_parity(q, k, v, q0, win, widths, f"rounded{case}", atom=8)
+
+
+def test_prefill_rounded_slice_workloads():
+    """Rounded slice: all rows of the 1K Qwen2.5-0.5B shape and of 700 Llama-3.2-3B rows
+    (effective table), then sampled rows of the 1M chunk."""
+    wl = W.WORKLOADS["qwen05b_prefill_1k"]
+    inp = W.make_inputs(wl)
+    win, widths = workload_window(wl, slice_pairs=8)
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, wl.name + " rounded", atom=8)
+    wl = W.WORKLOADS["llama3b_prefill_32k"]
+    inp = W.make_inputs(wl, n_k=700, n_q=700, q_pos0=0)
+    win, widths = workload_window(wl, slice_pairs=8)
+    _full_parity(inp["q"], inp["k"], inp["v"], 0, win, widths, "llama3 700 rounded", atom=8)
+    wl = W.WORKLOADS["qwen7b1m_prefill_chunk"]
+    note(f"generate {wl.name}")
+    inp = W.make_inputs(wl, device=DEV)
+    win, widths = workload_window(wl, slice_pairs=8)
+    note(f"prefill {wl.name} rounded")
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], wl.q_pos0, win)
+    rows = sample_rows(wl.batch, wl.n_q, wl.h_q, 32, seed=wl.seed + 2)
+    o_ref, lse_ref, _ = oracle.attend(inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu(), wl.q_pos0,
+                                      widths, rows=rows, atom=8)
+    og = torch.stack([o[b, i, h] for b, h, i in rows]).float().cpu().numpy()
+    lg = torch.stack([lse[b, h, i] for b, h, i in rows]).cpu().numpy()
+    compare(og, lg, o_ref, lse_ref, wl.name + " rounded")
 
 
 @pytest.mark.parametrize("name", ["qwen05b_prefill_8k", "qwen05b_prefill_32k",
