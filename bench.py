@@ -82,8 +82,10 @@ def profile_driver(name, iters, kinf):
         kp = torch.empty(atf.kcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
                          device=dev)
         atf.atf_pack_kcache(inp["k"], kp)
-        run = lambda: atf.atf_prefill(inp["q"], kp, inp["v"], o, lse, wl.q_pos0, win,
-                                      stream=stream)
+        vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_vcache(inp["v"], vp)
+        run = lambda: atf.atf_prefill(inp["q"], kp, vp, o, lse, wl.q_pos0, win, stream=stream)
     else:
         kp = torch.empty((wl.batch, wl.h_kv, d // 16, wl.n_k, 16), dtype=torch.bfloat16,
                          device=dev)
@@ -167,6 +169,10 @@ def config_table(atf, W, dev, stream):
         kp = torch.empty(atf.kcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
                          device=dev)
         atf.atf_pack_kcache(inp["k"], kp)
+        vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
+                         device=dev)
+        atf.atf_pack_vcache(inp["v"], vp)
+        del inp["k"], inp["v"]
         o = torch.empty_like(inp["q"])
         lse = torch.empty((wl.batch, wl.h_q, wl.n_q), dtype=torch.float32, device=dev)
         th = W.workload_theta(wl)
@@ -175,8 +181,7 @@ def config_table(atf, W, dev, stream):
             tables["raw_base"] = None
         iters = 5 if wl.n_q * wl.h_q >= 1 << 21 else 20
         off = atf.Window(d, wl.rope_base, math.inf)
-        run = lambda w: atf.atf_prefill(inp["q"], kp, inp["v"], o, lse, wl.q_pos0, w,
-                                        stream=stream)
+        run = lambda w: atf.atf_prefill(inp["q"], kp, vp, o, lse, wl.q_pos0, w, stream=stream)
         t_off = _median_ms(lambda: run(off), stream, 2, iters)
         wins = {tag: atf.Window(d, wl.rope_base, wl.k, table) for tag, table in tables.items()}
         if name in FAMILY_CONFIGS:
@@ -191,7 +196,7 @@ def config_table(atf, W, dev, stream):
                 "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
                 "full_window_ms": round(t_off, 4), "speedup_vs_full_window": round(t_off / t, 4),
                 "qk_pruned": round(1 - T / (C * d / 2), 4)}
-        del inp, kp, o, lse
+        del inp, kp, vp, o, lse
         torch.cuda.empty_cache()
     for name in DECODE_CONFIGS:
         wl = W.WORKLOADS[name]
@@ -340,7 +345,7 @@ def main():
     stream = torch.cuda.current_stream()
 
     def prefill(w):
-        atf.atf_prefill(q, kp, v, o, lse, pf.q_pos0, w, stream=stream)
+        atf.atf_prefill(q, kp, vp, o, lse, pf.q_pos0, w, stream=stream)
 
     def decode(w):
         atf.atf_decode(qd, kp, vp, od, lsed, dc.q_pos0, w, ws, stream=stream)

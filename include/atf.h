@@ -127,13 +127,16 @@ int atf_count_terms(const atf_window *w, int64_t n_q, int64_t q_pos0, int64_t n_
  * against n_k keys, tiled with an online softmax; the window is applied as a
  * per-tile slice of the QK contraction axis (Sec. 3.3): fully kept pair-chunks
  * are MFMA K-steps, fully pruned ones are neither loaded nor multiplied, and
- * pairs whose window ends inside the tile are masked per element.  The keys are
- * read from the pair-chunk-major K cache (the layout decode reads, produced by
- * atf_pack_kcache), so a pruned chunk of a key is never read from HBM.
+ * pairs whose window ends inside the tile are masked per element.  Keys and
+ * values are read from the caches decode reads (atf_pack_kcache, atf_pack_vcache,
+ * atf_cache_append), so one pair of caches serves a chunked prefill and the decode
+ * steps after it, and a pruned chunk of a key is never read from HBM.
  *   q        bf16 [batch][n_q][h_q][d]        rotated queries            (device, read)
  *   k_cache  bf16 [batch][h_kv][d/16][cache_tokens][16]  rotated keys, pair-chunk-major,
  *            see atf_pack_kcache; keys 0 .. n_k - 1 are read          (device, read)
- *   v        bf16 [batch][cache_tokens][h_kv][d]  values; rows 0 .. n_k - 1 read (device, read)
+ *   v_cache  bf16 [batch][h_kv][ceil(cache_tokens/16)][d][16]  values in 16-token blocks,
+ *            see atf_pack_vcache; tokens 0 .. n_k - 1 are used (later slots may hold
+ *            anything)                                                (device, read)
  *   o        bf16 [batch][n_q][h_q][d]        output, O/l rounded to nearest even (device, written)
  *   lse      fp32 [batch][h_q][n_q]           natural-log sum of exp of the scaled scores (device, written)
  * cache_tokens is the number of tokens each batch entry of the caches is
@@ -146,7 +149,7 @@ int atf_count_terms(const atf_window *w, int64_t n_q, int64_t q_pos0, int64_t n_
  * non-zero) or > 2^31 - 1, h_q % h_kv != 0, bad window, non-finite scale);
  * ATF_EUNSUPPORTED (d not 64 or 128, or h_q / h_kv above 128 at d = 64 or above 256 at
  * d = 128: the query heads of one KV head share a workgroup's rows); ATF_EHIP. */
-int atf_prefill(const void *q, const void *k_cache, const void *v, void *o, float *lse,
+int atf_prefill(const void *q, const void *k_cache, const void *v_cache, void *o, float *lse,
                 int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
                 int32_t h_q, int32_t h_kv, int64_t cache_tokens, const atf_window *w,
                 float softmax_scale, void *hip_stream);
@@ -180,6 +183,25 @@ size_t atf_vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_d
  * Errors: ATF_EINVAL, ATF_EUNSUPPORTED (d), ATF_EHIP. */
 int atf_pack_vcache(const void *v_bshd, void *v_pack, int32_t batch, int64_t n_k,
                     int32_t h_kv, int32_t head_dim, void *hip_stream);
+
+/* Append tokens to both caches: the keys and values of cache positions
+ * pos0 .. pos0 + n_new - 1, given as the projections produce them, are written
+ * into the pair-chunk-major K cache and the 16-token-block V cache of capacity
+ * cache_tokens (layouts of atf_pack_kcache and atf_pack_vcache).  No other token's
+ * data changes.  This is how a chunked prefill, an appended turn of a long session
+ * (the interval prefill of App. C) or a decode step extends the caches that
+ * atf_prefill and atf_decode read.  Pure data movement (bit-exact).
+ *   k_new, v_new  bf16 [batch][n_new][h_kv][d]                   (device, read)
+ *   k_cache       bf16 [batch][h_kv][d/16][cache_tokens][16]     (device, written at the new tokens)
+ *   v_cache       bf16 [batch][h_kv][ceil(cache_tokens/16)][d][16] (device, written at the new tokens' slots)
+ * All 16-byte aligned; the caches overlap neither each other nor the inputs.
+ * n_new == 0 is a no-op.
+ * Errors: ATF_EINVAL (NULL/misaligned/overlapping pointer, batch < 1, h_kv < 1,
+ * n_new < 0, pos0 < 0, cache_tokens < 1 or > 2^31 - 1, pos0 + n_new > cache_tokens),
+ * ATF_EUNSUPPORTED (d not 64 or 128), ATF_EHIP. */
+int atf_cache_append(const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+                     int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
+                     int64_t cache_tokens, void *hip_stream);
 
 /* Bytes of device workspace that atf_decode needs for these sizes (split-KV
  * partial softmax states).  Returns 0 for invalid sizes. */

@@ -12,7 +12,8 @@ The functions carry the C names of ``include/atf.h``:
   -- host only.
 - :func:`atf_prefill` -- windowed prefill (chunked via ``q_pos0``).
 - :func:`atf_pack_kcache`, :func:`atf_kcache_chunk_pairs` -- decode K-cache layout.
-- :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- decode V-cache layout.
+- :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- V-cache layout.
+- :func:`atf_cache_append` -- write new tokens into both caches at a position.
 - :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
 """
 from __future__ import annotations
@@ -67,6 +68,7 @@ def _load():
         "atf_pack_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
         "atf_vcache_bytes": (ctypes.c_size_t, [i32, i64, i32, i32]),
         "atf_pack_vcache": (ctypes.c_int, [P, P, i32, i64, i32, i32, P]),
+        "atf_cache_append": (ctypes.c_int, [P, P, P, P, i32, i64, i64, i32, i32, i64, P]),
         "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
         "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, f32, P,
                                       ctypes.c_size_t, P]),
@@ -81,7 +83,7 @@ def _load():
 
 _lib = _load()
 EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
-            "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache",
+            "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
             "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
 
 
@@ -216,11 +218,12 @@ def kcache_shape(batch: int, cache_tokens: int, h_kv: int, head_dim: int):
     return (batch, h_kv, head_dim // 16, cache_tokens, 16)
 
 
-def atf_prefill(q, k_cache, v, o, lse, q_pos0: int, window: Window, softmax_scale: float = 0.0,
-                stream=None, n_k: Optional[int] = None):
+def atf_prefill(q, k_cache, v_cache, o, lse, q_pos0: int, window: Window,
+                softmax_scale: float = 0.0, stream=None, n_k: Optional[int] = None):
     """q [B, n_q, h_q, d] bf16; k_cache [B, h_kv, d/16, C, 16] pair-chunk-major (see
-    atf_pack_kcache); v [B, C, h_kv, d]; o like q; lse [B, h_q, n_q] fp32.  C is the
-    caches' token capacity; keys 0 .. n_k - 1 are used (n_k defaults to C)."""
+    atf_pack_kcache); v_cache [B, h_kv, ceil(C/16), d, 16] (see atf_pack_vcache); o like
+    q; lse [B, h_q, n_q] fp32.  C is the caches' token capacity; keys 0 .. n_k - 1 are
+    used (n_k defaults to C)."""
     torch = _torch()
     B, n_q, h_q, d = q.shape
     if k_cache.dim() != 5:
@@ -228,12 +231,12 @@ def atf_prefill(q, k_cache, v, o, lse, q_pos0: int, window: Window, softmax_scal
     _, h_kv, _, cap, _ = k_cache.shape
     n_k = cap if n_k is None else int(n_k)
     if tuple(k_cache.shape) != kcache_shape(B, cap, h_kv, d) or \
-            tuple(v.shape) != (B, cap, h_kv, d) or tuple(o.shape) != tuple(q.shape) or \
-            tuple(lse.shape) != (B, h_q, n_q):
+            tuple(v_cache.shape) != vcache_shape(B, cap, h_kv, d) or \
+            tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q, n_q):
         raise ValueError("atf_prefill: inconsistent shapes")
     cw, keep = window.as_c()
     rc = _lib.atf_prefill(_dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_cache, torch.bfloat16, "k"),
-                          _dev_ptr(v, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+                          _dev_ptr(v_cache, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
                           _dev_ptr(lse, torch.float32, "lse"), B, n_q, n_k, q_pos0, h_q, h_kv,
                           cap, ctypes.byref(cw), float(softmax_scale), _stream_ptr(stream))
     _check(rc)
@@ -257,6 +260,25 @@ def atf_vcache_bytes(batch: int, n_k: int, h_kv: int, head_dim: int) -> int:
 def vcache_shape(batch: int, n_k: int, h_kv: int, head_dim: int):
     """Shape of the packed V cache: [B, h_kv, ceil(n_k/16), d, 16]."""
     return (batch, h_kv, (n_k + 15) // 16, head_dim, 16)
+
+
+def atf_cache_append(k_new, v_new, k_cache, v_cache, pos0: int, stream=None):
+    """k_new, v_new [B, n_new, h_kv, d] -> positions pos0 .. pos0 + n_new - 1 of
+    k_cache [B, h_kv, d/16, C, 16] and v_cache [B, h_kv, ceil(C/16), d, 16] (bf16)."""
+    torch = _torch()
+    B, n_new, h_kv, d = k_new.shape
+    if k_cache.dim() != 5:
+        raise ValueError("atf_cache_append: k_cache must be [B, h_kv, d/16, C, 16]")
+    cap = k_cache.shape[3]
+    if tuple(v_new.shape) != tuple(k_new.shape) or \
+            tuple(k_cache.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_cache.shape) != vcache_shape(B, cap, h_kv, d):
+        raise ValueError("atf_cache_append: inconsistent shapes")
+    _check(_lib.atf_cache_append(_dev_ptr(k_new, torch.bfloat16, "k_new"),
+                                 _dev_ptr(v_new, torch.bfloat16, "v_new"),
+                                 _dev_ptr(k_cache, torch.bfloat16, "k_cache"),
+                                 _dev_ptr(v_cache, torch.bfloat16, "v_cache"),
+                                 B, n_new, int(pos0), h_kv, d, cap, _stream_ptr(stream)))
 
 
 def atf_pack_vcache(v_bshd, v_pack, stream=None):

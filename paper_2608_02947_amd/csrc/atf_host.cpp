@@ -340,7 +340,7 @@ int atf_pack_kcache(const void* k_bshd, void* k_pcm, int32_t batch, int64_t n_k,
     int rc = check_pack("pack_kcache", k_bshd, k_pcm, batch, n_k, h_kv, head_dim, bytes);
     if (rc != ATF_OK) return rc;
     atf::PackParams p{static_cast<const uint16_t*>(k_bshd), static_cast<uint16_t*>(k_pcm), batch,
-                      static_cast<int32_t>(n_k), h_kv};
+                      static_cast<int32_t>(n_k), h_kv, 0, static_cast<int32_t>(n_k), 0};
     hipError_t e = atf::launch_pack_kcache(p, head_dim, static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return fail(ATF_EHIP, "pack_kcache: launch failed: %s", hipGetErrorString(e));
     return ATF_OK;
@@ -359,9 +359,49 @@ int atf_pack_vcache(const void* v_bshd, void* v_pack, int32_t batch, int64_t n_k
                             ? vcache_bytes(batch, n_k, h_kv, head_dim) : 0);
     if (rc != ATF_OK) return rc;
     atf::PackParams p{static_cast<const uint16_t*>(v_bshd), static_cast<uint16_t*>(v_pack), batch,
-                      static_cast<int32_t>(n_k), h_kv};
+                      static_cast<int32_t>(n_k), h_kv, 0, static_cast<int32_t>(n_k), 1};
     hipError_t e = atf::launch_pack_vcache(p, head_dim, static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return fail(ATF_EHIP, "pack_vcache: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
+}
+
+int atf_cache_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                     int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
+                     int64_t cache_tokens, void* hip_stream) {
+    if (head_dim != 64 && head_dim != 128)
+        return fail(ATF_EUNSUPPORTED, "cache_append: head_dim %d not built", head_dim);
+    if (batch < 1 || h_kv < 1 || n_new < 0 || pos0 < 0 || cache_tokens < 1 ||
+        cache_tokens > kPosLimit || pos0 > cache_tokens - n_new)
+        return fail(ATF_EINVAL,
+                    "cache_append: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0, "
+                    "1 <= cache_tokens < 2^31 and pos0 + n_new <= cache_tokens");
+    if (!k_new || !v_new || !k_cache || !v_cache)
+        return fail(ATF_EINVAL, "cache_append: NULL pointer");
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
+        return fail(ATF_EINVAL, "cache_append: pointers must be 16-byte aligned");
+    const size_t row = size_t(h_kv) * size_t(head_dim) * 2;
+    const char* bufs[4] = {static_cast<const char*>(k_new), static_cast<const char*>(v_new),
+                           static_cast<const char*>(k_cache), static_cast<const char*>(v_cache)};
+    const size_t sizes[4] = {size_t(batch) * size_t(n_new) * row, size_t(batch) * size_t(n_new) * row,
+                             size_t(batch) * size_t(cache_tokens) * row,
+                             vcache_bytes(batch, cache_tokens, h_kv, head_dim)};
+    for (int i = 0; i < 4; ++i)
+        for (int j = (i < 2 ? 2 : i + 1); j < 4; ++j)  // written buffers against all others
+            if (bufs[i] < bufs[j] + sizes[j] && bufs[j] < bufs[i] + sizes[i])
+                return fail(ATF_EINVAL, "cache_append: buffers overlap");
+    if (n_new == 0) return ATF_OK;
+    const hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    atf::PackParams pk{static_cast<const uint16_t*>(k_new), static_cast<uint16_t*>(k_cache), batch,
+                       static_cast<int32_t>(n_new), h_kv, static_cast<int32_t>(pos0),
+                       static_cast<int32_t>(cache_tokens), 0};
+    hipError_t e = atf::launch_pack_kcache(pk, head_dim, st);
+    if (e == hipSuccess) {
+        atf::PackParams pv = pk;
+        pv.src = static_cast<const uint16_t*>(v_new);
+        pv.dst = static_cast<uint16_t*>(v_cache);
+        e = atf::launch_pack_vcache(pv, head_dim, st);
+    }
+    if (e != hipSuccess) return fail(ATF_EHIP, "cache_append: launch failed: %s", hipGetErrorString(e));
     return ATF_OK;
 }
 

@@ -24,7 +24,7 @@ struct WindowTable {
 struct PrefillParams {
     const uint16_t* q;   // [B][n_q][h_q][d]
     const uint16_t* k;   // [B][h_kv][d/16][cache_tokens][16] (pair-chunk-major)
-    const uint16_t* v;   // [B][cache_tokens][h_kv][d]
+    const uint16_t* v;   // [B][h_kv][ceil(cache_tokens/16)][d][16] (see atf_pack_vcache)
     uint16_t* o;         // [B][n_q][h_q][d]
     float* lse;          // [B][h_q][n_q]
     int32_t batch, n_q, n_k, q_pos0, h_q, h_kv, group;
@@ -56,9 +56,13 @@ struct DecodeParams {
 };
 
 struct PackParams {
-    const uint16_t* src;  // [B][n_k][h_kv][d]
-    uint16_t* dst;        // K: [B][h_kv][d/16][n_k][16]; V: [B][h_kv][ceil(n_k/16)][d][16]
+    const uint16_t* src;  // [B][n_k][h_kv][d]: tokens pos0 .. pos0 + n_k - 1
+    uint16_t* dst;        // K: [B][h_kv][d/16][cache_tokens][16];
+                          // V: [B][h_kv][ceil(cache_tokens/16)][d][16]
     int32_t batch, n_k, h_kv;
+    int32_t pos0;          // cache position of the first source token
+    int32_t cache_tokens;  // capacity of dst
+    int32_t zero_tail;     // V: write zeros to the slots of the touched blocks past the source
 };
 
 // Kernel launchers (prefill.hip, decode.hip).  Return the HIP error of the launch.

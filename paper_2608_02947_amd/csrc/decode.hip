@@ -360,36 +360,42 @@ __global__ __launch_bounds__(256) void pack_kcache_kernel(const PackParams p) {
         const uint16_t* src = p.src + ((int64_t(b) * p.n_k + t) * p.h_kv + g) * D;
         const u32x4 lo = *reinterpret_cast<const u32x4*>(src + 8 * c);
         const u32x4 hi = *reinterpret_cast<const u32x4*>(src + D / 2 + 8 * c);
-        uint16_t* dst = p.dst + (((int64_t(b) * p.h_kv + g) * kChunks + c) * p.n_k + t) * 16;
+        uint16_t* dst = p.dst + (((int64_t(b) * p.h_kv + g) * kChunks + c) * p.cache_tokens +
+                                 p.pos0 + t) * 16;
         *reinterpret_cast<u32x4*>(dst) = lo;
         *reinterpret_cast<u32x4*>(dst + 8) = hi;
     }
 }
 
-// V blocks: one thread per (batch, kv head, 16-token block, dim); position
-// 8h + e of the row holds token 8*(e/4) + 4h + e%4 of the block.
+// V blocks: one thread per (batch, kv head, touched 16-token block, dim); slot
+// 8h + e of the row holds token 8*(e/4) + 4h + e%4 of the block.  Slots of
+// tokens outside pos0 .. pos0 + n_k - 1 keep their contents (or become 0 past the
+// source when zero_tail is set).
 template <int D>
 __global__ __launch_bounds__(256) void pack_vcache_kernel(const PackParams p) {
-    const int nblk = (p.n_k + 15) / 16;
+    const int blk0 = p.pos0 / 16;
+    const int nblk = (p.pos0 + p.n_k + 15) / 16 - blk0;  // blocks touched
+    const int cache_blk = (p.cache_tokens + 15) / 16;
     const int64_t total = int64_t(p.batch) * p.h_kv * nblk * D;
     for (int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x; idx < total;
          idx += int64_t(gridDim.x) * 256) {
         const int x = int(idx % D);
         int64_t r = idx / D;
-        const int blk = int(r % nblk);
+        const int blk = blk0 + int(r % nblk);
         r /= nblk;
         const int g = int(r % p.h_kv);
         const int b = int(r / p.h_kv);
-        uint16_t row[16];
+        uint16_t* dst = p.dst + ((int64_t(b) * p.h_kv + g) * cache_blk + blk) * int64_t(D) * 16 +
+                        int64_t(x) * 16;
 #pragma unroll
         for (int pos = 0; pos < 16; ++pos) {
             const int h = pos >> 3, e = pos & 7;
-            const int t = 16 * blk + 8 * (e >> 2) + 4 * h + (e & 3);
-            row[pos] = t < p.n_k ? p.src[((int64_t(b) * p.n_k + t) * p.h_kv + g) * D + x] : uint16_t(0);
+            const int t = 16 * blk + 8 * (e >> 2) + 4 * h + (e & 3) - p.pos0;  // source token
+            if (t >= 0 && t < p.n_k)
+                dst[pos] = p.src[((int64_t(b) * p.n_k + t) * p.h_kv + g) * D + x];
+            else if (t >= p.n_k && p.zero_tail)
+                dst[pos] = uint16_t(0);
         }
-        uint16_t* dst = p.dst + ((int64_t(b) * p.h_kv + g) * nblk + blk) * int64_t(D) * 16 + int64_t(x) * 16;
-#pragma unroll
-        for (int pos = 0; pos < 16; ++pos) dst[pos] = row[pos];
     }
 }
 
@@ -434,7 +440,8 @@ hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t str
 }
 
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream) {
-    const int64_t total = int64_t(p.batch) * p.h_kv * ((p.n_k + 15) / 16) * head_dim;
+    const int64_t total = int64_t(p.batch) * p.h_kv *
+                          ((p.pos0 + p.n_k + 15) / 16 - p.pos0 / 16) * head_dim;
     (void)hipGetLastError();
     if (head_dim == 64)
         hipLaunchKernelGGL(pack_vcache_kernel<64>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);

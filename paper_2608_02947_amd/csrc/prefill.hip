@@ -17,9 +17,10 @@
 // memory, and a chunk that no cell of the tile keeps is skipped by one
 // wave-uniform branch -- its bytes are never read from HBM.  In LDS the K tile is
 // [chunk][32-key block][half][key][8 bf16]: a fragment read of 64 lanes covers
-// 1 KB without bank conflicts.  The V tile is row-major [key][d] with rows padded
-// to d + 32 bf16 so that the transposed reads (4 rows x 32 bytes per 16 lanes)
-// hit distinct banks.
+// 1 KB without bank conflicts.  V also comes from the decode cache: 16-token
+// blocks stored [d][16 slots], slot 8h + e holding token 8(e/4) + 4h + e%4 of the
+// block.  A 64-key tile is four consecutive blocks, one contiguous copy into LDS,
+// and the 8 slots a lane needs for the PV operand are 16 contiguous bytes.
 //
 // Matrix layout (v_mfma_f32_32x32x16_bf16, lane l, c = l % 32, h = l / 32)
 //   S^T[key][row] = K[key][dims] * Q^T[dims][row]: A = K fragment (key c, dims
@@ -27,9 +28,9 @@
 //   query row c and keys 8*(v/4) + 4h + v%4 of a 32-key block (v < 16).  One query
 //   row per lane pair makes the row max and sum lane-local plus one exchange.
 //   O^T[d][row] += V^T[d][key] * P^T[key][row]: the S^T registers, rounded to
-//   bf16, are the B operand as they are; the V^T operand is read from the
-//   row-major V tile with ds_read_b64_tr_b16 (within 16 lanes, a transposed read:
-//   lane i gets column d0 + i of four consecutive key rows).
+//   bf16, are the B operand as they are (element e of lane half h = key
+//   8(e/4) + 4h + e%4 of a 16-key group); the V^T operand of lane (dim c, half h)
+//   is slots 8h .. 8h+7 of dim row c of the packed block: the same keys.
 //
 // Window as a K-slice (one K-step = one chunk of 8 rotary pairs = dims
 // [8c, 8c+8) and [d/2 + 8c, d/2 + 8c + 8)).  Whether pair r contributes to a cell
@@ -68,11 +69,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
-typedef short s16x8_t __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) char lds_char;
 typedef __attribute__((address_space(3))) u32x4_t lds_u32x4;
-typedef __attribute__((address_space(3))) s16x4_t lds_s16x4;
 
 constexpr int kBN = 64;           // keys per tile
 constexpr float kRescale = 8.0f;  // lazy-rescale threshold, log2 units
@@ -90,11 +88,9 @@ struct Cfg {
     static constexpr int kMinWavesPerSimd = kSmall ? 3 : 2;
     static constexpr int kHalf = D / 2;
     static constexpr int kChunks = D / 16;
-    static constexpr int kSegs = D / 8;             // 16-byte segments per V row
     static constexpr int kKTile = kChunks * kBN * 16;  // bf16; [chunk][block][half][key][8]
-    static constexpr int kVStride = D + 32;         // bf16 per V row in LDS
-    static constexpr int kVSlots = kVStride / 8;
-    static constexpr int kVTile = kBN * kVStride;
+    static constexpr int kVBlkBytes = D * 32;          // one packed 16-key V block [d][16]
+    static constexpr int kVTile = kBN * D;             // bf16; four packed blocks
     static constexpr int kKPerWave = 2 * kChunks / kWaves;  // K (chunk, block) units per wave
     static constexpr int kVLoads = kVTile / 512;      // wave-wide 1 KB loads per V tile
     static constexpr int kVPer = (kVLoads + kWaves - 1) / kWaves;
@@ -135,10 +131,6 @@ __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_ex
 // instructions' offset fields.
 __device__ __forceinline__ u32x4_t lds_read_b128(uint32_t byte_addr) {
     return *(const lds_u32x4*)(uintptr_t)byte_addr;
-}
-// transposed 4x4-block read of 16-bit elements (ds_read_b64_tr_b16)
-__device__ __forceinline__ s16x4_t lds_read_tr(uint32_t byte_addr) {
-    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(uintptr_t)byte_addr);
 }
 // byte offset of the LDS buffer of a tile.  Passed through readfirstlane so the
 // compiler treats it as one opaque scalar per tile instead of re-deriving it in
@@ -216,13 +208,14 @@ prefill_kernel(const PrefillParams p) {
     // lane r holds the threshold of pair r (pairs past d/2 never count)
     const int my_w = lane < C::kHalf ? p.win.W[lane] : -1;
 
-    const uint32_t row_bytes = uint32_t(p.h_kv) * D * 2;
     // K: pair-chunk-major streams of cache_tokens keys, chunk c of this head =
     // 32 bytes per key; V: rows of h_kv * d bf16
     const int64_t chunk_bytes = int64_t(p.cache_tokens) * 32;
     const char* kpcm = reinterpret_cast<const char*>(p.k) + (int64_t(b) * p.h_kv + g) * C::kChunks * chunk_bytes;
     const uint32_t k_piece = uint32_t((lane & 31) * 32 + (lane >> 5) * 16);
-    const char* vbytes = reinterpret_cast<const char*>(p.v + (int64_t(b) * p.cache_tokens * p.h_kv + g) * D);
+    // V: packed 16-key blocks [d][16] of this head, ceil(cache_tokens / 16) of them
+    const int n_vblk = (p.cache_tokens + 15) / 16;
+    const char* vhead = reinterpret_cast<const char*>(p.v) + (int64_t(b) * p.h_kv + g) * n_vblk * int64_t(C::kVBlkBytes);
 
     // query fragments (B operand): row `col`, dims of half hh of every chunk
     u32x4_t qf[C::kChunks];
@@ -242,20 +235,12 @@ prefill_kernel(const PrefillParams p) {
     // loads units w, w + 8, ...: lane i reads 16 bytes of key i % 32, half i / 32,
     // so the wave's 1 KB of global memory is contiguous.  A unit whose chunk no
     // cell of the workgroup tile keeps is skipped; the last chunk is always loaded
-    // because the QK of a block always multiplies it.  V: wave w issues the tile's
-    // wave-wide loads w, w + 8, ...; slot s = 64 * load + lane holds (row s /
-    // slots-per-row, segment s % slots-per-row), padding slots re-read segment 0.
-    // In a tile that crosses n_k, keys past it re-read the last key (finite
-    // values; their scores are masked).
+    // because the QK of a block always multiplies it.  V: the tile's four packed
+    // blocks are one contiguous run; wave w copies its kilobytes w, w + W, ...
+    // Blocks past the cache's last one re-read that block (their keys are past
+    // n_k and masked).
     const uint32_t ks_lds = lds_addr(&Ks[0][0]);
     const uint32_t vs_lds = lds_addr(&Vs[0][0]);
-    uint32_t v_dma[C::kVPer];
-#pragma unroll
-    for (int t = 0; t < C::kVPer; ++t) {
-        const int s = 64 * (wave + C::kWaves * t) + lane;
-        const int seg = s % C::kVSlots;
-        v_dma[t] = uint32_t(s / C::kVSlots) * row_bytes + 16u * uint32_t(seg < C::kSegs ? seg : 0);
-    }
     auto tile_need = [&](int j0) __attribute__((always_inline)) -> uint32_t {
         if (!kWin) return (1u << C::kChunks) - 1u;
         const int zlo = max(0, pos_first - (j0 + kBN - 1));
@@ -267,9 +252,6 @@ prefill_kernel(const PrefillParams p) {
     };
     auto issue = [&](int j0, int buf) __attribute__((always_inline)) {
         const uint32_t need = tile_need(j0);
-        const char* vt = vbytes + int64_t(j0) * row_bytes;  // wave-uniform tile base
-        const bool tail = j0 + kBN > p.n_k;
-        const uint32_t last = uint32_t(p.n_k - 1 - j0);
         const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
         for (int t = 0; t < C::kKPerWave; ++t) {
@@ -288,24 +270,18 @@ prefill_kernel(const PrefillParams p) {
         for (int t = 0; t < C::kVPer; ++t) {
             const int u = wave + C::kWaves * t;
             if (u >= C::kVLoads) break;
-            uint32_t off = v_dma[t];
-            if (tail) {
-                const int s = 64 * u + lane;
-                off = min(uint32_t(s / C::kVSlots), last) * row_bytes + (off % row_bytes);
-            }
-            load_to_lds(vt, off, vdst + 1024u * u);
+            const int blk = min(j0 / 16 + (1024 * u) / C::kVBlkBytes, n_vblk - 1);
+            load_to_lds(vhead + int64_t(blk) * C::kVBlkBytes + (1024 * u) % C::kVBlkBytes,
+                        uint32_t(lane) * 16u, vdst + 1024u * u);
         }
     };
 
     // per-lane LDS byte bases of the fragment reads (buffer 0, block 0)
     //   K: unit (chunk c, block kb) at 1 KB * (2 c + kb), half hh, key col
-    //   V: lane group of 16 reads key rows 4 * hh + (l % 16) / 4 (8 rows further
-    //      for elements 4..7), dims 16 * ((l / 16) % 2) + 4 * (l % 4) of each
-    //      32-dim block
+    //   V: packed block q of the tile at q * kVBlkBytes, dim 32 i + col at 1 KB * i,
+    //      slots 8 hh .. 8 hh + 7
     const uint32_t k_lane = ks_lds + uint32_t(hh * 512 + col * 16);
-    const int v_dsub = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-    const int v_row = 4 * hh + ((lane & 15) >> 2);
-    const uint32_t v_lane = vs_lds + uint32_t((v_row * C::kVStride + v_dsub) * 2);
+    const uint32_t v_lane = vs_lds + uint32_t(col * 32 + hh * 16);
 
     f32x16_t oacc[D / 32];
 #pragma unroll
@@ -453,14 +429,29 @@ prefill_kernel(const PrefillParams p) {
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
-                for (int i = 0; i < D / 32; ++i) {
-                    const uint32_t o = uint32_t(((32 * kb + 16 * ks) * C::kVStride + 32 * i) * 2);
-                    const s16x4_t lo = lds_read_tr(vb + o);
-                    const s16x4_t hi = lds_read_tr(vb + o + 8 * C::kVStride * 2);
-                    const s16x8_t both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-                    oacc[i] = mfma(__builtin_bit_cast(u32x4_t, both), pb[ks], oacc[i]);
-                }
+                for (int i = 0; i < D / 32; ++i)
+                    oacc[i] = mfma(lds_read_b128(vb + uint32_t((2 * kb + ks) * C::kVBlkBytes + 1024 * i)),
+                                   pb[ks], oacc[i]);
         }
+    };
+
+    // The V slots of keys at or past n_k in the LDS copy of a tile that crosses n_k
+    // (only the last tile can) are set to zero by the whole workgroup before any
+    // wave reads them: the cache past n_k need not hold finite values, and a zero
+    // probability does not cancel a NaN in the matrix product.
+    auto zero_v_tail = [&](int u) __attribute__((always_inline)) {
+        const int j0 = u * kBN;
+        if (j0 + kBN <= p.n_k) return;
+        uint16_t* vt = &Vs[u % C::kStages][0];
+        for (int row = tid; row < 4 * D; row += C::kThreads) {  // row = block * D + dim
+            const int kblk = j0 + 16 * (row / D);
+#pragma unroll
+            for (int sl = 0; sl < 16; ++sl) {
+                const int key = kblk + 8 * ((sl & 7) >> 2) + 4 * (sl >> 3) + (sl & 3);
+                if (key >= p.n_k) vt[row * 16 + sl] = 0;
+            }
+        }
+        __syncthreads();
     };
 
     const int n_tiles = (key_end + kBN - 1) / kBN;
@@ -469,6 +460,7 @@ prefill_kernel(const PrefillParams p) {
     // await this wave's loads of the next tile, barrier
     auto run_tile = [&](int u, auto&& qk) __attribute__((always_inline)) {
         if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
+        zero_v_tail(u);
         if (active(u)) {
             qk(u);
             softmax_pv(u);
@@ -557,6 +549,7 @@ prefill_kernel(const PrefillParams p) {
             default:  // idle: keep the barrier count
                 for (; u < seg_end; ++u) {
                     if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
+                    zero_v_tail(u);
                     vm_wait();
                     barrier();
                 }

@@ -64,16 +64,18 @@ def family_windows_for(head_dim, rope_base, theta, family):
     return win, widths
 
 
-def gpu_prefill(q, k, v, q_pos0, win, scale=0.0, kp=None, n_k=None):
-    """q [B, n_q, h_q, d]; k, v [B, C, h_kv, d] (K is packed pair-chunk-major by the
-    library first unless kp is given); keys 0 .. n_k - 1 (default C) are used."""
+def gpu_prefill(q, k, v, q_pos0, win, scale=0.0, kp=None, n_k=None, vp=None):
+    """q [B, n_q, h_q, d]; k, v [B, C, h_kv, d], packed into the caches by the library
+    first unless kp / vp are given; keys 0 .. n_k - 1 (default C) are used."""
     import paper_2608_02947_amd as atf
     B, n_q, h_q, d = q.shape
     if kp is None:
         kp = pack_kcache(k)
+    if vp is None:
+        vp = pack_vcache(v)
     o = torch.empty_like(q)
     lse = torch.empty((B, h_q, n_q), dtype=torch.float32, device=q.device)
-    atf.atf_prefill(q, kp, v, o, lse, q_pos0, win, scale, n_k=n_k)
+    atf.atf_prefill(q, kp, vp, o, lse, q_pos0, win, scale, n_k=n_k)
     torch.cuda.synchronize()
     return o, lse
 
@@ -99,9 +101,9 @@ def gpu_decode(q, k_bshd, v_bshd, q_pos, win, scale=0.0, kp=None, vp=None, n_k=N
     first; keys 0 .. n_k - 1 (default C) are used."""
     import paper_2608_02947_amd as atf
     B, h_q, d = q.shape
-    _, cap, h_kv, _ = k_bshd.shape
     if kp is None:
         kp = pack_kcache(k_bshd)
+    _, h_kv, _, cap, _ = kp.shape
     if vp is None:
         vp = pack_vcache(v_bshd)
     if n_k is None:

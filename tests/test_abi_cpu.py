@@ -328,3 +328,26 @@ def test_vpack_validation_and_size():
     assert lib.atf_pack_vcache(24, 1 << 20, 1, 4, 1, 64, None) == atf.ATF_EINVAL  # alignment
     assert lib.atf_pack_vcache(16, 1 << 20, 1, 4, 0, 64, None) == atf.ATF_EINVAL
     assert atf.vcache_shape(2, 33, 4, 128) == (2, 4, 3, 128, 16)
+
+
+def test_cache_append_validation_before_launch():
+    lib = atf.library()
+    A = 1 << 30  # four far-apart fake device addresses (nothing is launched)
+    kn, vn, kc, vc = A, 2 * A, 3 * A, 4 * A
+    ok = dict(batch=1, n=4, pos0=8, h_kv=2, d=64, cap=16)
+
+    def call(**kw):
+        a = dict(ok, kn=kn, vn=vn, kc=kc, vc=vc)
+        a.update(kw)
+        return lib.atf_cache_append(a["kn"], a["vn"], a["kc"], a["vc"], a["batch"], a["n"],
+                                    a["pos0"], a["h_kv"], a["d"], a["cap"], None)
+    assert call(n=0) == atf.ATF_OK                          # nothing to write
+    assert call(d=96) == atf.ATF_EUNSUPPORTED
+    for bad in (dict(batch=0), dict(h_kv=0), dict(n=-1), dict(pos0=-1), dict(cap=0),
+                dict(pos0=13), dict(cap=2 ** 31), dict(kn=None), dict(vc=None),
+                dict(kc=kc + 8),                             # misaligned
+                dict(kc=vc + 256),                           # K cache inside the V cache
+                dict(vn=vc + 512),                           # input inside the V cache
+                dict(kn=kc + 64 * 2 * 2 * 4)):               # input inside the K cache
+        assert call(**bad) == atf.ATF_EINVAL, bad
+        assert "cache_append" in atf.atf_last_error()

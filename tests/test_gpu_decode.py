@@ -67,6 +67,33 @@ def test_vpack_bit_exact(shape):
     assert torch.equal(vp.view(torch.int16), ref.view(torch.int16))
 
 
+@pytest.mark.parametrize("shape,cuts", [((2, 100, 3, 128), (0, 7, 40, 41, 100)),
+                                        ((1, 333, 2, 64), (0, 16, 17, 300, 333))])
+def test_cache_append_bit_exact(shape, cuts):
+    """Appending a sequence in pieces at arbitrary offsets writes exactly the packed
+    layouts, and slots of tokens not yet appended keep what the cache held."""
+    import paper_2608_02947_amd as atf
+    B, n, h_kv, d = shape
+    cap = n + 21
+    note(f"cache append {shape} {cuts}")
+    k = W.random_bf16(shape, seed=sum(shape) + 2).to(DEV)
+    v = W.random_bf16(shape, seed=sum(shape) + 3).to(DEV)
+    sentinel = -7.0
+    kc = torch.full(atf.kcache_shape(B, cap, h_kv, d), sentinel, dtype=torch.bfloat16, device=DEV)
+    vc = torch.full(atf.vcache_shape(B, cap, h_kv, d), sentinel, dtype=torch.bfloat16, device=DEV)
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        atf.atf_cache_append(k[:, a:b].contiguous(), v[:, a:b].contiguous(), kc, vc, a)
+        torch.cuda.synchronize()
+        kfull = torch.full((B, cap, h_kv, d), sentinel, dtype=torch.bfloat16, device=DEV)
+        kfull[:, :b] = k[:, :b]
+        assert torch.equal(kc.view(torch.int16), _ref_pack(kfull).view(torch.int16))
+        vfull = torch.full((B, (cap + 15) // 16 * 16, h_kv, d), sentinel, dtype=torch.bfloat16,
+                           device=DEV)
+        vfull[:, :b] = v[:, :b]
+        ref = _ref_vpack(vfull)
+        assert torch.equal(vc.view(torch.int16), ref.view(torch.int16))
+
+
 def _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed, theta=None):
     g = torch.Generator(device="cpu").manual_seed(seed)
     q = torch.randn((B, 1, h_q, d), generator=g).to(torch.bfloat16)

@@ -14,8 +14,8 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, family_windows_for, gpu_prefill, note, pack_kcache, sample_rows,
-                    to_f64, windows_for, workload_window)
+from parity import (compare, family_windows_for, gpu_decode, gpu_prefill, note, pack_kcache,
+                    pack_vcache, sample_rows, to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs a GPU")]
@@ -235,12 +235,52 @@ def test_prefill_chunked_equals_single_shot():
     win, _ = workload_window(wl)
     note("prefill chunked vs single")
     kp = pack_kcache(inp["k"])
-    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win, kp=kp)
+    vp = pack_vcache(inp["v"])
+    o, lse = gpu_prefill(inp["q"], inp["k"], inp["v"], 0, win, kp=kp, vp=vp)
     for s in range(0, n, chunk):
         qc = inp["q"][:, s:s + chunk].contiguous()
-        oc, lc = gpu_prefill(qc, inp["k"], inp["v"], s, win, kp=kp, n_k=s + chunk)
+        oc, lc = gpu_prefill(qc, inp["k"], inp["v"], s, win, kp=kp, vp=vp, n_k=s + chunk)
         assert torch.equal(oc, o[:, s:s + chunk])
         assert torch.equal(lc, lse[:, :, s:s + chunk])
+
+
+def test_prefill_chunks_appended_to_shared_caches_then_decode():
+    """The pipeline of one request: caches allocated for the whole context; each
+    chunk's keys and values are appended (atf_cache_append) and its rows attend the
+    keys written so far; the result is bit-identical to one call over the packed
+    context; then decode steps append their token and read the same caches.
+    Chunk boundaries are multiples of the position tile (floor(256 / G) at d = 128)."""
+    import paper_2608_02947_amd as atf
+    wl = W.WORKLOADS["llama3b_prefill_32k"]
+    tile = 256 // wl.group
+    chunk = tile * 9
+    n = 3 * chunk + tile   # a shorter last chunk
+    cap = n + 40           # room for decode steps, not a multiple of 16
+    inp = W.make_inputs(wl, device=DEV, n_q=n + 2, n_k=n + 2, q_pos0=0)
+    win, widths = workload_window(wl)
+    d, h_kv = wl.head_dim, wl.h_kv
+    note("prefill appended chunks")
+    o_ref, lse_ref = gpu_prefill(inp["q"][:, :n].contiguous(), inp["k"][:, :n].contiguous(),
+                                 inp["v"][:, :n].contiguous(), 0, win)
+    kc = torch.full(atf.kcache_shape(wl.batch, cap, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                    device=DEV)
+    vc = torch.full(atf.vcache_shape(wl.batch, cap, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                    device=DEV)
+    for s in range(0, n, chunk):
+        e = min(s + chunk, n)
+        atf.atf_cache_append(inp["k"][:, s:e].contiguous(), inp["v"][:, s:e].contiguous(), kc, vc, s)
+        oc, lc = gpu_prefill(inp["q"][:, s:e].contiguous(), None, None, s, win, kp=kc, vp=vc, n_k=e)
+        assert torch.equal(oc, o_ref[:, s:e])
+        assert torch.equal(lc, lse_ref[:, :, s:e])
+    # two decode steps at positions n and n + 1 over the same caches
+    for pos in (n, n + 1):
+        atf.atf_cache_append(inp["k"][:, pos:pos + 1].contiguous(),
+                             inp["v"][:, pos:pos + 1].contiguous(), kc, vc, pos)
+        qd = inp["q"][:, pos].contiguous()
+        od, ld = gpu_decode(qd, None, None, pos, win, kp=kc, vp=vc, n_k=pos + 1)
+        o1, l1, _ = oracle.attend(inp["q"][:, pos:pos + 1].cpu(), inp["k"][:, :pos + 1].cpu(),
+                                  inp["v"][:, :pos + 1].cpu(), pos, widths)
+        compare(to_f64(od), to_f64(ld), o1[:, 0], l1[:, :, 0], f"decode at {pos}")
 
 
 def test_prefill_cache_capacity_and_uninitialised_tail():
