@@ -258,14 +258,14 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "c719073f8ef6a073e309e64a4a8c274446c720e171dd87838b0e2afa6c89a6d1",
-        "fetch_kib": 79793418.94, "write_kib": 1020823.06,
+        "sha256": "62cd98c4d4032477332eaf068cd0e0ab2a1256d4b8f9326f59eaa8969a4bd2f3",
+        "fetch_kib": 79575537.13, "write_kib": 933438.34,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "33bbe14e0fd352c0b347be7cb3c111eecf74a53139a0b5531beafb1eaf1795c0",
-        "fetch_kib": 737777.44, "write_kib": 4062.9,
+        "sha256": "33d119042201d3f5b4dd9d1d0558f5b0d641235d32e332478876bd392052eaa5",
+        "fetch_kib": 737777.79, "write_kib": 4061.39,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
