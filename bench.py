@@ -246,7 +246,54 @@ def config_table(atf, W, dev, stream):
                 "speedup_vs_full_window": round(t_off / t, 4), "cache_sets": nset}
         del sets, qd, od, lsed, ws
         torch.cuda.empty_cache()
+    out.update(ragged_decode_config(atf, W, dev, stream))
     return out
+
+
+RAGGED_ROWS = [131072, 98304, 65536, 32768, 16384, 8192, 120000, 4096]
+
+
+def ragged_decode_config(atf, W, dev, stream):
+    """A ragged decode batch on the Llama-3.2-3B-shaped 128K caches: row b holds
+    RAGGED_ROWS[b] keys and its query at that position (atf_decode_ragged, row
+    arrays on the device).  Bytes are summed per row like the uniform decode."""
+    wl = W.WORKLOADS["llama3b_decode_128k"]
+    d, B = wl.head_dim, wl.batch
+    assert len(RAGGED_ROWS) == B and max(RAGGED_ROWS) <= wl.n_k
+    inp = W.make_inputs(wl, device=dev)
+    kp = torch.empty(atf.kcache_shape(B, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
+    vp = torch.empty(atf.vcache_shape(B, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
+    atf.atf_pack_kcache(inp["k"], kp)
+    atf.atf_pack_vcache(inp["v"], vp)
+    qd = inp["q"][:, 0].contiguous()  # timing only: the query values do not change the work
+    del inp
+    od = torch.empty_like(qd)
+    lsed = torch.empty((B, wl.h_q), dtype=torch.float32, device=dev)
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, wl.h_q, wl.h_kv, wl.n_k, d),
+                     dtype=torch.uint8, device=dev)
+    rows = torch.tensor(RAGGED_ROWS, dtype=torch.int32, device=dev)
+    th = W.workload_theta(wl)
+    win = atf.Window(d, wl.rope_base, wl.k, None if th is None else th.numpy())
+    off = atf.Window(d, wl.rope_base, math.inf)
+
+    def nbytes(w):
+        tot = 0
+        for nk in RAGGED_ROWS:
+            R, Cd = atf.atf_count_terms(w, 1, nk, nk)
+            tot += wl.h_kv * (4 * R + 2 * d * Cd) + wl.h_q * d * 4
+        return tot
+    run = lambda w: atf.atf_decode_ragged(qd, kp, vp, od, lsed, rows, rows, wl.n_k, w, ws,
+                                          stream=stream)
+    t_off = _median_ms(lambda: run(off), stream, 3, 30)
+    t = _median_ms(lambda: run(win), stream, 3, 30)
+    nb = nbytes(win)
+    gbs = nb / (t * 1e-3) / 1e9
+    del kp, vp, qd, od, lsed, ws
+    torch.cuda.empty_cache()
+    return {"llama3b_decode_ragged_b8": {
+        "ms": round(t, 4), "GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": nb, "rows": RAGGED_ROWS, "full_window_ms": round(t_off, 4),
+        "speedup_vs_full_window": round(t_off / t, 4)}}
 
 
 # HBM bytes moved by one launch of a kernel at the benchmark workload, from two

@@ -236,6 +236,29 @@ int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o,
                int64_t cache_tokens, const atf_window *w, float softmax_scale,
                void *workspace, size_t workspace_bytes, void *hip_stream);
 
+/* Decode of a ragged batch: row b holds one query token at position q_pos_rows[b]
+ * against keys 0 .. min(q_pos_rows[b], n_k_rows[b] - 1) of its own cache entry
+ * (Sec. 5: the last query row of each sequence, for a batch of sequences of
+ * different lengths).  Everything else is atf_decode: same layouts, window,
+ * split-KV plan and merge, with n_k replaced by max_n_k for the plan.
+ *   n_k_rows    int32 [batch], DEVICE, 4-byte aligned: keys of each row's cache
+ *   q_pos_rows  int32 [batch], DEVICE, 4-byte aligned: query position of each row
+ *   max_n_k     host bound on n_k_rows (1 .. cache_tokens); the workspace is
+ *               atf_decode_workspace_bytes(batch, h_q, h_kv, max_n_k, d)
+ * The row arrays stay on the device (no host synchronisation).  The kernel clamps
+ * each row to n_k_rows[b] in [0, max_n_k] and q_pos_rows[b] in [0, 2^31 - 3], so it
+ * never reads outside the row's cache whatever the arrays hold; values outside
+ * those ranges are a caller error that this clamping makes harmless, not a
+ * supported input.  A row with no key (n_k_rows[b] == 0) has an empty softmax:
+ * its output is 0 and its LSE is -INFINITY.
+ * Errors: as atf_decode, plus ATF_EINVAL for NULL/misaligned row arrays and
+ * max_n_k < 1 or > cache_tokens.  Deterministic: equal inputs give equal bits. */
+int atf_decode_ragged(const void *q, const void *k_cache, const void *v_cache, void *o, float *lse,
+                      int32_t batch, const int32_t *n_k_rows, const int32_t *q_pos_rows,
+                      int64_t max_n_k, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
+                      const atf_window *w, float softmax_scale, void *workspace,
+                      size_t workspace_bytes, void *hip_stream);
+
 /* Message of the most recent failed call on this thread ("" if none). */
 const char *atf_last_error(void);
 

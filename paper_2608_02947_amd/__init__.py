@@ -15,6 +15,7 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- V-cache layout.
 - :func:`atf_cache_append` -- write new tokens into both caches at a position.
 - :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
+- :func:`atf_decode_ragged` -- the same for a batch of sequences of different lengths.
 """
 from __future__ import annotations
 
@@ -72,6 +73,8 @@ def _load():
         "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
         "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, f32, P,
                                       ctypes.c_size_t, P]),
+        "atf_decode_ragged": (ctypes.c_int, [P, P, P, P, P, i32, P, P, i64, i32, i32, i64, W, f32,
+                                             P, ctypes.c_size_t, P]),
         "atf_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -84,7 +87,7 @@ def _load():
 _lib = _load()
 EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
-            "atf_decode_workspace_bytes", "atf_decode", "atf_last_error")
+            "atf_decode_workspace_bytes", "atf_decode", "atf_decode_ragged", "atf_last_error")
 
 
 def library():
@@ -315,4 +318,32 @@ def atf_decode(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window, workspace,
                          ctypes.byref(cw), float(softmax_scale),
                          _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
                          _stream_ptr(stream))
+    _check(rc)
+
+
+def atf_decode_ragged(q, k_pcm, v_pack, o, lse, n_k_rows, q_pos_rows, max_n_k: int,
+                      window: Window, workspace, softmax_scale: float = 0.0, stream=None):
+    """Ragged batch: q [B, h_q, d]; row b attends keys 0 .. min(q_pos_rows[b],
+    n_k_rows[b] - 1) of its cache entry.  n_k_rows and q_pos_rows: int32 device tensors
+    [B]; max_n_k bounds n_k_rows and sizes the workspace
+    (atf_decode_workspace_bytes(B, h_q, h_kv, max_n_k, d)).  Other arguments as
+    atf_decode."""
+    torch = _torch()
+    B, h_q, d = q.shape
+    if k_pcm.dim() != 5:
+        raise ValueError("atf_decode_ragged: k_pcm must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_pcm.shape
+    if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
+            tuple(k_pcm.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_pack.shape) != vcache_shape(B, cap, h_kv, d) or \
+            tuple(n_k_rows.shape) != (B,) or tuple(q_pos_rows.shape) != (B,):
+        raise ValueError("atf_decode_ragged: inconsistent shapes")
+    cw, keep = window.as_c()
+    rc = _lib.atf_decode_ragged(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pcm, torch.bfloat16, "k"),
+        _dev_ptr(v_pack, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+        _dev_ptr(lse, torch.float32, "lse"), B, _dev_ptr(n_k_rows, torch.int32, "n_k_rows"),
+        _dev_ptr(q_pos_rows, torch.int32, "q_pos_rows"), int(max_n_k), h_q, h_kv, cap,
+        ctypes.byref(cw), float(softmax_scale), _dev_ptr(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _stream_ptr(stream))
     _check(rc)

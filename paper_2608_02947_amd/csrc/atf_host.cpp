@@ -432,40 +432,53 @@ size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int6
     return ws_layout(batch, h_q, s, head_dim).total;
 }
 
-int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
-               int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
-               int64_t cache_tokens, const atf_window* w, float softmax_scale, void* workspace,
-               size_t workspace_bytes, void* hip_stream) {
-    if (w == nullptr) return fail(ATF_EINVAL, "decode: NULL window");
+}  // extern "C"
+
+namespace {
+
+// Shared by atf_decode (every row has n_k keys and its query at q_pos) and
+// atf_decode_ragged (row b has n_k_rows[b] keys and its query at q_pos_rows[b],
+// device arrays; n_k is then their upper bound and q_pos is unused).
+int decode_impl(const char* fn, const void* q, const void* k_cache, const void* v_cache, void* o,
+                float* lse, int32_t batch, int64_t n_k, int64_t q_pos, const int32_t* n_k_rows,
+                const int32_t* q_pos_rows, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
+                const atf_window* w, float softmax_scale, void* workspace, size_t workspace_bytes,
+                void* hip_stream) {
+    const bool ragged = n_k_rows != nullptr || q_pos_rows != nullptr;
+    if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
     const int d = w->head_dim;
     if (d != 64 && d != 128)
-        return fail(ATF_EUNSUPPORTED, "decode: head_dim %d not built (64 or 128)", d);
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
     if (batch < 1 || n_k < 1 || q_pos < 0 || h_q < 1 || h_kv < 1)
-        return fail(ATF_EINVAL, "decode: need batch >= 1, n_k >= 1, q_pos >= 0, heads >= 1");
+        return fail(ATF_EINVAL, "%s: need batch >= 1, n_k >= 1, q_pos >= 0, heads >= 1", fn);
     if (h_q % h_kv != 0)
-        return fail(ATF_EINVAL, "decode: h_q %d not a multiple of h_kv %d", h_q, h_kv);
+        return fail(ATF_EINVAL, "%s: h_q %d not a multiple of h_kv %d", fn, h_q, h_kv);
     if (q_pos >= kPosLimit || n_k > kPosLimit)
-        return fail(ATF_EINVAL, "decode: positions must stay below 2^31 - 1");
+        return fail(ATF_EINVAL, "%s: positions must stay below 2^31 - 1", fn);
     if (cache_tokens == 0) cache_tokens = n_k;
     if (cache_tokens < n_k || cache_tokens > kPosLimit)
-        return fail(ATF_EINVAL, "decode: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1",
+        return fail(ATF_EINVAL, "%s: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1", fn,
                     (long long)cache_tokens, (long long)n_k);
     if (!std::isfinite(softmax_scale))
-        return fail(ATF_EINVAL, "decode: softmax_scale must be finite");
+        return fail(ATF_EINVAL, "%s: softmax_scale must be finite", fn);
     atf::DecodeParams p{};
     int rc = build_table(w, &p.win);
     if (rc != ATF_OK) return rc;
     if (!q || !k_cache || !v_cache || !o || !lse)
-        return fail(ATF_EINVAL, "decode: NULL tensor pointer");
+        return fail(ATF_EINVAL, "%s: NULL tensor pointer", fn);
+    if (ragged && (!n_k_rows || !q_pos_rows))
+        return fail(ATF_EINVAL, "%s: NULL row-length or row-position array", fn);
     if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(o, 16) ||
         !aligned(lse, 4))
-        return fail(ATF_EINVAL, "decode: q/k/v/o must be 16-byte and lse 4-byte aligned");
+        return fail(ATF_EINVAL, "%s: q/k/v/o must be 16-byte and lse 4-byte aligned", fn);
+    if (ragged && (!aligned(n_k_rows, 4) || !aligned(q_pos_rows, 4)))
+        return fail(ATF_EINVAL, "%s: row arrays must be 4-byte aligned", fn);
     const int32_t splits = atf::decode_splits(batch, h_kv, n_k);
     const WsLayout L = ws_layout(batch, h_q, splits, d);
     if (workspace == nullptr || workspace_bytes < L.total)
-        return fail(ATF_EWORKSPACE, "decode: workspace of %zu bytes needed, %zu given", L.total,
+        return fail(ATF_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, L.total,
                     workspace == nullptr ? size_t(0) : workspace_bytes);
-    if (!aligned(workspace, 16)) return fail(ATF_EINVAL, "decode: workspace must be 16-byte aligned");
+    if (!aligned(workspace, 16)) return fail(ATF_EINVAL, "%s: workspace must be 16-byte aligned", fn);
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
     const int32_t group = h_q / h_kv;
     int32_t hpb = 1;
@@ -491,19 +504,48 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
     p.h_kv = h_kv;
     p.group = group;
     p.heads_per_block = hpb;
-    const int64_t last = q_pos < n_k - 1 ? q_pos : n_k - 1;
+    p.n_k_rows = n_k_rows;
+    p.q_pos_rows = q_pos_rows;
+    // keys any row can reach: the split plan covers them (rows with fewer keys leave
+    // their later splits empty)
+    const int64_t last = ragged ? n_k - 1 : (q_pos < n_k - 1 ? q_pos : n_k - 1);
     p.n_valid = static_cast<int32_t>(last + 1);
     p.splits = splits;
     const int64_t per = (p.n_valid + splits - 1) / splits;
     const int64_t step_tokens = (per + atf::kDecodeTokenStep - 1) / atf::kDecodeTokenStep *
                                 atf::kDecodeTokenStep;
     if (step_tokens * splits >= kPosLimit)
-        return fail(ATF_EINVAL, "decode: cache too long for the split plan");
+        return fail(ATF_EINVAL, "%s: cache too long for the split plan", fn);
     p.split_tokens = static_cast<int32_t>(step_tokens);
     p.scale_log2 = scale * 1.4426950408889634f;
     hipError_t e = atf::launch_decode(p, d, static_cast<hipStream_t>(hip_stream));
-    if (e != hipSuccess) return fail(ATF_EHIP, "decode: launch failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return ATF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+               int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q, int32_t h_kv,
+               int64_t cache_tokens, const atf_window* w, float softmax_scale, void* workspace,
+               size_t workspace_bytes, void* hip_stream) {
+    return decode_impl("decode", q, k_cache, v_cache, o, lse, batch, n_k, q_pos, nullptr, nullptr,
+                       h_q, h_kv, cache_tokens, w, softmax_scale, workspace, workspace_bytes,
+                       hip_stream);
+}
+
+int atf_decode_ragged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
+                      int32_t batch, const int32_t* n_k_rows, const int32_t* q_pos_rows,
+                      int64_t max_n_k, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
+                      const atf_window* w, float softmax_scale, void* workspace,
+                      size_t workspace_bytes, void* hip_stream) {
+    if (!n_k_rows || !q_pos_rows)
+        return fail(ATF_EINVAL, "decode_ragged: NULL row-length or row-position array");
+    return decode_impl("decode_ragged", q, k_cache, v_cache, o, lse, batch, max_n_k, 0, n_k_rows,
+                       q_pos_rows, h_q, h_kv, cache_tokens, w, softmax_scale, workspace,
+                       workspace_bytes, hip_stream);
 }
 
 }  // extern "C"

@@ -49,6 +49,10 @@ struct DecodeParams {
     int32_t cache_tokens;     // tokens each cache entry is allocated for (>= n_k)
     int32_t heads_per_block;  // query heads handled by one workgroup (divides group, <= 32)
     int32_t n_valid;          // keys 0 .. n_valid - 1 are causal
+    const int32_t* n_k_rows;  // ragged batch: device [B] keys of each row (clamped to
+                              // [0, n_k]), or nullptr: every row has n_k keys
+    const int32_t* q_pos_rows;  // ragged batch: device [B] query position of each row
+                                // (clamped to [0, 2^31 - 2]), or nullptr: q_pos
     int32_t splits;
     int32_t split_tokens;     // tokens per split (multiple of the workgroup's token step)
     float scale_log2;

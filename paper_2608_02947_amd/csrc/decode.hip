@@ -89,8 +89,16 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     const int hq0 = g * p.group + sub * NH;
     const bool head_ok = col < NH;
 
+    // this row's keys and query position (a ragged batch gives them per row; the
+    // clamps keep every read inside the row's cache)
+    int n_k = p.n_k, q_pos = p.q_pos, n_valid = p.n_valid;
+    if (p.n_k_rows != nullptr) {
+        n_k = min(max(p.n_k_rows[b], 0), p.n_k);
+        q_pos = min(max(p.q_pos_rows[b], 0), 0x7FFFFFFD);
+        n_valid = min(n_k, q_pos + 1);
+    }
     const int t_begin = split * p.split_tokens;
-    const int t_end = min(p.n_valid, t_begin + p.split_tokens);
+    const int t_end = min(n_valid, t_begin + p.split_tokens);
     const int64_t cap = p.cache_tokens;  // stream length of the caches
     const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * cap * 16;
     const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * ((cap + 15) / 16) * D * 16;
@@ -117,8 +125,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 
     for (int t0 = t_begin + 32 * wave; t0 < t_end; t0 += 32 * kWaves) {
         const int t_last = min(t0 + 31, t_end - 1);
-        const int zhi = p.q_pos - t0;
-        const int zlo = max(0, p.q_pos - t_last);
+        const int zhi = q_pos - t0;
+        const int zlo = max(0, q_pos - t_last);
         const uint64_t full = __ballot(my_w >= zhi);
         const uint64_t keep = __ballot(my_w >= zlo);
 
@@ -146,12 +154,12 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 #pragma unroll
             for (int i = 0; i < kDB; ++i) {
                 u32x4_t z = {0u, 0u, 0u, 0u};
-                if (16 * blk < p.n_k)
+                if (16 * blk < n_k)
                     z = *reinterpret_cast<const u32x4_t*>(vblocks + (int64_t(blk) * D + 32 * i + col) * 16 + 8 * hh);
                 vf[ks][i] = z;
             }
-            if (16 * blk < p.n_k && 16 * blk + 16 > p.n_k) {
-                const int lim = p.n_k - 16 * blk - 4 * hh;  // slot e valid iff 8(e/4) + e%4 < lim
+            if (16 * blk < n_k && 16 * blk + 16 > n_k) {
+                const int lim = n_k - 16 * blk - 4 * hh;  // slot e valid iff 8(e/4) + e%4 < lim
 #pragma unroll
                 for (int i = 0; i < kDB; ++i)
 #pragma unroll
@@ -194,7 +202,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                     qfc = qf[cc];
                 }
             const f32x16_t t = mfma(kfc, keep_pairs(qfc, uint32_t(grp >> (8 * c))), zero16());
-            const int thr = p.q_pos - t0 - 4 * hh - wr;  // keep iff off(v) >= thr
+            const int thr = q_pos - t0 - 4 * hh - wr;  // keep iff off(v) >= thr
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const int off = 8 * (v / 4) + (v % 4);
@@ -339,8 +347,10 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
         float acc = 0.f;
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc += s_red[tid + 32 * k];
-        p.o[int64_t(bh) * D + d0 + x] = __builtin_bit_cast(uint16_t, (__bf16)(acc / L));
-        if (blockIdx.y == 0 && tid == 0) p.lse[bh] = M * 0.69314718055994531f + logf(L);
+        // a ragged row without keys has an empty softmax: O = 0, LSE = -inf
+        const bool empty = !(L > 0.f);
+        p.o[int64_t(bh) * D + d0 + x] = __builtin_bit_cast(uint16_t, (__bf16)(empty ? 0.f : acc / L));
+        if (blockIdx.y == 0 && tid == 0) p.lse[bh] = empty ? -INFINITY : M * 0.69314718055994531f + logf(L);
     }
 }
 

@@ -304,6 +304,34 @@ def test_decode_validation_before_launch():
     assert call(ws_bytes=need, cache_tokens=131071) == atf.ATF_EINVAL   # below n_k
 
 
+def test_decode_ragged_validation_before_launch():
+    """Every call below fails validation, so nothing is launched (the pointers are
+    placeholders)."""
+    lib = atf.library()
+    need = atf.atf_decode_workspace_bytes(8, 24, 8, 131072, 128)
+
+    def call(ws=16, ws_bytes=None, d=128, nk_rows=1 << 12, qp_rows=1 << 13, **kw):
+        a = dict(batch=8, max_n_k=131072, h_q=24, h_kv=8, cache_tokens=0)
+        a.update(kw)
+        w, kp = atf.Window(d, 5e5, 2.0).as_c()
+        return lib.atf_decode_ragged(16, 16, 16, 16, 16, a["batch"], nk_rows, qp_rows,
+                                     a["max_n_k"], a["h_q"], a["h_kv"], a["cache_tokens"],
+                                     ctypes.byref(w), 0.0, ws,
+                                     need - 1 if ws_bytes is None else ws_bytes, None)
+    assert call() == atf.ATF_EWORKSPACE              # everything else valid
+    assert call(ws=None, ws_bytes=need) == atf.ATF_EWORKSPACE
+    assert call(nk_rows=None) == atf.ATF_EINVAL
+    assert call(qp_rows=None) == atf.ATF_EINVAL
+    assert call(nk_rows=(1 << 12) + 2) == atf.ATF_EINVAL   # row arrays are int32, 4-byte aligned
+    assert call(qp_rows=(1 << 13) + 1) == atf.ATF_EINVAL
+    assert call(max_n_k=0) == atf.ATF_EINVAL
+    assert call(max_n_k=131072, cache_tokens=1000) == atf.ATF_EINVAL   # bound above the capacity
+    assert call(d=80) == atf.ATF_EUNSUPPORTED
+    assert call(h_kv=5) == atf.ATF_EINVAL
+    assert call(batch=0) == atf.ATF_EINVAL
+    assert "decode_ragged" in atf.atf_last_error()
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

@@ -239,3 +239,123 @@ def test_decode_cache_capacity_and_uninitialised_tail():
     o, lse = gpu_decode(qd, kc.to(DEV), vc.to(DEV), n_k, win, n_k=n_k)
     o_ref, lse_ref, _ = oracle.attend(q, k, v, n_k, widths)
     compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], "capacity")
+
+
+# ---------------------------------------------------------------------------
+# ragged batch: per-row cache length and query position (device arrays)
+# ---------------------------------------------------------------------------
+def _ragged_inputs(n_ks, q_poss, cap, h_q, h_kv, d, base, seed, fill=float("nan")):
+    """Row b: q at q_poss[b], keys 0 .. n_ks[b] - 1 (rotated at their positions);
+    cache slots past n_ks[b] hold `fill` (they must never be used)."""
+    B = len(n_ks)
+    th = W.rope_theta(d, base)
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.empty((B, 1, h_q, d), dtype=torch.bfloat16)
+    kc = torch.full((B, cap, h_kv, d), fill, dtype=torch.bfloat16)
+    vc = torch.full((B, cap, h_kv, d), fill, dtype=torch.bfloat16)
+    for b, (nk, qp) in enumerate(zip(n_ks, q_poss)):
+        qb = torch.randn((1, 1, h_q, d), generator=g).to(torch.bfloat16)
+        q[b:b + 1] = W.rotate_half(qb, torch.tensor([qp]), th)
+        if nk:
+            kb = torch.randn((1, nk, h_kv, d), generator=g).to(torch.bfloat16)
+            kc[b:b + 1, :nk] = W.rotate_half(kb, torch.arange(0, nk), th)
+            vc[b:b + 1, :nk] = torch.randn((1, nk, h_kv, d), generator=g).to(torch.bfloat16)
+    return q, kc, vc
+
+
+def _gpu_decode_ragged(q, kc, vc, n_ks, q_poss, max_n_k, win):
+    import paper_2608_02947_amd as atf
+    B, h_q, d = q.shape
+    kp, vp = pack_kcache(kc), pack_vcache(vc)
+    h_kv = kp.shape[1]
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, max_n_k, d), dtype=torch.uint8,
+                     device=DEV)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, h_q), dtype=torch.float32, device=DEV)
+    nk_d = torch.tensor(n_ks, dtype=torch.int32, device=DEV)
+    qp_d = torch.tensor(q_poss, dtype=torch.int32, device=DEV)
+    atf.atf_decode_ragged(q, kp, vp, o, lse, nk_d, qp_d, max_n_k, win, ws)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+def _ragged_parity(n_ks, q_poss, cap, h_q, h_kv, d, base, kwin, seed, max_n_k=None, label=""):
+    note(f"decode ragged {label} n_k={n_ks} q_pos={q_poss} cap={cap} h={h_q}/{h_kv} d={d}")
+    q, kc, vc = _ragged_inputs(n_ks, q_poss, cap, h_q, h_kv, d, base, seed)
+    max_n_k = max(max(n_ks), 1) if max_n_k is None else max_n_k
+    win, _ = windows_for(d, base, kwin, None, n_ctx=max(q_poss) + 1)
+    o, lse = _gpu_decode_ragged(q[:, 0].contiguous().to(DEV), kc.to(DEV), vc.to(DEV), n_ks,
+                                q_poss, max_n_k, win)
+    o, lse = to_f64(o), to_f64(lse)
+    for b, (nk, qp) in enumerate(zip(n_ks, q_poss)):
+        if nk == 0:
+            # no key: an empty softmax gives O = 0 and LSE = -inf
+            assert np.all(o[b] == 0.0) and np.all(lse[b] == -np.inf), (label, b)
+            continue
+        _, widths = windows_for(d, base, kwin, None, n_ctx=qp + 1)
+        o_ref, lse_ref, _ = oracle.attend(q[b:b + 1], kc[b:b + 1, :nk], vc[b:b + 1, :nk], qp,
+                                          widths)
+        compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"{label} row {b}")
+
+
+RAGGED_CASES = [
+    # n_k per row, q_pos per row, cache capacity, h_q, h_kv, d, base, k
+    ([1, 5, 300, 1000, 2049, 777], [1, 5, 300, 1000, 2049, 777], 2100, 7, 1, 128, 1e4, 2.0),
+    ([2049, 33, 1500, 1], [5000, 33, 700, 0], 2049, 8, 2, 64, 1e6, 2.0),   # past / inside the cache
+    ([0, 400, 0, 129], [0, 400, 10, 129], 512, 6, 2, 128, 5e5, 2.0),       # empty rows
+    ([4096, 4000, 17], [4096, 4000, 17], 4096, 16, 2, 128, 100.0, 2.0),   # saturated windows
+    ([999, 3, 640], [999, 3, 640], 1024, 3, 1, 128, 1e4, math.inf),       # window off
+]
+
+
+@pytest.mark.parametrize("case", RAGGED_CASES, ids=lambda c: f"B{len(c[0])}_d{c[5]}_k{c[7]}")
+def test_decode_ragged_rows(case):
+    n_ks, q_poss, cap, h_q, h_kv, d, base, kwin = case
+    _ragged_parity(n_ks, q_poss, cap, h_q, h_kv, d, base, kwin, seed=sum(n_ks) % 9973,
+                   label=f"ragged d={d}")
+
+
+def test_decode_ragged_max_bound_above_rows():
+    """max_n_k larger than every row (a cache allocated for longer sequences)."""
+    _ragged_parity([300, 70, 1], [300, 70, 1], 4096, 14, 2, 64, 1e6, 2.0, seed=5, max_n_k=4000,
+                   label="loose bound")
+
+
+def test_decode_ragged_equals_uniform_bit_exact():
+    """Equal rows take the same split plan and arithmetic as atf_decode: equal bits."""
+    B, n_k, h_q, h_kv, d = 4, 1500, 12, 4, 128
+    q, kc, vc = _ragged_inputs([n_k] * B, [n_k] * B, n_k, h_q, h_kv, d, 1e4, seed=11)
+    win, _ = windows_for(d, 1e4, 2.0, None, n_ctx=n_k + 1)
+    qd = q[:, 0].contiguous().to(DEV)
+    o_r, lse_r = _gpu_decode_ragged(qd, kc.to(DEV), vc.to(DEV), [n_k] * B, [n_k] * B, n_k, win)
+    o_u, lse_u = gpu_decode(qd, kc.to(DEV), vc.to(DEV), n_k, win)
+    assert torch.equal(o_r, o_u) and torch.equal(lse_r, lse_u)
+
+
+def test_decode_ragged_llama_128k_rows():
+    """Llama-3.2-3B-shaped ragged batch of 8 up to 128K keys (llama3-effective
+    table): every (row, head) against the oracle."""
+    wl = W.WORKLOADS["llama3b_decode_128k"]
+    d, cap = wl.head_dim, wl.n_k
+    n_ks = [cap, 65536, 100000, 3, 1, 77777, cap - 5, 32768]
+    note(f"decode ragged llama 128K n_k={n_ks}")
+    th = W.workload_theta(wl)
+    g = torch.Generator(device="cpu").manual_seed(wl.seed)
+    q = torch.empty((8, 1, wl.h_q, d), dtype=torch.bfloat16)
+    kc = torch.zeros((8, cap, wl.h_kv, d), dtype=torch.bfloat16)
+    vc = torch.zeros((8, cap, wl.h_kv, d), dtype=torch.bfloat16)
+    rth = W.rotation_theta(wl)
+    for b, nk in enumerate(n_ks):
+        q[b:b + 1] = W.rotate_half(torch.randn((1, 1, wl.h_q, d), generator=g).to(torch.bfloat16),
+                                   torch.tensor([nk]), rth)
+        kc[b:b + 1, :nk] = W.rotate_half(
+            torch.randn((1, nk, wl.h_kv, d), generator=g).to(torch.bfloat16), torch.arange(0, nk), rth)
+        vc[b:b + 1, :nk] = torch.randn((1, nk, wl.h_kv, d), generator=g).to(torch.bfloat16)
+    win, _ = windows_for(d, wl.rope_base, wl.k, th, n_ctx=cap + 1)
+    o, lse = _gpu_decode_ragged(q[:, 0].contiguous().to(DEV), kc.to(DEV), vc.to(DEV), n_ks, n_ks,
+                                cap, win)
+    o, lse = to_f64(o), to_f64(lse)
+    for b, nk in enumerate(n_ks):
+        _, widths = windows_for(d, wl.rope_base, wl.k, th, n_ctx=nk + 1)
+        o_ref, lse_ref, _ = oracle.attend(q[b:b + 1], kc[b:b + 1, :nk], vc[b:b + 1, :nk], nk, widths)
+        compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"llama128k row {b}")
