@@ -305,14 +305,14 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "62cd98c4d4032477332eaf068cd0e0ab2a1256d4b8f9326f59eaa8969a4bd2f3",
+        "sha256": "1eed185d89ac8d3cc1f4ba5f6564ef9ee96645d687a5c501ce0fc92ec73eae20",
         "fetch_kib": 79575537.13, "write_kib": 933438.34,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "33d119042201d3f5b4dd9d1d0558f5b0d641235d32e332478876bd392052eaa5",
-        "fetch_kib": 737777.79, "write_kib": 4061.39,
+        "sha256": "106b95273e061b9ad4561b7842cd24c14f0be3b86e32394af93379abd9da6557",
+        "fetch_kib": 737755.96, "write_kib": 4062.14,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
