@@ -305,13 +305,13 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "1eed185d89ac8d3cc1f4ba5f6564ef9ee96645d687a5c501ce0fc92ec73eae20",
+        "sha256": "2875d0a02000ad90ce53d38e435918acc0baea4af9e8e9fc13409da41135d490",
         "fetch_kib": 79575537.13, "write_kib": 933438.34,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "106b95273e061b9ad4561b7842cd24c14f0be3b86e32394af93379abd9da6557",
+        "sha256": "afc073f3a32a1e944a72518ee50517b02723d24eb92802f4ab6da26aa28f4791",
         "fetch_kib": 737755.96, "write_kib": 4062.14,
     },
 }

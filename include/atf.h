@@ -203,8 +203,9 @@ int atf_cache_append(const void *k_new, const void *v_new, void *k_cache, void *
                      int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
                      int64_t cache_tokens, void *hip_stream);
 
-/* Bytes of device workspace that atf_decode needs for these sizes (split-KV
- * partial softmax states).  Returns 0 for invalid sizes. */
+/* Bytes of device workspace that atf_decode and atf_decode_ragged need for these
+ * sizes (split-KV partial softmax states; the figure covers the split plans of both
+ * calls).  Returns 0 for invalid sizes. */
 size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int64_t n_k,
                                   int32_t head_dim);
 

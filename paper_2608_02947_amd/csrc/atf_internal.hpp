@@ -76,7 +76,7 @@ hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t str
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan: number of KV splits per (batch, kv head) for these sizes.
-int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);
+int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k, bool ragged);
 // Tokens handled per decode workgroup iteration (the split granularity).
 constexpr int32_t kDecodeTokenStep = 128;
 // Largest split count the merge kernel accepts.

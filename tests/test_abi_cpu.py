@@ -292,9 +292,11 @@ def test_decode_validation_before_launch():
         a = dict(batch=8, n_k=131072, q_pos=131072, h_q=24, h_kv=8, cache_tokens=0)
         a.update(kw)
         w, kp = atf.Window(d, 5e5, 2.0).as_c()
+        # the default workspace (16 bytes) is too small for any split plan, so a call
+        # whose other arguments are valid still fails before launching
         return lib.atf_decode(16, 16, 16, 16, 16, a["batch"], a["n_k"], a["q_pos"], a["h_q"],
                               a["h_kv"], a["cache_tokens"], ctypes.byref(w), 0.0, ws,
-                              need - 1 if ws_bytes is None else ws_bytes, None)
+                              16 if ws_bytes is None else ws_bytes, None)
     assert call() == atf.ATF_EWORKSPACE
     assert call(ws=None, ws_bytes=need) == atf.ATF_EWORKSPACE
     assert call(d=80) == atf.ATF_EUNSUPPORTED
@@ -317,7 +319,7 @@ def test_decode_ragged_validation_before_launch():
         return lib.atf_decode_ragged(16, 16, 16, 16, 16, a["batch"], nk_rows, qp_rows,
                                      a["max_n_k"], a["h_q"], a["h_kv"], a["cache_tokens"],
                                      ctypes.byref(w), 0.0, ws,
-                                     need - 1 if ws_bytes is None else ws_bytes, None)
+                                     16 if ws_bytes is None else ws_bytes, None)
     assert call() == atf.ATF_EWORKSPACE              # everything else valid
     assert call(ws=None, ws_bytes=need) == atf.ATF_EWORKSPACE
     assert call(nk_rows=None) == atf.ATF_EINVAL

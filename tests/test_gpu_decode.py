@@ -322,7 +322,8 @@ def test_decode_ragged_max_bound_above_rows():
 
 
 def test_decode_ragged_equals_uniform_bit_exact():
-    """Equal rows take the same split plan and arithmetic as atf_decode: equal bits."""
+    """Equal rows at a size where both split plans are capped by the 128-token step
+    (12 splits) take the same plan and arithmetic as atf_decode: equal bits."""
     B, n_k, h_q, h_kv, d = 4, 1500, 12, 4, 128
     q, kc, vc = _ragged_inputs([n_k] * B, [n_k] * B, n_k, h_q, h_kv, d, 1e4, seed=11)
     win, _ = windows_for(d, 1e4, 2.0, None, n_ctx=n_k + 1)
