@@ -132,6 +132,29 @@ def compare(o_gpu, lse_gpu, o_ref, lse_ref, label=""):
     return mx, mean, ml
 
 
+def compare_rounding_bound(o_gpu, lse_gpu, o_ref, lse_ref, o_absv_ref, label=""):
+    """Element-wise check against the error the arithmetic implies when scores are
+    large and the softmax is peaked (where a fixed 1e-2 on O does not hold).  Each
+    weight p_ij carries the bf16 rounding of P in the PV product (relative 2^-9) and
+    the error of its score, accumulated in fp32 at magnitudes up to ~10^3 (up to
+    ~2e-3 relative: the order the LSE check below bounds); O is rounded to bf16
+    (relative 2^-9).  o_absv_ref is the oracle's output for |V|, i.e.
+    sum_j p_ij |v_j| / l_i, and with a factor 2 over 2^-9 + 2e-3 the bound is
+        |dO| <= 2^-7 * o_absv_ref + 2^-9 * |O| + 1e-4,   |dLSE| <= 1e-3.
+    A missing or wrong rescale of O or of the normaliser gives errors of the order
+    of |O| itself."""
+    og = np.asarray(o_gpu, dtype=np.float64)
+    lg = np.asarray(lse_gpu, dtype=np.float64)
+    assert og.shape == o_ref.shape and lg.shape == lse_ref.shape, label
+    assert np.all(np.isfinite(og)) and np.all(np.isfinite(lg)), f"{label}: non-finite output"
+    bound = 2.0 ** -7 * o_absv_ref + 2.0 ** -9 * np.abs(o_ref) + 1e-4
+    ratio = float(np.max(np.abs(og - o_ref) / bound))
+    ml = float(np.max(np.abs(lg - lse_ref)))
+    assert ratio <= 1.0, f"{label}: O error {ratio:.3f} x its rounding bound"
+    assert ml <= LSE_MAX_ABS, f"{label}: LSE max-abs {ml}"
+    return ratio, ml
+
+
 def to_f64(t):
     return t.detach().float().cpu().numpy().astype(np.float64)
 

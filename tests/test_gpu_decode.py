@@ -14,7 +14,7 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, family_windows_for, gpu_decode, note, pack_kcache, pack_vcache,
+from parity import (compare_rounding_bound, compare, family_windows_for, gpu_decode, note, pack_kcache, pack_vcache,
                     to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
@@ -360,3 +360,28 @@ def test_decode_ragged_llama_128k_rows():
         _, widths = windows_for(d, wl.rope_base, wl.k, th, n_ctx=nk + 1)
         o_ref, lse_ref, _ = oracle.attend(q[b:b + 1], kc[b:b + 1, :nk], vc[b:b + 1, :nk], nk, widths)
         compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"llama128k row {b}")
+
+
+@pytest.mark.parametrize("pattern", ["rising", "lognormal"])
+def test_decode_large_scores_rescale(pattern):
+    """Scores of order 100s along the cache: split partials with very different
+    maxima and repeated raises of the running max within each split."""
+    B, n_k, h_q, h_kv, d = 2, 5000, 8, 2, 128
+    g = torch.Generator(device="cpu").manual_seed(123)
+    q = torch.randn((B, 1, h_q, d), generator=g) * 3.0
+    k = torch.randn((B, n_k, h_kv, d), generator=g)
+    if pattern == "rising":
+        k = k * torch.linspace(0.5, 6.0, n_k)[None, :, None, None]
+    else:
+        k = k * torch.exp(torch.randn((n_k,), generator=g))[None, :, None, None]
+    v = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    th = W.rope_theta(d, 1e4)
+    q = W.rotate_half(q.to(torch.bfloat16), torch.tensor([n_k]), th)
+    k = W.rotate_half(k.to(torch.bfloat16), torch.arange(0, n_k), th)
+    win, widths = windows_for(d, 1e4, 2.0, None, n_ctx=n_k + 1)
+    note(f"decode large scores {pattern}")
+    o, lse = gpu_decode(q[:, 0].contiguous().to(DEV), k.to(DEV), v.to(DEV), n_k, win, scale=1.0)
+    o_ref, lse_ref, _ = oracle.attend(q, k, v, n_k, widths, scale=1.0)
+    o_abs, _, _ = oracle.attend(q, k, v.abs(), n_k, widths, scale=1.0)
+    compare_rounding_bound(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], o_abs[:, 0],
+                           f"large {pattern}")

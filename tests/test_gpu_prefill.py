@@ -14,7 +14,7 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare, family_windows_for, gpu_decode, gpu_prefill, note, pack_kcache,
+from parity import (compare_rounding_bound, compare, family_windows_for, gpu_decode, gpu_prefill, note, pack_kcache,
                     pack_vcache, sample_rows, to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
@@ -297,3 +297,37 @@ def test_prefill_cache_capacity_and_uninitialised_tail():
     o, lse = gpu_prefill(q.to(DEV), kc.to(DEV), vc.to(DEV), n_k - n_q, win, n_k=n_k)
     o_ref, lse_ref, _ = oracle.attend(q, k, v, n_k - n_q, widths)
     compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "capacity")
+
+
+def _large_score_inputs(n_q, n_k, q0, h_q, h_kv, d, base, pattern, seed):
+    """Scores of order 100s (scaled queries, keys whose magnitude grows along the
+    sequence or is log-normal), so the running max of the online softmax is raised
+    many times along each row and O and the normaliser are rescaled."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((1, n_q, h_q, d), generator=g) * 3.0
+    k = torch.randn((1, n_k, h_kv, d), generator=g)
+    if pattern == "rising":
+        k = k * torch.linspace(0.5, 6.0, n_k)[None, :, None, None]
+    else:
+        k = k * torch.exp(torch.randn((n_k,), generator=g))[None, :, None, None]
+    v = torch.randn((1, n_k, h_kv, d), generator=g)
+    th = W.rope_theta(d, base)
+    q = W.rotate_half(q.to(torch.bfloat16), torch.arange(q0, q0 + n_q), th)
+    k = W.rotate_half(k.to(torch.bfloat16), torch.arange(0, n_k), th)
+    return q, k, v.to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("pattern", ["rising", "lognormal"])
+@pytest.mark.parametrize("d,h_q,h_kv", [(128, 6, 2), (64, 7, 1)])
+def test_prefill_large_scores_rescale(pattern, d, h_q, h_kv):
+    """Every row against the oracle within the rounding bound of the arithmetic (see
+    compare_rounding_bound), windowed and with the window off."""
+    q, k, v = _large_score_inputs(700, 700, 0, h_q, h_kv, d, 1e4, pattern, seed=77 + d)
+    for kwin in (2.0, math.inf):
+        win, widths = windows_for(d, 1e4, kwin, None, n_ctx=700)
+        note(f"prefill large scores {pattern} d={d} k={kwin}")
+        o, lse = gpu_prefill(q.to(DEV), k.to(DEV), v.to(DEV), 0, win, 1.0)
+        o_ref, lse_ref, _ = oracle.attend(q, k, v, 0, widths, scale=1.0)
+        o_abs, _, _ = oracle.attend(q, k, v.abs(), 0, widths, scale=1.0)
+        compare_rounding_bound(to_f64(o), to_f64(lse), o_ref, lse_ref, o_abs,
+                               f"large scores {pattern} d={d} k={kwin}")
