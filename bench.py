@@ -288,12 +288,41 @@ def ragged_decode_config(atf, W, dev, stream):
     t = _median_ms(lambda: run(win), stream, 3, 30)
     nb = nbytes(win)
     gbs = nb / (t * 1e-3) / 1e9
-    del kp, vp, qd, od, lsed, ws
-    torch.cuda.empty_cache()
-    return {"llama3b_decode_ragged_b8": {
+    out = {"llama3b_decode_ragged_b8": {
         "ms": round(t, 4), "GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
         "algorithmic_bytes": nb, "rows": RAGGED_ROWS, "full_window_ms": round(t_off, 4),
         "speedup_vs_full_window": round(t_off / t, 4)}}
+    del kp, vp
+    torch.cuda.empty_cache()
+    # the same rows over paged caches: 128-token pages, each row's pages in shuffled
+    # order in one pool (atf_cache_append_paged fills them from the same inputs)
+    pt = 128
+    maxp = wl.n_k // pt
+    counts = [-(-n // pt) for n in RAGGED_ROWS]
+    perm = np.random.default_rng(20260099).permutation(sum(counts))
+    bt = np.full((B, maxp), -1, dtype=np.int32)
+    at = 0
+    for b, c in enumerate(counts):
+        bt[b, :c] = perm[at:at + c]
+        at += c
+    btd = torch.from_numpy(bt).to(dev)
+    kpool = torch.empty(atf.kpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
+    vpool = torch.empty(atf.vpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
+    inp = W.make_inputs(wl, device=dev)
+    atf.atf_cache_append_paged(inp["k"], inp["v"], kpool, vpool, btd, 0, stream=stream)
+    del inp
+    runp = lambda w: atf.atf_decode_paged(qd, kpool, vpool, od, lsed, btd, rows, rows, wl.n_k, w, ws,
+                                          stream=stream)
+    tp_off = _median_ms(lambda: runp(off), stream, 3, 30)
+    tp = _median_ms(lambda: runp(win), stream, 3, 30)
+    gbsp = nb / (tp * 1e-3) / 1e9
+    out["llama3b_decode_paged_b8"] = {
+        "ms": round(tp, 4), "GBps": round(gbsp, 1), "frac_hbm_peak": round(gbsp / PEAK_HBM_GBS, 4),
+        "algorithmic_bytes": nb, "rows": RAGGED_ROWS, "page_tokens": pt,
+        "full_window_ms": round(tp_off, 4), "speedup_vs_full_window": round(tp_off / tp, 4)}
+    del kpool, vpool, qd, od, lsed, ws, btd
+    torch.cuda.empty_cache()
+    return out
 
 
 # HBM bytes moved by one launch of a kernel at the benchmark workload, from two
@@ -305,14 +334,14 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "2875d0a02000ad90ce53d38e435918acc0baea4af9e8e9fc13409da41135d490",
+        "sha256": "fa4c21d422327fee7a9d939ead0aaf8462631f60b5a5bf670a17f02312c0ccae",
         "fetch_kib": 79575537.13, "write_kib": 933438.34,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "afc073f3a32a1e944a72518ee50517b02723d24eb92802f4ab6da26aa28f4791",
-        "fetch_kib": 737755.96, "write_kib": 4062.14,
+        "sha256": "1cda64e00cef0ac3fa98cad83e8886900b2bdb830099c0a880aaefd740251993",
+        "fetch_kib": 737770.17, "write_kib": 4062.38,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy

@@ -260,6 +260,51 @@ int atf_decode_ragged(const void *q, const void *k_cache, const void *v_cache, v
                       const atf_window *w, float softmax_scale, void *workspace,
                       size_t workspace_bytes, void *hip_stream);
 
+/* Paged caches: the K and V caches of all rows live in pools of pages of
+ * page_tokens tokens (a multiple of 32, the decode kernel's token block).  Page i of
+ * the pools holds
+ *   k_pages  bf16 [num_pages][h_kv][d/16][page_tokens][16]  pair-chunk-major within
+ *            the page (chunk c of a head is a contiguous stream over its tokens, as in
+ *            the contiguous K cache: a pruned chunk is never read)
+ *   v_pages  bf16 [num_pages][h_kv][page_tokens/16][d][16]   16-token blocks as in
+ *            the contiguous V cache (see atf_pack_vcache)
+ * Row b's token t lives in page block_table[b * max_pages_per_row + t / page_tokens],
+ * at token t % page_tokens of that page.  block_table: int32, DEVICE.  Pages may be
+ * shared between rows or unused; the library never allocates or frees them.
+ *
+ * Write n_new tokens of every row, at row positions pos0 .. pos0 + n_new - 1, into
+ * the pages the block table names for them.  Pure data movement (bit-exact).
+ *   k_new, v_new  bf16 [batch][n_new][h_kv][d]                   (device, read)
+ * Page entries outside [0, num_pages) are skipped (the caller's error; nothing is
+ * written outside the pools).  The slots of a page's 16-token V block that the call
+ * does not write keep their contents.  n_new == 0 is a no-op.
+ * Errors: ATF_EINVAL (NULL/misaligned pointer, batch < 1, h_kv < 1, n_new < 0, pos0 < 0,
+ * page_tokens not a positive multiple of 32, num_pages < 1, max_pages_per_row < 1,
+ * pos0 + n_new > max_pages_per_row * page_tokens), ATF_EUNSUPPORTED (d not 64/128),
+ * ATF_EHIP. */
+int atf_cache_append_paged(const void *k_new, const void *v_new, void *k_pages, void *v_pages,
+                           const int32_t *block_table, int32_t max_pages_per_row,
+                           int32_t num_pages, int32_t page_tokens, int32_t batch,
+                           int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
+                           void *hip_stream);
+
+/* Decode of a ragged batch over paged caches: atf_decode_ragged with row b's keys read
+ * through its block table (layouts above).  max_n_k bounds n_k_rows and must not
+ * exceed max_pages_per_row * page_tokens; the workspace is
+ * atf_decode_workspace_bytes(batch, h_q, h_kv, max_n_k, d).  The kernel clamps row
+ * lengths and positions as atf_decode_ragged does and page entries to
+ * [0, num_pages), so it never reads outside the pools whatever the arrays hold;
+ * such values are a caller error made harmless, not a supported input.
+ * Errors: as atf_decode_ragged, plus ATF_EINVAL for a NULL/misaligned block table,
+ * page_tokens not a positive multiple of 32, num_pages < 1, max_pages_per_row < 1,
+ * max_n_k > max_pages_per_row * page_tokens.  Deterministic. */
+int atf_decode_paged(const void *q, const void *k_pages, const void *v_pages, void *o, float *lse,
+                     int32_t batch, const int32_t *block_table, int32_t max_pages_per_row,
+                     int32_t num_pages, int32_t page_tokens, const int32_t *n_k_rows,
+                     const int32_t *q_pos_rows, int64_t max_n_k, int32_t h_q, int32_t h_kv,
+                     const atf_window *w, float softmax_scale, void *workspace,
+                     size_t workspace_bytes, void *hip_stream);
+
 /* Message of the most recent failed call on this thread ("" if none). */
 const char *atf_last_error(void);
 

@@ -16,6 +16,7 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_cache_append` -- write new tokens into both caches at a position.
 - :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
 - :func:`atf_decode_ragged` -- the same for a batch of sequences of different lengths.
+- :func:`atf_cache_append_paged`, :func:`atf_decode_paged` -- paged caches (block tables).
 """
 from __future__ import annotations
 
@@ -75,6 +76,10 @@ def _load():
                                       ctypes.c_size_t, P]),
         "atf_decode_ragged": (ctypes.c_int, [P, P, P, P, P, i32, P, P, i64, i32, i32, i64, W, f32,
                                              P, ctypes.c_size_t, P]),
+        "atf_cache_append_paged": (ctypes.c_int, [P, P, P, P, P, i32, i32, i32, i32, i64, i64,
+                                                  i32, i32, P]),
+        "atf_decode_paged": (ctypes.c_int, [P, P, P, P, P, i32, P, i32, i32, i32, P, P, i64, i32,
+                                            i32, W, f32, P, ctypes.c_size_t, P]),
         "atf_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -87,7 +92,8 @@ def _load():
 _lib = _load()
 EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
-            "atf_decode_workspace_bytes", "atf_decode", "atf_decode_ragged", "atf_last_error")
+            "atf_decode_workspace_bytes", "atf_decode", "atf_decode_ragged", "atf_cache_append_paged",
+            "atf_decode_paged", "atf_last_error")
 
 
 def library():
@@ -344,6 +350,68 @@ def atf_decode_ragged(q, k_pcm, v_pack, o, lse, n_k_rows, q_pos_rows, max_n_k: i
         _dev_ptr(v_pack, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
         _dev_ptr(lse, torch.float32, "lse"), B, _dev_ptr(n_k_rows, torch.int32, "n_k_rows"),
         _dev_ptr(q_pos_rows, torch.int32, "q_pos_rows"), int(max_n_k), h_q, h_kv, cap,
+        ctypes.byref(cw), float(softmax_scale), _dev_ptr(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _stream_ptr(stream))
+    _check(rc)
+
+
+def kpages_shape(num_pages: int, page_tokens: int, h_kv: int, head_dim: int):
+    """K page pool [num_pages, h_kv, d/16, page_tokens, 16] (pair-chunk-major pages)."""
+    return (num_pages, h_kv, head_dim // 16, page_tokens, 16)
+
+
+def vpages_shape(num_pages: int, page_tokens: int, h_kv: int, head_dim: int):
+    """V page pool [num_pages, h_kv, page_tokens/16, d, 16] (16-token blocks)."""
+    return (num_pages, h_kv, page_tokens // 16, head_dim, 16)
+
+
+def _pages(k_pages, v_pages, fn):
+    if k_pages.dim() != 5 or v_pages.dim() != 5:
+        raise ValueError(f"{fn}: page pools must be 5-d (see kpages_shape, vpages_shape)")
+    num_pages, h_kv, c16, pt, _ = k_pages.shape
+    d = 16 * c16
+    if tuple(k_pages.shape) != kpages_shape(num_pages, pt, h_kv, d) or \
+            tuple(v_pages.shape) != vpages_shape(num_pages, pt, h_kv, d):
+        raise ValueError(f"{fn}: inconsistent page pool shapes")
+    return num_pages, h_kv, pt, d
+
+
+def atf_cache_append_paged(k_new, v_new, k_pages, v_pages, block_table, pos0: int, stream=None):
+    """Write k_new, v_new [B, n_new, h_kv, d] at row positions pos0 .. into the pages
+    block_table [B, max_pages] (int32, device) names."""
+    torch = _torch()
+    num_pages, h_kv, pt, d = _pages(k_pages, v_pages, "atf_cache_append_paged")
+    B, n_new, hk, dd = k_new.shape
+    if tuple(v_new.shape) != tuple(k_new.shape) or hk != h_kv or dd != d or \
+            block_table.dim() != 2 or block_table.shape[0] != B:
+        raise ValueError("atf_cache_append_paged: inconsistent shapes")
+    rc = _lib.atf_cache_append_paged(
+        _dev_ptr(k_new, torch.bfloat16, "k_new"), _dev_ptr(v_new, torch.bfloat16, "v_new"),
+        _dev_ptr(k_pages, torch.bfloat16, "k_pages"), _dev_ptr(v_pages, torch.bfloat16, "v_pages"),
+        _dev_ptr(block_table, torch.int32, "block_table"), block_table.shape[1], num_pages, pt, B,
+        n_new, int(pos0), h_kv, d, _stream_ptr(stream))
+    _check(rc)
+
+
+def atf_decode_paged(q, k_pages, v_pages, o, lse, block_table, n_k_rows, q_pos_rows,
+                     max_n_k: int, window: Window, workspace, softmax_scale: float = 0.0,
+                     stream=None):
+    """atf_decode_ragged over paged caches: row b's keys are read through
+    block_table[b] (int32 [B, max_pages], device)."""
+    torch = _torch()
+    num_pages, h_kv, pt, d = _pages(k_pages, v_pages, "atf_decode_paged")
+    B, h_q, dq = q.shape
+    if dq != d or tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
+            block_table.dim() != 2 or block_table.shape[0] != B or \
+            tuple(n_k_rows.shape) != (B,) or tuple(q_pos_rows.shape) != (B,):
+        raise ValueError("atf_decode_paged: inconsistent shapes")
+    cw, keep = window.as_c()
+    rc = _lib.atf_decode_paged(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pages, torch.bfloat16, "k_pages"),
+        _dev_ptr(v_pages, torch.bfloat16, "v_pages"), _dev_ptr(o, torch.bfloat16, "o"),
+        _dev_ptr(lse, torch.float32, "lse"), B, _dev_ptr(block_table, torch.int32, "block_table"),
+        block_table.shape[1], num_pages, pt, _dev_ptr(n_k_rows, torch.int32, "n_k_rows"),
+        _dev_ptr(q_pos_rows, torch.int32, "q_pos_rows"), int(max_n_k), h_q, h_kv,
         ctypes.byref(cw), float(softmax_scale), _dev_ptr(workspace, torch.uint8, "workspace"),
         workspace.numel(), _stream_ptr(stream))
     _check(rc)

@@ -442,11 +442,16 @@ namespace {
 // Shared by atf_decode (every row has n_k keys and its query at q_pos) and
 // atf_decode_ragged (row b has n_k_rows[b] keys and its query at q_pos_rows[b],
 // device arrays; n_k is then their upper bound and q_pos is unused).
+struct PagedArgs {
+    const int32_t* block_table = nullptr;
+    int32_t max_pages = 0, num_pages = 0, page_tokens = 0;
+};
+
 int decode_impl(const char* fn, const void* q, const void* k_cache, const void* v_cache, void* o,
                 float* lse, int32_t batch, int64_t n_k, int64_t q_pos, const int32_t* n_k_rows,
                 const int32_t* q_pos_rows, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
                 const atf_window* w, float softmax_scale, void* workspace, size_t workspace_bytes,
-                void* hip_stream) {
+                void* hip_stream, const PagedArgs& pg = PagedArgs()) {
     const bool ragged = n_k_rows != nullptr || q_pos_rows != nullptr;
     if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
     const int d = w->head_dim;
@@ -476,6 +481,8 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
         return fail(ATF_EINVAL, "%s: q/k/v/o must be 16-byte and lse 4-byte aligned", fn);
     if (ragged && (!aligned(n_k_rows, 4) || !aligned(q_pos_rows, 4)))
         return fail(ATF_EINVAL, "%s: row arrays must be 4-byte aligned", fn);
+    if (pg.block_table != nullptr && !aligned(pg.block_table, 4))
+        return fail(ATF_EINVAL, "%s: block table must be 4-byte aligned", fn);
     const int32_t splits = atf::decode_splits(batch, h_kv, n_k, ragged);
     const WsLayout L = ws_layout(batch, h_q, splits, d);
     if (workspace == nullptr || workspace_bytes < L.total)
@@ -509,6 +516,10 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
     p.heads_per_block = hpb;
     p.n_k_rows = n_k_rows;
     p.q_pos_rows = q_pos_rows;
+    p.block_table = pg.block_table;
+    p.max_pages = pg.max_pages;
+    p.num_pages = pg.num_pages;
+    p.page_tokens = pg.page_tokens;
     // keys any row can reach: the split plan covers them (rows with fewer keys leave
     // their later splits empty)
     const int64_t last = ragged ? n_k - 1 : (q_pos < n_k - 1 ? q_pos : n_k - 1);
@@ -549,6 +560,78 @@ int atf_decode_ragged(const void* q, const void* k_cache, const void* v_cache, v
     return decode_impl("decode_ragged", q, k_cache, v_cache, o, lse, batch, max_n_k, 0, n_k_rows,
                        q_pos_rows, h_q, h_kv, cache_tokens, w, softmax_scale, workspace,
                        workspace_bytes, hip_stream);
+}
+
+int atf_decode_paged(const void* q, const void* k_pages, const void* v_pages, void* o, float* lse,
+                     int32_t batch, const int32_t* block_table, int32_t max_pages_per_row,
+                     int32_t num_pages, int32_t page_tokens, const int32_t* n_k_rows,
+                     const int32_t* q_pos_rows, int64_t max_n_k, int32_t h_q, int32_t h_kv,
+                     const atf_window* w, float softmax_scale, void* workspace,
+                     size_t workspace_bytes, void* hip_stream) {
+    if (!block_table) return fail(ATF_EINVAL, "decode_paged: NULL block table");
+    if (!n_k_rows || !q_pos_rows)
+        return fail(ATF_EINVAL, "decode_paged: NULL row-length or row-position array");
+    if (page_tokens < 32 || page_tokens % 32 != 0)
+        return fail(ATF_EINVAL, "decode_paged: page_tokens %d must be a positive multiple of 32",
+                    page_tokens);
+    if (num_pages < 1 || max_pages_per_row < 1)
+        return fail(ATF_EINVAL, "decode_paged: need num_pages >= 1 and max_pages_per_row >= 1");
+    const int64_t row_cap = int64_t(max_pages_per_row) * page_tokens;
+    if (max_n_k > row_cap || row_cap > kPosLimit)
+        return fail(ATF_EINVAL, "decode_paged: max_n_k %lld exceeds the %lld tokens a row's pages "
+                    "hold (or that exceeds 2^31 - 1)", (long long)max_n_k, (long long)row_cap);
+    PagedArgs pg;
+    pg.block_table = block_table;
+    pg.max_pages = max_pages_per_row;
+    pg.num_pages = num_pages;
+    pg.page_tokens = page_tokens;
+    // the contiguous-cache capacity is the rows' span; the kernel addresses pages instead
+    return decode_impl("decode_paged", q, k_pages, v_pages, o, lse, batch, max_n_k, 0, n_k_rows,
+                       q_pos_rows, h_q, h_kv, row_cap, w, softmax_scale, workspace,
+                       workspace_bytes, hip_stream, pg);
+}
+
+int atf_cache_append_paged(const void* k_new, const void* v_new, void* k_pages, void* v_pages,
+                           const int32_t* block_table, int32_t max_pages_per_row,
+                           int32_t num_pages, int32_t page_tokens, int32_t batch, int64_t n_new,
+                           int64_t pos0, int32_t h_kv, int32_t head_dim, void* hip_stream) {
+    if (head_dim != 64 && head_dim != 128)
+        return fail(ATF_EUNSUPPORTED, "cache_append_paged: head_dim %d not built", head_dim);
+    if (batch < 1 || h_kv < 1 || n_new < 0 || pos0 < 0)
+        return fail(ATF_EINVAL, "cache_append_paged: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0");
+    if (page_tokens < 32 || page_tokens % 32 != 0)
+        return fail(ATF_EINVAL, "cache_append_paged: page_tokens %d must be a positive multiple of 32",
+                    page_tokens);
+    if (num_pages < 1 || max_pages_per_row < 1)
+        return fail(ATF_EINVAL, "cache_append_paged: need num_pages >= 1 and max_pages_per_row >= 1");
+    const int64_t row_cap = int64_t(max_pages_per_row) * page_tokens;
+    if (row_cap > kPosLimit || pos0 + n_new > row_cap)
+        return fail(ATF_EINVAL, "cache_append_paged: tokens %lld .. %lld do not fit the %lld tokens "
+                    "of a row's pages", (long long)pos0, (long long)(pos0 + n_new), (long long)row_cap);
+    if (!k_new || !v_new || !k_pages || !v_pages || !block_table)
+        return fail(ATF_EINVAL, "cache_append_paged: NULL pointer");
+    if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pages, 16) ||
+        !aligned(v_pages, 16) || !aligned(block_table, 4))
+        return fail(ATF_EINVAL, "cache_append_paged: tensors must be 16-byte, the table 4-byte aligned");
+    if (n_new == 0) return ATF_OK;
+    if (int64_t(batch) * n_new * h_kv > kPosLimit)
+        return fail(ATF_EINVAL, "cache_append_paged: too many tokens for one call");
+    atf::AppendPagedParams p{};
+    p.k_src = static_cast<const uint16_t*>(k_new);
+    p.v_src = static_cast<const uint16_t*>(v_new);
+    p.k_pages = static_cast<uint16_t*>(k_pages);
+    p.v_pages = static_cast<uint16_t*>(v_pages);
+    p.block_table = block_table;
+    p.batch = batch;
+    p.n_new = static_cast<int32_t>(n_new);
+    p.pos0 = static_cast<int32_t>(pos0);
+    p.h_kv = h_kv;
+    p.max_pages = max_pages_per_row;
+    p.num_pages = num_pages;
+    p.page_tokens = page_tokens;
+    hipError_t e = atf::launch_append_paged(p, head_dim, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "cache_append_paged: launch failed: %s", hipGetErrorString(e));
+    return ATF_OK;
 }
 
 }  // extern "C"

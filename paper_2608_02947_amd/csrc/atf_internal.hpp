@@ -53,10 +53,23 @@ struct DecodeParams {
                               // [0, n_k]), or nullptr: every row has n_k keys
     const int32_t* q_pos_rows;  // ragged batch: device [B] query position of each row
                                 // (clamped to [0, 2^31 - 2]), or nullptr: q_pos
+    const int32_t* block_table;  // paged caches: device [B][max_pages] page of each row's
+                                 // page_tokens-token span (clamped to [0, num_pages)),
+                                 // or nullptr: contiguous caches
+    int32_t max_pages, num_pages, page_tokens;
     int32_t splits;
     int32_t split_tokens;     // tokens per split (multiple of the workgroup's token step)
     float scale_log2;
     WindowTable win;
+};
+
+struct AppendPagedParams {
+    const uint16_t* k_src;     // [B][n_new][h_kv][d]: tokens pos0 .. pos0 + n_new - 1
+    const uint16_t* v_src;
+    uint16_t* k_pages;         // [num_pages][h_kv][d/16][page_tokens][16]
+    uint16_t* v_pages;         // [num_pages][h_kv][page_tokens/16][d][16]
+    const int32_t* block_table;  // [B][max_pages]
+    int32_t batch, n_new, pos0, h_kv, max_pages, num_pages, page_tokens;
 };
 
 struct PackParams {
@@ -74,6 +87,7 @@ hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stre
 hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan: number of KV splits per (batch, kv head) for these sizes.
 int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k, bool ragged);

@@ -125,6 +125,21 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 
     for (int t0 = t_begin + 32 * wave; t0 < t_end; t0 += 32 * kWaves) {
         const int t_last = min(t0 + 31, t_end - 1);
+        // where the block's 32 tokens live: the row's contiguous cache, or the page the
+        // block table names (a page holds a whole number of 32-token blocks)
+        const uint16_t* kb = kstream;   // chunk c of token t at kb + (c * kstride + t - tb) * 16
+        const uint16_t* vb = vblocks;   // 16-token block j at vb + (j - tb / 16) * D * 16
+        int64_t kstride = cap;
+        int tb = 0;
+        if (p.block_table != nullptr) {
+            const int pt = p.page_tokens;
+            const int page = min(max(p.block_table[int64_t(b) * p.max_pages + t0 / pt], 0),
+                                 p.num_pages - 1);
+            kb = p.kpcm + (int64_t(page) * p.h_kv + g) * kChunks * int64_t(pt) * 16;
+            vb = p.vpk + (int64_t(page) * p.h_kv + g) * (pt / 16) * int64_t(D) * 16;
+            kstride = pt;
+            tb = t0 - t0 % pt;
+        }
         const int zhi = q_pos - t0;
         const int zlo = max(0, q_pos - t_last);
         const uint64_t full = __ballot(my_w >= zhi);
@@ -140,7 +155,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             u32x4_t z = {0u, 0u, 0u, 0u};
             const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
             if (kept && tok_ok)
-                z = *reinterpret_cast<const u32x4_t*>(kstream + (int64_t(c) * cap + tok) * 16 + 8 * hh);
+                z = *reinterpret_cast<const u32x4_t*>(kb + (int64_t(c) * kstride + tok - tb) * 16 + 8 * hh);
             kf[c] = z;
         }
         // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each
@@ -155,7 +170,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             for (int i = 0; i < kDB; ++i) {
                 u32x4_t z = {0u, 0u, 0u, 0u};
                 if (16 * blk < n_k)
-                    z = *reinterpret_cast<const u32x4_t*>(vblocks + (int64_t(blk) * D + 32 * i + col) * 16 + 8 * hh);
+                    z = *reinterpret_cast<const u32x4_t*>(vb + (int64_t(blk - tb / 16) * D + 32 * i + col) * 16 + 8 * hh);
                 vf[ks][i] = z;
             }
             if (16 * blk < n_k && 16 * blk + 16 > n_k) {
@@ -409,6 +424,43 @@ __global__ __launch_bounds__(256) void pack_vcache_kernel(const PackParams p) {
     }
 }
 
+// Paged append: one thread per (batch, new token, kv head, 8-dim piece); K pieces
+// go to the token's chunk stream in its page, V elements to the slots of the
+// token's 16-token block in its page (slot 8h + e holds token 8(e/4) + 4h + e%4).
+template <int D>
+__global__ __launch_bounds__(256) void append_paged_kernel(const AppendPagedParams p) {
+    constexpr int kChunks = D / 16;
+    constexpr int kPieces = D / 8;  // 8-dim pieces of one (token, head) row
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const int64_t total = int64_t(p.batch) * p.n_new * p.h_kv * kPieces;
+    for (int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x; idx < total;
+         idx += int64_t(gridDim.x) * 256) {
+        const int pc = int(idx % kPieces);
+        int64_t r = idx / kPieces;
+        const int g = int(r % p.h_kv);
+        r /= p.h_kv;
+        const int t = int(r % p.n_new);
+        const int b = int(r / p.n_new);
+        const int pos = p.pos0 + t;
+        const int page = p.block_table[int64_t(b) * p.max_pages + pos / p.page_tokens];
+        if (page < 0 || page >= p.num_pages) continue;
+        const int slot = pos % p.page_tokens;
+        const int64_t src = ((int64_t(b) * p.n_new + t) * p.h_kv + g) * D + 8 * pc;
+        // K: piece pc = dims [8 pc, 8 pc + 8) is half (pc >= kChunks) of chunk pc % kChunks
+        const int c = pc % kChunks, half = pc / kChunks;
+        uint16_t* kd = p.k_pages + (((int64_t(page) * p.h_kv + g) * kChunks + c) * p.page_tokens +
+                                    slot) * 16 + 8 * half;
+        *reinterpret_cast<u32x4*>(kd) = *reinterpret_cast<const u32x4*>(p.k_src + src);
+        // V: dims 8 pc .. 8 pc + 7 of this token, one slot each
+        const int e16 = slot % 16;  // token within its 16-token block
+        const int h = (e16 % 8) / 4, e = (e16 / 8) * 4 + e16 % 4;  // slot 8h + e
+        uint16_t* vd = p.v_pages + ((int64_t(page) * p.h_kv + g) * (p.page_tokens / 16) + slot / 16) *
+                                       int64_t(D) * 16 + 8 * h + e;
+#pragma unroll
+        for (int x = 0; x < 8; ++x) vd[int64_t(8 * pc + x) * 16] = p.v_src[src + x];
+    }
+}
+
 template <int D>
 hipError_t launch_decode_d(const DecodeParams& p, hipStream_t stream) {
     const dim3 grid(unsigned(p.splits), unsigned(p.h_kv * (p.group / p.heads_per_block)),
@@ -446,6 +498,16 @@ hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t str
         hipLaunchKernelGGL(pack_kcache_kernel<64>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
     else
         hipLaunchKernelGGL(pack_kcache_kernel<128>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream) {
+    const int64_t total = int64_t(p.batch) * p.n_new * p.h_kv * (head_dim / 8);
+    (void)hipGetLastError();
+    if (head_dim == 64)
+        hipLaunchKernelGGL(append_paged_kernel<64>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL(append_paged_kernel<128>, dim3(pack_blocks(total)), dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

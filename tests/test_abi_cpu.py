@@ -334,6 +334,51 @@ def test_decode_ragged_validation_before_launch():
     assert "decode_ragged" in atf.atf_last_error()
 
 
+def test_paged_validation_before_launch():
+    """Every call below fails validation, so nothing is launched (the pointers are
+    placeholders)."""
+    lib = atf.library()
+
+    def app(**kw):
+        a = dict(k=16, v=16, kp=1 << 20, vp=1 << 21, bt=1 << 12, max_pages=4, num_pages=8, pt=64,
+                 batch=2, n_new=10, pos0=0, h_kv=2, d=128)
+        a.update(kw)
+        return lib.atf_cache_append_paged(a["k"], a["v"], a["kp"], a["vp"], a["bt"], a["max_pages"],
+                                          a["num_pages"], a["pt"], a["batch"], a["n_new"],
+                                          a["pos0"], a["h_kv"], a["d"], None)
+    assert app(pt=48) == atf.ATF_EINVAL
+    assert app(pt=0) == atf.ATF_EINVAL
+    assert app(num_pages=0) == atf.ATF_EINVAL
+    assert app(max_pages=0) == atf.ATF_EINVAL
+    assert app(pos0=250) == atf.ATF_EINVAL          # 250 + 10 > 4 pages of 64
+    assert app(bt=None) == atf.ATF_EINVAL
+    assert app(bt=(1 << 12) + 2) == atf.ATF_EINVAL  # int32 table, 4-byte aligned
+    assert app(k=24) == atf.ATF_EINVAL              # 16-byte alignment
+    assert app(d=80) == atf.ATF_EUNSUPPORTED
+    assert app(n_new=-1) == atf.ATF_EINVAL
+    assert app(n_new=0) == atf.ATF_OK               # no-op: nothing launched
+
+    need = atf.atf_decode_workspace_bytes(2, 24, 8, 256, 128)
+    assert need > 0
+
+    def dec(ws=16, ws_bytes=16, **kw):
+        a = dict(bt=1 << 12, max_pages=4, num_pages=8, pt=64, max_n_k=256, nk=1 << 13, qp=1 << 14)
+        a.update(kw)
+        w, kp = atf.Window(128, 5e5, 2.0).as_c()
+        return lib.atf_decode_paged(16, 16, 16, 16, 16, 2, a["bt"], a["max_pages"], a["num_pages"],
+                                    a["pt"], a["nk"], a["qp"], a["max_n_k"], 24, 8, ctypes.byref(w),
+                                    0.0, ws, ws_bytes, None)
+    assert dec() == atf.ATF_EWORKSPACE              # everything else valid
+    assert dec(bt=None) == atf.ATF_EINVAL
+    assert dec(bt=(1 << 12) + 1) == atf.ATF_EINVAL
+    assert dec(nk=None) == atf.ATF_EINVAL
+    assert dec(pt=40) == atf.ATF_EINVAL
+    assert dec(num_pages=0) == atf.ATF_EINVAL
+    assert dec(max_n_k=257) == atf.ATF_EINVAL       # more than 4 pages of 64 tokens
+    assert dec(max_n_k=0) == atf.ATF_EINVAL
+    assert "decode_paged" in atf.atf_last_error()
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

@@ -385,3 +385,132 @@ def test_decode_large_scores_rescale(pattern):
     o_abs, _, _ = oracle.attend(q, k, v.abs(), n_k, widths, scale=1.0)
     compare_rounding_bound(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], o_abs[:, 0],
                            f"large {pattern}")
+
+
+# ---------------------------------------------------------------------------
+# paged caches: page pools + block tables
+# ---------------------------------------------------------------------------
+def _block_tables(n_rows, pages_per_row, num_pages, seed, share_prefix=0):
+    """Distinct pages per row from a shuffled pool; with share_prefix > 0 every row
+    reuses row 0's first share_prefix pages (a shared prompt prefix)."""
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(num_pages)
+    bt = np.full((n_rows, pages_per_row), -1, dtype=np.int32)
+    nxt = 0
+    for b in range(n_rows):
+        for j in range(pages_per_row):
+            if b > 0 and j < share_prefix:
+                bt[b, j] = bt[0, j]
+            else:
+                bt[b, j] = perm[nxt]
+                nxt += 1
+    assert nxt <= num_pages
+    return bt
+
+
+def _ref_pages(k_bshd, v_bshd, bt, num_pages, pt):
+    """Reference page pools from the contiguous reference layouts: page bt[b, j] holds
+    row b's tokens j*pt .. j*pt + pt - 1 (rows written in order, later rows win on
+    shared pages)."""
+    B, n, h_kv, d = k_bshd.shape
+    kref = _ref_pack(k_bshd)          # [B, h_kv, d/16, n, 16]
+    vref = _ref_vpack(v_bshd)         # [B, h_kv, n/16, d, 16]
+    kp = torch.zeros((num_pages, h_kv, d // 16, pt, 16), dtype=torch.bfloat16, device=k_bshd.device)
+    vp = torch.zeros((num_pages, h_kv, pt // 16, d, 16), dtype=torch.bfloat16, device=k_bshd.device)
+    for b in range(B):
+        for j in range(n // pt):
+            kp[bt[b, j]] = kref[b, :, :, j * pt:(j + 1) * pt]
+            vp[bt[b, j]] = vref[b, :, j * pt // 16:(j + 1) * pt // 16]
+    return kp, vp
+
+
+@pytest.mark.parametrize("pt,d", [(32, 64), (64, 128), (128, 128)])
+def test_cache_append_paged_bit_exact(pt, d):
+    """Pools written by atf_cache_append_paged in three appends (ragged cuts inside
+    pages and 16-token blocks) equal the reference pages bit for bit."""
+    import paper_2608_02947_amd as atf
+    B, h_kv, pages = 3, 2, 5
+    n = pages * pt
+    num_pages = B * pages + 3
+    bt = _block_tables(B, pages, num_pages, seed=pt + d)
+    k = W.random_bf16((B, n, h_kv, d), seed=d).to(DEV)
+    v = W.random_bf16((B, n, h_kv, d), seed=d + 1).to(DEV)
+    note(f"append paged pt={pt} d={d}")
+    kpool = torch.zeros(atf.kpages_shape(num_pages, pt, h_kv, d), dtype=torch.bfloat16, device=DEV)
+    vpool = torch.zeros(atf.vpages_shape(num_pages, pt, h_kv, d), dtype=torch.bfloat16, device=DEV)
+    btd = torch.from_numpy(bt).to(DEV)
+    cuts = [0, 7, pt + 21, n]
+    for a, c in zip(cuts[:-1], cuts[1:]):
+        atf.atf_cache_append_paged(k[:, a:c].contiguous(), v[:, a:c].contiguous(), kpool, vpool,
+                                   btd, a)
+    torch.cuda.synchronize()
+    kref, vref = _ref_pages(k, v, bt, num_pages, pt)
+    assert torch.equal(kpool.view(torch.int16), kref.view(torch.int16))
+    assert torch.equal(vpool.view(torch.int16), vref.view(torch.int16))
+
+
+def _paged_setup(n_ks, q_poss, pt, h_q, h_kv, d, base, seed, share_prefix=0):
+    import paper_2608_02947_amd as atf
+    B = len(n_ks)
+    pages = max(1, -(-max(max(n_ks), 1) // pt))
+    cap = pages * pt
+    q, kc, vc = _ragged_inputs(n_ks, q_poss, cap, h_q, h_kv, d, base, seed, fill=0.0)
+    if share_prefix:
+        kc[1:, :share_prefix * pt] = kc[:1, :share_prefix * pt]
+        vc[1:, :share_prefix * pt] = vc[:1, :share_prefix * pt]
+    num_pages = B * pages + 2
+    bt = _block_tables(B, pages, num_pages, seed, share_prefix)
+    kpool = torch.full(atf.kpages_shape(num_pages, pt, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                       device=DEV)
+    vpool = torch.full(atf.vpages_shape(num_pages, pt, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                       device=DEV)
+    btd = torch.from_numpy(bt).to(DEV)
+    atf.atf_cache_append_paged(kc.to(DEV), vc.to(DEV), kpool, vpool, btd, 0)
+    return q, kc, vc, kpool, vpool, btd, cap
+
+
+def _gpu_decode_paged(q, kpool, vpool, btd, n_ks, q_poss, max_n_k, win):
+    import paper_2608_02947_amd as atf
+    B, h_q, d = q.shape
+    h_kv = kpool.shape[1]
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, max_n_k, d), dtype=torch.uint8,
+                     device=DEV)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, h_q), dtype=torch.float32, device=DEV)
+    atf.atf_decode_paged(q, kpool, vpool, o, lse, btd, torch.tensor(n_ks, dtype=torch.int32, device=DEV),
+                         torch.tensor(q_poss, dtype=torch.int32, device=DEV), max_n_k, win, ws)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+PAGED_CASES = [
+    # n_k per row, q_pos per row, page tokens, h_q, h_kv, d, base, k, shared prefix pages
+    ([1000, 1, 333, 0, 700], [1000, 1, 333, 0, 700], 64, 7, 1, 128, 1e4, 2.0, 0),
+    ([2049, 100, 1500], [3000, 100, 900], 128, 8, 2, 64, 1e6, 2.0, 0),
+    ([4096, 4000, 2300], [4096, 4000, 2300], 32, 6, 2, 128, 5e5, 2.0, 0),
+    ([1500, 1700, 1300], [1500, 1700, 1300], 64, 12, 4, 128, 1e4, 2.0, 16),   # shared prefix
+    ([999, 640], [999, 640], 128, 3, 1, 128, 1e4, math.inf, 0),                 # window off
+]
+
+
+@pytest.mark.parametrize("case", PAGED_CASES, ids=lambda c: f"B{len(c[0])}_pt{c[2]}_d{c[5]}_share{c[8]}")
+def test_decode_paged_rows(case):
+    n_ks, q_poss, pt, h_q, h_kv, d, base, kwin, share = case
+    note(f"decode paged n_k={n_ks} q_pos={q_poss} pt={pt} d={d} share={share}")
+    q, kc, vc, kpool, vpool, btd, cap = _paged_setup(n_ks, q_poss, pt, h_q, h_kv, d, base,
+                                                     seed=sum(n_ks) % 997, share_prefix=share)
+    win, _ = windows_for(d, base, kwin, None, n_ctx=max(q_poss) + 1)
+    max_n_k = max(max(n_ks), 1)
+    qd = q[:, 0].contiguous().to(DEV)
+    o, lse = _gpu_decode_paged(qd, kpool, vpool, btd, n_ks, q_poss, max_n_k, win)
+    # the same batch over contiguous caches takes the same plan and arithmetic
+    o_c, lse_c = _gpu_decode_ragged(qd, kc.to(DEV), vc.to(DEV), n_ks, q_poss, max_n_k, win)
+    assert torch.equal(o, o_c) and torch.equal(lse, lse_c)
+    o, lse = to_f64(o), to_f64(lse)
+    for b, (nk, qp) in enumerate(zip(n_ks, q_poss)):
+        if nk == 0:
+            assert np.all(o[b] == 0.0) and np.all(lse[b] == -np.inf)
+            continue
+        _, widths = windows_for(d, base, kwin, None, n_ctx=qp + 1)
+        o_ref, lse_ref, _ = oracle.attend(q[b:b + 1], kc[b:b + 1, :nk], vc[b:b + 1, :nk], qp, widths)
+        compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"paged row {b}")
