@@ -260,9 +260,11 @@ int atf_decode_ragged(const void *q, const void *k_cache, const void *v_cache, v
                       const atf_window *w, float softmax_scale, void *workspace,
                       size_t workspace_bytes, void *hip_stream);
 
-/* Paged caches: the K and V caches of all rows live in pools of pages of
- * page_tokens tokens (a multiple of 32, the decode kernel's token block).  Page i of
- * the pools holds
+/* Paged caches (a serving layout the paper does not use: its decode reads one
+ * contiguous cache per request, Sec. 5; the window applies per 32-token block of a
+ * page exactly as in atf_decode): the K and V caches of all rows live in pools of
+ * pages of page_tokens tokens (a multiple of 32, the decode kernel's token block).
+ * Page i of the pools holds
  *   k_pages  bf16 [num_pages][h_kv][d/16][page_tokens][16]  pair-chunk-major within
  *            the page (chunk c of a head is a contiguous stream over its tokens, as in
  *            the contiguous K cache: a pruned chunk is never read)
