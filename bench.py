@@ -61,10 +61,12 @@ def parse():
                          "workloads.WORKLOADS) --profile-iters times and print its timings")
     ap.add_argument("--profile-iters", type=int, default=3)
     ap.add_argument("--profile-kinf", action="store_true", help="profiling driver at k = +inf")
+    ap.add_argument("--profile-raw-base", action="store_true",
+                    help="profiling driver: window table from the raw RoPE base (Llama shapes)")
     return ap.parse_args()
 
 
-def profile_driver(name, iters, kinf):
+def profile_driver(name, iters, kinf, raw_base=False):
     """Run one workload's prefill or decode `iters` times (for rocprofv3 runs)."""
     import paper_2608_02947_amd as atf
     import workloads as W
@@ -73,7 +75,7 @@ def profile_driver(name, iters, kinf):
     inp = W.make_inputs(wl, device=dev)
     th = W.workload_theta(wl)
     win = atf.Window(wl.head_dim, wl.rope_base, math.inf if kinf else wl.k,
-                     None if th is None else th.numpy())
+                     None if th is None or raw_base else th.numpy())
     stream = torch.cuda.current_stream()
     d = wl.head_dim
     if wl.kind == "prefill":
@@ -374,7 +376,8 @@ def main():
         copy_calibration()
         return
     if args.profile_workload:
-        profile_driver(args.profile_workload, args.profile_iters, args.profile_kinf)
+        profile_driver(args.profile_workload, args.profile_iters, args.profile_kinf,
+                       args.profile_raw_base)
         return
 
     import paper_2608_02947_amd as atf
