@@ -241,7 +241,10 @@ int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o,
  * against keys 0 .. min(q_pos_rows[b], n_k_rows[b] - 1) of its own cache entry
  * (Sec. 5: the last query row of each sequence, for a batch of sequences of
  * different lengths).  Everything else is atf_decode: same layouts, window,
- * split-KV plan and merge, with n_k replaced by max_n_k for the plan.
+ * split-KV partial states and merge.  The split plan follows the rows' lengths
+ * on the device: the batch's causal keys are cut into spans of equal length (a
+ * multiple of 128 tokens, about 2048 workgroups in all), each row into whole
+ * spans of its own keys, so a short row takes few workgroups and a long one many.
  *   n_k_rows    int32 [batch], DEVICE, 4-byte aligned: keys of each row's cache
  *   q_pos_rows  int32 [batch], DEVICE, 4-byte aligned: query position of each row
  *   max_n_k     host bound on n_k_rows (1 .. cache_tokens); the workspace is

@@ -167,17 +167,26 @@ u128 pair_count(int64_t W, int64_t p0, int64_t p1, int64_t n_k) {
 
 namespace atf {
 
-int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k, bool ragged) {
+int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k) {
     // enough workgroups to fill 256 CUs several times over, but never a split
-    // shorter than one workgroup step.  A ragged batch plans for its longest row
-    // and leaves the splits of shorter rows past their keys empty, so it takes four
-    // times as many (shorter) splits to keep the CUs busy (measured on a batch of 8
-    // rows of 4K .. 128K keys: 10 % faster; the same on a uniform 1M row: 14 % slower)
-    const int64_t target_groups = ragged ? 4096 : 1024;
+    // shorter than one workgroup step
+    const int64_t target_groups = 1024;
     int64_t s = (target_groups + int64_t(batch) * h_kv - 1) / (int64_t(batch) * h_kv);
     const int64_t max_s = (n_k + kDecodeTokenStep - 1) / kDecodeTokenStep;
     if (s > max_s) s = max_s;
     if (s > kDecodeMaxSplits) s = kDecodeMaxSplits;
+    if (s < 1) s = 1;
+    return static_cast<int32_t>(s);
+}
+
+int32_t decode_ragged_items(int32_t cols) {
+    // the batch's keys are cut into about this many equal spans per column, whatever
+    // the row lengths (measured on batches of 8 rows at d = 128 with 8 KV heads:
+    // 2048 workgroups beat 1024 by 5-12 % and 4096 by 0-20 %, on rows of 4K-128K keys,
+    // of 128K keys, and of one 128K row beside seven 1K rows)
+    const int64_t target_groups = 2048;
+    int64_t s = (target_groups + cols - 1) / cols;
+    if (s > kDecodeMaxSplits - 1) s = kDecodeMaxSplits - 1;
     if (s < 1) s = 1;
     return static_cast<int32_t>(s);
 }
@@ -412,17 +421,37 @@ namespace {
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 struct WsLayout {
-    size_t off_m, off_l, off_o, total;
+    size_t off_plan, off_m, off_l, off_o, total;
 };
 
-WsLayout ws_layout(int32_t batch, int32_t h_q, int32_t splits, int32_t head_dim) {
-    const size_t n = size_t(batch) * size_t(h_q) * size_t(splits);
+// Partial states of `slots` (split or work item) x h_q heads, after `plan_ints` int32.
+WsLayout ws_layout(size_t slots, int32_t h_q, int32_t head_dim, size_t plan_ints) {
+    const size_t n = slots * size_t(h_q);
     WsLayout L;
-    L.off_m = 0;
-    L.off_l = align_up(n * 4, 256);
+    L.off_plan = 0;
+    L.off_m = align_up(plan_ints * 4, 256);
+    L.off_l = L.off_m + align_up(n * 4, 256);
     L.off_o = L.off_l + align_up(n * 4, 256);
     L.total = L.off_o + align_up(n * size_t(head_dim) * 4, 256);
     return L;
+}
+
+// query heads per decode workgroup: the largest divisor of the group up to 32
+int32_t decode_heads_per_block(int32_t group) {
+    for (int32_t c = atf::kDecodeMaxHeads; c >= 1; --c)
+        if (group % c == 0) return c;
+    return 1;
+}
+
+WsLayout uniform_layout(int32_t batch, int32_t h_q, int32_t h_kv, int64_t n_k, int32_t head_dim) {
+    return ws_layout(size_t(batch) * size_t(atf::decode_splits(batch, h_kv, n_k)), h_q, head_dim, 0);
+}
+
+// ragged batch: at most items + batch work items (each row rounds its count up once)
+WsLayout ragged_layout(int32_t batch, int32_t h_q, int32_t h_kv, int32_t head_dim) {
+    const int32_t cols = h_kv * (h_q / h_kv / decode_heads_per_block(h_q / h_kv));
+    const size_t items = size_t(atf::decode_ragged_items(cols)) + size_t(batch);
+    return ws_layout(items, h_q, head_dim, size_t(batch) + 1);
 }
 }  // namespace
 
@@ -431,8 +460,10 @@ size_t atf_decode_workspace_bytes(int32_t batch, int32_t h_q, int32_t h_kv, int6
     if (batch < 1 || h_q < 1 || h_kv < 1 || h_q % h_kv || n_k < 1 || n_k > kPosLimit ||
         (head_dim != 64 && head_dim != 128))
         return 0;
-    const int32_t s = atf::decode_splits(batch, h_kv, n_k, true);  // covers both plans
-    return ws_layout(batch, h_q, s, head_dim).total;
+    // covers both plans: uniform (atf_decode) and ragged (atf_decode_ragged / _paged)
+    const size_t u = uniform_layout(batch, h_q, h_kv, n_k, head_dim).total;
+    const size_t r = ragged_layout(batch, h_q, h_kv, head_dim).total;
+    return u > r ? u : r;
 }
 
 }  // extern "C"
@@ -483,26 +514,22 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
         return fail(ATF_EINVAL, "%s: row arrays must be 4-byte aligned", fn);
     if (pg.block_table != nullptr && !aligned(pg.block_table, 4))
         return fail(ATF_EINVAL, "%s: block table must be 4-byte aligned", fn);
-    const int32_t splits = atf::decode_splits(batch, h_kv, n_k, ragged);
-    const WsLayout L = ws_layout(batch, h_q, splits, d);
+    const WsLayout L = ragged ? ragged_layout(batch, h_q, h_kv, d)
+                              : uniform_layout(batch, h_q, h_kv, n_k, d);
     if (workspace == nullptr || workspace_bytes < L.total)
         return fail(ATF_EWORKSPACE, "%s: workspace of %zu bytes needed, %zu given", fn, L.total,
                     workspace == nullptr ? size_t(0) : workspace_bytes);
     if (!aligned(workspace, 16)) return fail(ATF_EINVAL, "%s: workspace must be 16-byte aligned", fn);
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
     const int32_t group = h_q / h_kv;
-    int32_t hpb = 1;
-    for (int32_t c = atf::kDecodeMaxHeads; c >= 1; --c)
-        if (group % c == 0) {
-            hpb = c;
-            break;
-        }
+    const int32_t hpb = decode_heads_per_block(group);
     char* ws = static_cast<char*>(workspace);
     p.q = static_cast<const uint16_t*>(q);
     p.kpcm = static_cast<const uint16_t*>(k_cache);
     p.vpk = static_cast<const uint16_t*>(v_cache);
     p.o = static_cast<uint16_t*>(o);
     p.lse = lse;
+    p.ws_plan = ragged ? reinterpret_cast<int32_t*>(ws + L.off_plan) : nullptr;
     p.ws_m = reinterpret_cast<float*>(ws + L.off_m);
     p.ws_l = reinterpret_cast<float*>(ws + L.off_l);
     p.ws_o = reinterpret_cast<float*>(ws + L.off_o);
@@ -520,17 +547,25 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
     p.max_pages = pg.max_pages;
     p.num_pages = pg.num_pages;
     p.page_tokens = pg.page_tokens;
-    // keys any row can reach: the split plan covers them (rows with fewer keys leave
-    // their later splits empty)
-    const int64_t last = ragged ? n_k - 1 : (q_pos < n_k - 1 ? q_pos : n_k - 1);
-    p.n_valid = static_cast<int32_t>(last + 1);
-    p.splits = splits;
-    const int64_t per = (p.n_valid + splits - 1) / splits;
-    const int64_t step_tokens = (per + atf::kDecodeTokenStep - 1) / atf::kDecodeTokenStep *
-                                atf::kDecodeTokenStep;
-    if (step_tokens * splits >= kPosLimit)
-        return fail(ATF_EINVAL, "%s: cache too long for the split plan", fn);
-    p.split_tokens = static_cast<int32_t>(step_tokens);
+    if (ragged) {
+        // the work items are laid out on the device from the row arrays: the batch's
+        // keys in about `splits` equal spans (multiples of the workgroup's token step)
+        // per column, each row cut into whole spans of its own keys
+        p.n_valid = static_cast<int32_t>(n_k);
+        p.splits = atf::decode_ragged_items(h_kv * (group / hpb));
+        p.split_tokens = 0;
+    } else {
+        const int64_t last = q_pos < n_k - 1 ? q_pos : n_k - 1;
+        p.n_valid = static_cast<int32_t>(last + 1);
+        const int32_t splits = atf::decode_splits(batch, h_kv, n_k);
+        p.splits = splits;
+        const int64_t per = (p.n_valid + splits - 1) / splits;
+        const int64_t step_tokens = (per + atf::kDecodeTokenStep - 1) / atf::kDecodeTokenStep *
+                                    atf::kDecodeTokenStep;
+        if (step_tokens * splits >= kPosLimit)
+            return fail(ATF_EINVAL, "%s: cache too long for the split plan", fn);
+        p.split_tokens = static_cast<int32_t>(step_tokens);
+    }
     p.scale_log2 = scale * 1.4426950408889634f;
     hipError_t e = atf::launch_decode(p, d, static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));

@@ -57,8 +57,12 @@ struct DecodeParams {
                                  // page_tokens-token span (clamped to [0, num_pages)),
                                  // or nullptr: contiguous caches
     int32_t max_pages, num_pages, page_tokens;
-    int32_t splits;
-    int32_t split_tokens;     // tokens per split (multiple of the workgroup's token step)
+    int32_t* ws_plan;         // ragged batch: [B + 1] index of each row's first work item
+                              // (written by the split kernel for the merge), else unused
+    int32_t splits;           // uniform batch: splits per row; ragged batch: work items the
+                              // batch's keys are spread over (a row adds at most one more)
+    int32_t split_tokens;     // uniform batch: tokens per split (multiple of the workgroup's
+                              // token step); ragged batch: unused (derived on the device)
     float scale_log2;
     WindowTable win;
 };
@@ -89,8 +93,10 @@ hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t str
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream);
 
-// Decode split plan: number of KV splits per (batch, kv head) for these sizes.
-int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k, bool ragged);
+// Decode split plan of a uniform batch: number of KV splits per (batch, kv head).
+int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);
+// Work items of a ragged batch (per column of `cols` = kv heads x head subgroups).
+int32_t decode_ragged_items(int32_t cols);
 // Tokens handled per decode workgroup iteration (the split granularity).
 constexpr int32_t kDecodeTokenStep = 128;
 // Largest split count the merge kernel accepts.

@@ -66,6 +66,59 @@ __device__ __forceinline__ u32x4_t keep_pairs(u32x4_t x, uint32_t mask) {
 
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Keys of ragged row r that its query reaches (the clamps keep every read inside the
+// row's cache): min(n_k_rows[r], q_pos_rows[r] + 1), within [0, n_k].
+__device__ __forceinline__ int ragged_valid(const DecodeParams& p, int r) {
+    const int nk = min(max(p.n_k_rows[r], 0), p.n_k);
+    const int qp = min(max(p.q_pos_rows[r], 0), 0x7FFFFFFD);
+    return min(nk, qp + 1);
+}
+
+// Work plan of a ragged batch, the same in every wave that computes it: the batch's
+// causal keys are cut into spans of `span` tokens (about total / p.splits, a multiple
+// of the workgroup's token step), each row into ceil(n_valid / span) items of its own
+// keys, items numbered row by row.  Returns the row of `item` (or -1 past the last
+// item) and its first token; with `plan` set, also writes the index of each row's
+// first item and the item count at plan[B].
+__device__ int ragged_item(const DecodeParams& p, int item, int& t_first, int64_t& span,
+                           int32_t* plan) {
+    const int lane = threadIdx.x & 63;
+    int64_t total = 0;
+    for (int r0 = 0; r0 < p.batch; r0 += 64) {
+        int64_t nv = r0 + lane < p.batch ? ragged_valid(p, r0 + lane) : 0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) nv += __shfl_xor(nv, o);
+        total += nv;
+    }
+    span = (total + p.splits - 1) / p.splits;
+    span = (span + kDecodeTokenStep - 1) / kDecodeTokenStep * kDecodeTokenStep;
+    if (span < kDecodeTokenStep) span = kDecodeTokenStep;
+    int row = -1, first = 0;
+    int before = 0;  // items of the rows below r0
+    for (int r0 = 0; r0 < p.batch; r0 += 64) {
+        const int r = r0 + lane;
+        const int cnt = r < p.batch ? int((ragged_valid(p, r) + span - 1) / span) : 0;
+        int incl = cnt;  // inclusive prefix over the wave's rows
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(incl, o);
+            if (lane >= o) incl += y;
+        }
+        incl += before;
+        if (plan != nullptr && r < p.batch) plan[r] = incl - cnt;
+        const uint64_t hit = __ballot(item < incl);
+        if (row < 0 && hit != 0) {
+            const int l = __builtin_ctzll(hit);
+            row = r0 + l;
+            first = item - __shfl(incl - cnt, l);
+        }
+        before = __shfl(incl, 63);
+    }
+    if (plan != nullptr && lane == 0) plan[p.batch] = before;
+    t_first = int(int64_t(first) * span);
+    return row;
+}
+
 template <int D>
 __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const DecodeParams p) {
     constexpr int kChunks = D / 16;
@@ -85,20 +138,30 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     const int subgroups = p.group / NH;
     const int g = blockIdx.y / subgroups;
     const int sub = blockIdx.y % subgroups;
-    const int b = blockIdx.z;
     const int hq0 = g * p.group + sub * NH;
     const bool head_ok = col < NH;
 
-    // this row's keys and query position (a ragged batch gives them per row; the
-    // clamps keep every read inside the row's cache)
-    int n_k = p.n_k, q_pos = p.q_pos, n_valid = p.n_valid;
+    // this workgroup's row and tokens: a uniform batch has row blockIdx.z and split
+    // `split` of p.split_tokens tokens; a ragged batch gives each row its own keys and
+    // query position, and blockIdx.x is a work item of the plan (ragged_item)
+    int b, n_k = p.n_k, q_pos = p.q_pos, n_valid = p.n_valid, t_begin, t_end;
+    int64_t slot0;  // partial-state slot of head hq0 (heads follow at stride 1)
     if (p.n_k_rows != nullptr) {
+        int64_t span;
+        int32_t* plan = (blockIdx.x == 0 && blockIdx.y == 0 && wave == 0) ? p.ws_plan : nullptr;
+        b = ragged_item(p, split, t_begin, span, plan);
+        if (b < 0) return;  // past the last item (the whole workgroup: wave-uniform)
         n_k = min(max(p.n_k_rows[b], 0), p.n_k);
         q_pos = min(max(p.q_pos_rows[b], 0), 0x7FFFFFFD);
         n_valid = min(n_k, q_pos + 1);
+        t_end = int(min(int64_t(n_valid), int64_t(t_begin) + span));
+        slot0 = int64_t(split) * p.h_q + hq0;
+    } else {
+        b = blockIdx.z;
+        t_begin = split * p.split_tokens;
+        t_end = min(n_valid, t_begin + p.split_tokens);
+        slot0 = (int64_t(b) * p.h_q + hq0) * p.splits + split;
     }
-    const int t_begin = split * p.split_tokens;
-    const int t_end = min(n_valid, t_begin + p.split_tokens);
     const int64_t cap = p.cache_tokens;  // stream length of the caches
     const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * cap * 16;
     const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * ((cap + 15) / 16) * D * 16;
@@ -309,7 +372,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             for (int w = 0; w < kWaves; ++w)
                 if (red_m[w][h] != -INFINITY) L += red_l[w][h] * exp2_fast(red_m[w][h] - M);
         }
-        const int64_t slot = (int64_t(b) * p.h_q + hq0 + h) * p.splits + split;
+        const int64_t slot = p.n_k_rows != nullptr ? slot0 + h : slot0 + int64_t(h) * p.splits;
         if (x == 0) {
             p.ws_m[slot] = M;
             p.ws_l[slot] = L;
@@ -327,9 +390,21 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
     const int bh = blockIdx.x;  // b * h_q + hq
     const int d0 = 32 * blockIdx.y;
     const int tid = threadIdx.x;
-    const int64_t base = int64_t(bh) * p.splits;
+    // partial state s of this (row, head) at slot base + s * stride: a uniform batch
+    // has p.splits of them per head; a ragged row has the items the plan gave it
+    int64_t base = int64_t(bh) * p.splits, stride = 1;
+    int count = p.splits;
+    if (p.n_k_rows != nullptr) {
+        const int b = bh / p.h_q;
+        // (the clamps only restate what the plan guarantees: items < splits + batch)
+        const int first = min(max(p.ws_plan[b], 0), p.splits + p.batch);
+        count = min(min(max(p.ws_plan[b + 1] - first, 0), kDecodeMaxSplits),
+                    p.splits + p.batch - first);
+        base = int64_t(first) * p.h_q + bh % p.h_q;
+        stride = p.h_q;
+    }
     float M = -INFINITY;
-    for (int s = tid; s < p.splits; s += 256) M = fmaxf(M, p.ws_m[base + s]);
+    for (int s = tid; s < count; s += 256) M = fmaxf(M, p.ws_m[base + s * stride]);
     s_red[tid] = M;
     __syncthreads();
     for (int off = 128; off > 0; off >>= 1) {
@@ -339,11 +414,11 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
     M = s_red[0];
     __syncthreads();
     float L = 0.f;
-    for (int s = tid; s < p.splits; s += 256) {
-        const float ms = p.ws_m[base + s];
+    for (int s = tid; s < count; s += 256) {
+        const float ms = p.ws_m[base + s * stride];
         const float w = ms == -INFINITY ? 0.f : exp2_fast(ms - M);  // split with no causal key
         s_w[s] = w;
-        L += p.ws_l[base + s] * w;
+        L += p.ws_l[base + s * stride] * w;
     }
     s_red[tid] = L;
     __syncthreads();
@@ -355,7 +430,7 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
     __syncthreads();
     const int x = tid & 31, sl = tid >> 5;
     float O = 0.f;
-    for (int s = sl; s < p.splits; s += 8) O += s_w[s] * p.ws_o[(base + s) * D + d0 + x];
+    for (int s = sl; s < count; s += 8) O += s_w[s] * p.ws_o[(base + s * stride) * D + d0 + x];
     s_red[tid] = O;
     __syncthreads();
     if (tid < 32) {
@@ -463,8 +538,10 @@ __global__ __launch_bounds__(256) void append_paged_kernel(const AppendPagedPara
 
 template <int D>
 hipError_t launch_decode_d(const DecodeParams& p, hipStream_t stream) {
-    const dim3 grid(unsigned(p.splits), unsigned(p.h_kv * (p.group / p.heads_per_block)),
-                    unsigned(p.batch));
+    // ragged: one workgroup per possible work item (at most p.splits + batch)
+    const bool ragged = p.n_k_rows != nullptr;
+    const dim3 grid(unsigned(ragged ? p.splits + p.batch : p.splits),
+                    unsigned(p.h_kv * (p.group / p.heads_per_block)), unsigned(ragged ? 1 : p.batch));
     hipLaunchKernelGGL(decode_split_kernel<D>, grid, dim3(kWaves * 64), 0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -485,7 +562,11 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream
     if (p.heads_per_block < 1 || p.heads_per_block > kDecodeMaxHeads ||
         p.group % p.heads_per_block != 0)
         return hipErrorInvalidValue;
-    if (int64_t(p.splits) * p.split_tokens < p.n_valid || p.split_tokens % kDecodeTokenStep != 0)
+    if (p.n_k_rows == nullptr &&
+        (int64_t(p.splits) * p.split_tokens < p.n_valid || p.split_tokens % kDecodeTokenStep != 0))
+        return hipErrorInvalidValue;
+    if (p.n_k_rows != nullptr && (p.q_pos_rows == nullptr || p.ws_plan == nullptr ||
+                                  p.splits > kDecodeMaxSplits - 1))
         return hipErrorInvalidValue;
     (void)hipGetLastError();
     return head_dim == 64 ? launch_decode_d<64>(p, stream) : launch_decode_d<128>(p, stream);

@@ -305,7 +305,25 @@ RAGGED_CASES = [
     ([0, 400, 0, 129], [0, 400, 10, 129], 512, 6, 2, 128, 5e5, 2.0),       # empty rows
     ([4096, 4000, 17], [4096, 4000, 17], 4096, 16, 2, 128, 100.0, 2.0),   # saturated windows
     ([999, 3, 640], [999, 3, 640], 1024, 3, 1, 128, 1e4, math.inf),       # window off
+    ([0, 0, 0], [0, 5, 0], 64, 4, 2, 128, 1e4, 2.0),                       # no key in the batch
 ]
+
+
+def _many_rows(n, cap, seed):
+    """n row lengths in [0, cap] (some empty, some full) and query positions at,
+    past or inside each row's cache."""
+    rng = np.random.default_rng(seed)
+    n_ks = [int(x) for x in rng.integers(0, cap + 1, size=n)]
+    n_ks[3] = n_ks[70] = 0
+    n_ks[5] = n_ks[129 % n] = cap
+    q_poss = [nk if i % 3 else nk + int(rng.integers(0, 500)) for i, nk in enumerate(n_ks)]
+    q_poss[7] = max(0, n_ks[7] // 2)
+    return n_ks, q_poss
+
+
+# more rows than one wave scans at once: the device-side work plan runs over the rows
+# in several 64-row steps
+RAGGED_CASES.append(_many_rows(130, 2500, 17) + (2500, 4, 2, 64, 1e6, 2.0))
 
 
 @pytest.mark.parametrize("case", RAGGED_CASES, ids=lambda c: f"B{len(c[0])}_d{c[5]}_k{c[7]}")
