@@ -336,14 +336,14 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "fa4c21d422327fee7a9d939ead0aaf8462631f60b5a5bf670a17f02312c0ccae",
-        "fetch_kib": 79575537.13, "write_kib": 933438.34,
+        "sha256": "4c83e6536f142e9aed990a5d762f358c708abee29e4f01e3ec7b769250f1e3b5",
+        "fetch_kib": 79575537.25, "write_kib": 933437.88,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "1cda64e00cef0ac3fa98cad83e8886900b2bdb830099c0a880aaefd740251993",
-        "fetch_kib": 737770.17, "write_kib": 4062.38,
+        "sha256": "f81dbf6475c3251be05ac5e34dccfddaaa510f896678ed49cf64c7ad3ca4a0a4",
+        "fetch_kib": 737793.15, "write_kib": 4057.15,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy

@@ -381,12 +381,15 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     }
 }
 
-// Merge of the split partials of one (batch, head) and 32 output dims: 256 threads
-// = 8 split lanes x 32 dims.
+// Merge of the split partials of one (batch, head) and 32 output dims: 256 threads.
+// The weights take one state per thread; the output sums take 8 quads of 4 dims x 32
+// state lanes, each lane reading 16 bytes per state, so that all of a thread's loads
+// can be in flight at once.
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p) {
     __shared__ float s_w[kDecodeMaxSplits];  // split weights exp2(m_s - M)
-    __shared__ float s_red[256];
+    __shared__ float s_red[8];     // per-wave max, then per-wave sum
+    __shared__ float s_o[32][33];  // output partial sums of the 32 state lanes
     const int bh = blockIdx.x;  // b * h_q + hq
     const int d0 = 32 * blockIdx.y;
     const int tid = threadIdx.x;
@@ -403,16 +406,14 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
         base = int64_t(first) * p.h_q + bh % p.h_q;
         stride = p.h_q;
     }
+    const int wave = tid >> 6;
     float M = -INFINITY;
     for (int s = tid; s < count; s += 256) M = fmaxf(M, p.ws_m[base + s * stride]);
-    s_red[tid] = M;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+    if ((tid & 63) == 0) s_red[wave] = M;
     __syncthreads();
-    for (int off = 128; off > 0; off >>= 1) {
-        if (tid < off) s_red[tid] = fmaxf(s_red[tid], s_red[tid + off]);
-        __syncthreads();
-    }
-    M = s_red[0];
-    __syncthreads();
+    M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
     float L = 0.f;
     for (int s = tid; s < count; s += 256) {
         const float ms = p.ws_m[base + s * stride];
@@ -420,23 +421,32 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(const DecodeParams p)
         s_w[s] = w;
         L += p.ws_l[base + s * stride] * w;
     }
-    s_red[tid] = L;
-    __syncthreads();
-    for (int off = 128; off > 0; off >>= 1) {
-        if (tid < off) s_red[tid] += s_red[tid + off];
-        __syncthreads();
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o);
+    if ((tid & 63) == 0) s_red[4 + wave] = L;
+    __syncthreads();  // also publishes s_w
+    L = (s_red[4] + s_red[5]) + (s_red[6] + s_red[7]);
+    const int q = tid & 7, sl = tid >> 3;  // dims d0 + 4q .. d0 + 4q + 3, state lane sl
+    float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int s = sl; s < count; s += 32) {
+        const float w = s_w[s];
+        const float4 v = *reinterpret_cast<const float4*>(p.ws_o + (base + s * stride) * D + d0 + 4 * q);
+        O.x += w * v.x;
+        O.y += w * v.y;
+        O.z += w * v.z;
+        O.w += w * v.w;
     }
-    L = s_red[0];
-    __syncthreads();
-    const int x = tid & 31, sl = tid >> 5;
-    float O = 0.f;
-    for (int s = sl; s < count; s += 8) O += s_w[s] * p.ws_o[(base + s * stride) * D + d0 + x];
-    s_red[tid] = O;
+    s_o[sl][4 * q] = O.x;
+    s_o[sl][4 * q + 1] = O.y;
+    s_o[sl][4 * q + 2] = O.z;
+    s_o[sl][4 * q + 3] = O.w;
     __syncthreads();
     if (tid < 32) {
+        const int x = tid;
         float acc = 0.f;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) acc += s_red[tid + 32 * k];
+        for (int k = 0; k < 32; ++k) acc += s_o[k][x];
         // a ragged row without keys has an empty softmax: O = 0, LSE = -inf
         const bool empty = !(L > 0.f);
         p.o[int64_t(bh) * D + d0 + x] = __builtin_bit_cast(uint16_t, (__bf16)(empty ? 0.f : acc / L));
