@@ -337,13 +337,13 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
         "sha256": "4c83e6536f142e9aed990a5d762f358c708abee29e4f01e3ec7b769250f1e3b5",
-        "fetch_kib": 79575537.25, "write_kib": 933437.88,
+        "fetch_kib": 79575536.00, "write_kib": 933438.84,
     },
     "decode_split_kernel<128>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "f81dbf6475c3251be05ac5e34dccfddaaa510f896678ed49cf64c7ad3ca4a0a4",
-        "fetch_kib": 737793.15, "write_kib": 4057.15,
+        "sha256": "392a8b5c497079ff4f3f736e9846fc6339afcc06ebf4861a4de01bde3f14deca",
+        "fetch_kib": 737787.19, "write_kib": 4055.65,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
