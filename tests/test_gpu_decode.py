@@ -127,6 +127,7 @@ CASES = [
     (1, 4096, 4096, 16, 2, 128, 100.0, 2.0),    # saturated windows
     (1, 513, 513, 2, 2, 64, 1e4, 0.05),         # tiny k: empty score sums
     (1, 999, 999, 3, 1, 128, 1e4, math.inf),    # window off
+    (1, 300000, 300000, 8, 1, 64, 1e6, 2.0),    # 1024 splits: several merge passes per head
 ]
 
 
@@ -324,6 +325,8 @@ def _many_rows(n, cap, seed):
 # more rows than one wave scans at once: the device-side work plan runs over the rows
 # in several 64-row steps
 RAGGED_CASES.append(_many_rows(130, 2500, 17) + (2500, 4, 2, 64, 1e6, 2.0))
+# one KV head: a long row gets over a thousand work items, merged in several passes
+RAGGED_CASES.append(([300000, 5, 1000], [300000, 5, 1000], 300000, 8, 1, 64, 1e6, 2.0))
 
 
 @pytest.mark.parametrize("case", RAGGED_CASES, ids=lambda c: f"B{len(c[0])}_d{c[5]}_k{c[7]}")
