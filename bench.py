@@ -524,6 +524,23 @@ def main():
         decode_info["full_window_GBps"] = round(
             bytes_decode_full / (full["decode_ms"] * 1e-3) / 1e9, 1)
 
+    # ---- the same decode from unrotated caches (RoPE applied at read time, App. B): the
+    # same bytes, plus one rotation per kept (token, pair) in the kernel; timed on the
+    # same buffers (the work does not depend on the values)
+    def decode_unrot(w):
+        atf.atf_decode_unrotated(qd, kp, vp, od, lsed, dc.q_pos0, w, ws, stream=stream)
+
+    tu = _median_ms(lambda: decode_unrot(win), stream, 3, args.decode_iters)
+    decode_info["unrotated_cache"] = {
+        "ms": round(tu, 4), "GBps": round(bytes_decode / (tu * 1e-3) / 1e9, 1),
+        "frac_hbm_peak": round(bytes_decode / (tu * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "time_vs_rotated_cache": round(tu / dec_med, 4),
+        "rotated_token_pairs_per_kv_head": Td, "full_window_rotations_per_kv_head": Td_full}
+    if full is not None:
+        tu_off = _median_ms(lambda: decode_unrot(win_off), stream, 3, args.decode_iters)
+        decode_info["unrotated_cache"]["full_window_ms"] = round(tu_off, 4)
+        decode_info["unrotated_cache"]["speedup_vs_full_window"] = round(tu_off / tu, 4)
+
     # ---- other windows on the same inputs: the variable-k profile 16 -> 2 and uniform
     # k = 64 (App. A, tab:absbench), and the rounded slice (Sec. 3.3, tab:c2e2e)
     family = None

@@ -17,6 +17,9 @@ module only marshals numpy arrays into it:
 - :func:`attend` -- windowed causal attention, plain two-pass softmax, for all
   or a sample of query rows; O, LSE and the per-row retained-term count.
 - :func:`count_terms` -- the retained-term and causal-cell counts of Sec. 4.
+- :func:`rope_rotate` -- the RoPE rotation of Sec. 3.1 (pair r rotated by
+  position * theta_r, rotate-half pairing), in numpy fp64: the reference for
+  decode from unrotated caches (App. B, rotation at read time).
 
 Every function whose result is checked against something other than itself is
 listed in ``tests/test_oracle.py``; none is "parity unpinned".
@@ -237,3 +240,26 @@ def count_terms(widths, n_q: int, q_pos0: int, n_k: int, atom: int = 0, by_dista
     if rc != 0:
         raise ValueError("oracle_count_terms: bad arguments")
     return int(ret[0]), int(cau[0])
+
+
+def rope_rotate(x, positions, theta):
+    """RoPE rotation in fp64 (Sec. 3.1): x [..., n, h, d] at positions [n]; pair r
+    is dims (r, r + d/2), rotated by angle positions[i] * theta[r]:
+    x'_r = x_r cos - x_{r+d/2} sin, x'_{r+d/2} = x_{r+d/2} cos + x_r sin.
+    x may be a bf16 torch tensor, bf16 bits as uint16, or a float array."""
+    xa, dt = _as_input(x)
+    if dt == _BF16:
+        xa = (xa.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    d = xa.shape[-1]
+    h = d // 2
+    pos = np.asarray(positions, dtype=np.float64)
+    th = np.asarray(theta, dtype=np.float64)
+    assert th.shape == (h,) and pos.shape == (xa.shape[-3],)
+    ang = pos[:, None] * th[None, :]                 # [n, h]
+    c = np.cos(ang)[:, None, :]                      # [n, 1, h]: the same for every head
+    s_ = np.sin(ang)[:, None, :]
+    a, b = xa[..., :h], xa[..., h:]
+    out = np.empty_like(xa)
+    out[..., :h] = a * c - b * s_
+    out[..., h:] = b * c + a * s_
+    return out

@@ -478,11 +478,44 @@ struct PagedArgs {
     int32_t max_pages = 0, num_pages = 0, page_tokens = 0;
 };
 
+// RoPE at read time (q and the K cache unrotated): theta_r = rope_inv_freq[r] if given,
+// else the window's frequencies (its inv_freq, or rope_base^(-2r/d)).
+struct RopeArgs {
+    bool rotate = false;
+    const double* inv_freq = nullptr;
+};
+
+// rho_r = theta_r / (2 pi) mod 1 as a 0.64 fixed-point fraction, in extended precision
+int rope_fractions(const char* fn, const atf_window* w, const double* inv_freq,
+                   atf::DecodeParams* p) {
+    const int d = w->head_dim;
+    const long double two_pi = 6.283185307179586476925286766559L;
+    for (int r = 0; r < d / 2; ++r) {
+        double th;
+        if (inv_freq != nullptr)
+            th = inv_freq[r];
+        else if (w->inv_freq != nullptr)
+            th = w->inv_freq[r];
+        else
+            th = std::pow(w->rope_base, -2.0 * r / d);
+        if (!(th >= 0.0) || std::isinf(th))
+            return fail(ATF_EINVAL, "%s: rotation frequency %d = %g must be finite and >= 0", fn, r,
+                        th);
+        long double f = static_cast<long double>(th) / two_pi;
+        f -= std::floor(f);
+        long double scaled = std::ldexp(f, 64);
+        uint64_t fx = scaled >= 18446744073709551615.0L ? UINT64_MAX : static_cast<uint64_t>(scaled);
+        p->rope_rho_hi[r] = static_cast<uint32_t>(fx >> 32);
+        p->rope_rho_lo[r] = static_cast<uint32_t>(fx);
+    }
+    return ATF_OK;
+}
+
 int decode_impl(const char* fn, const void* q, const void* k_cache, const void* v_cache, void* o,
                 float* lse, int32_t batch, int64_t n_k, int64_t q_pos, const int32_t* n_k_rows,
                 const int32_t* q_pos_rows, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
                 const atf_window* w, float softmax_scale, void* workspace, size_t workspace_bytes,
-                void* hip_stream, const PagedArgs& pg = PagedArgs()) {
+                void* hip_stream, const PagedArgs& pg = PagedArgs(), const RopeArgs& rope = RopeArgs()) {
     const bool ragged = n_k_rows != nullptr || q_pos_rows != nullptr;
     if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
     const int d = w->head_dim;
@@ -503,6 +536,11 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
     atf::DecodeParams p{};
     int rc = build_table(w, &p.win);
     if (rc != ATF_OK) return rc;
+    if (rope.rotate) {
+        rc = rope_fractions(fn, w, rope.inv_freq, &p);
+        if (rc != ATF_OK) return rc;
+        p.rotate = 1;
+    }
     if (!q || !k_cache || !v_cache || !o || !lse)
         return fail(ATF_EINVAL, "%s: NULL tensor pointer", fn);
     if (ragged && (!n_k_rows || !q_pos_rows))
@@ -585,6 +623,19 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
                        hip_stream);
 }
 
+int atf_decode_unrotated(const void* q, const void* k_cache, const void* v_cache, void* o,
+                         float* lse, int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q,
+                         int32_t h_kv, int64_t cache_tokens, const atf_window* w,
+                         const double* rope_inv_freq, float softmax_scale, void* workspace,
+                         size_t workspace_bytes, void* hip_stream) {
+    RopeArgs rope;
+    rope.rotate = true;
+    rope.inv_freq = rope_inv_freq;
+    return decode_impl("decode_unrotated", q, k_cache, v_cache, o, lse, batch, n_k, q_pos, nullptr,
+                       nullptr, h_q, h_kv, cache_tokens, w, softmax_scale, workspace,
+                       workspace_bytes, hip_stream, PagedArgs(), rope);
+}
+
 int atf_decode_ragged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                       int32_t batch, const int32_t* n_k_rows, const int32_t* q_pos_rows,
                       int64_t max_n_k, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
@@ -597,33 +648,68 @@ int atf_decode_ragged(const void* q, const void* k_cache, const void* v_cache, v
                        workspace_bytes, hip_stream);
 }
 
-int atf_decode_paged(const void* q, const void* k_pages, const void* v_pages, void* o, float* lse,
-                     int32_t batch, const int32_t* block_table, int32_t max_pages_per_row,
-                     int32_t num_pages, int32_t page_tokens, const int32_t* n_k_rows,
-                     const int32_t* q_pos_rows, int64_t max_n_k, int32_t h_q, int32_t h_kv,
-                     const atf_window* w, float softmax_scale, void* workspace,
-                     size_t workspace_bytes, void* hip_stream) {
-    if (!block_table) return fail(ATF_EINVAL, "decode_paged: NULL block table");
+}  // extern "C"
+
+namespace {
+int decode_paged_impl(const char* fn, const void* q, const void* k_pages, const void* v_pages,
+                      void* o, float* lse, int32_t batch, const int32_t* block_table,
+                      int32_t max_pages_per_row, int32_t num_pages, int32_t page_tokens,
+                      const int32_t* n_k_rows, const int32_t* q_pos_rows, int64_t max_n_k,
+                      int32_t h_q, int32_t h_kv, const atf_window* w, float softmax_scale,
+                      void* workspace, size_t workspace_bytes, void* hip_stream,
+                      const RopeArgs& rope) {
+    if (!block_table) return fail(ATF_EINVAL, "%s: NULL block table", fn);
     if (!n_k_rows || !q_pos_rows)
-        return fail(ATF_EINVAL, "decode_paged: NULL row-length or row-position array");
+        return fail(ATF_EINVAL, "%s: NULL row-length or row-position array", fn);
     if (page_tokens < 32 || page_tokens % 32 != 0)
-        return fail(ATF_EINVAL, "decode_paged: page_tokens %d must be a positive multiple of 32",
-                    page_tokens);
+        return fail(ATF_EINVAL, "%s: page_tokens %d must be a positive multiple of 32",
+                    fn, page_tokens);
     if (num_pages < 1 || max_pages_per_row < 1)
-        return fail(ATF_EINVAL, "decode_paged: need num_pages >= 1 and max_pages_per_row >= 1");
+        return fail(ATF_EINVAL, "%s: need num_pages >= 1 and max_pages_per_row >= 1", fn);
     const int64_t row_cap = int64_t(max_pages_per_row) * page_tokens;
     if (max_n_k > row_cap || row_cap > kPosLimit)
-        return fail(ATF_EINVAL, "decode_paged: max_n_k %lld exceeds the %lld tokens a row's pages "
-                    "hold (or that exceeds 2^31 - 1)", (long long)max_n_k, (long long)row_cap);
+        return fail(ATF_EINVAL, "%s: max_n_k %lld exceeds the %lld tokens a row's pages "
+                    "hold (or that exceeds 2^31 - 1)", fn, (long long)max_n_k, (long long)row_cap);
     PagedArgs pg;
     pg.block_table = block_table;
     pg.max_pages = max_pages_per_row;
     pg.num_pages = num_pages;
     pg.page_tokens = page_tokens;
     // the contiguous-cache capacity is the rows' span; the kernel addresses pages instead
-    return decode_impl("decode_paged", q, k_pages, v_pages, o, lse, batch, max_n_k, 0, n_k_rows,
-                       q_pos_rows, h_q, h_kv, row_cap, w, softmax_scale, workspace,
-                       workspace_bytes, hip_stream, pg);
+    return decode_impl(fn, q, k_pages, v_pages, o, lse, batch, max_n_k, 0, n_k_rows, q_pos_rows,
+                       h_q, h_kv, row_cap, w, softmax_scale, workspace, workspace_bytes, hip_stream,
+                       pg, rope);
+}
+}  // namespace
+
+extern "C" {
+
+int atf_decode_paged(const void* q, const void* k_pages, const void* v_pages, void* o, float* lse,
+                     int32_t batch, const int32_t* block_table, int32_t max_pages_per_row,
+                     int32_t num_pages, int32_t page_tokens, const int32_t* n_k_rows,
+                     const int32_t* q_pos_rows, int64_t max_n_k, int32_t h_q, int32_t h_kv,
+                     const atf_window* w, float softmax_scale, void* workspace,
+                     size_t workspace_bytes, void* hip_stream) {
+    return decode_paged_impl("decode_paged", q, k_pages, v_pages, o, lse, batch, block_table,
+                             max_pages_per_row, num_pages, page_tokens, n_k_rows, q_pos_rows,
+                             max_n_k, h_q, h_kv, w, softmax_scale, workspace, workspace_bytes,
+                             hip_stream, RopeArgs());
+}
+
+int atf_decode_paged_unrotated(const void* q, const void* k_pages, const void* v_pages, void* o,
+                               float* lse, int32_t batch, const int32_t* block_table,
+                               int32_t max_pages_per_row, int32_t num_pages, int32_t page_tokens,
+                               const int32_t* n_k_rows, const int32_t* q_pos_rows,
+                               int64_t max_n_k, int32_t h_q, int32_t h_kv, const atf_window* w,
+                               const double* rope_inv_freq, float softmax_scale, void* workspace,
+                               size_t workspace_bytes, void* hip_stream) {
+    RopeArgs rope;
+    rope.rotate = true;
+    rope.inv_freq = rope_inv_freq;
+    return decode_paged_impl("decode_paged_unrotated", q, k_pages, v_pages, o, lse, batch,
+                             block_table, max_pages_per_row, num_pages, page_tokens, n_k_rows,
+                             q_pos_rows, max_n_k, h_q, h_kv, w, softmax_scale, workspace,
+                             workspace_bytes, hip_stream, rope);
 }
 
 int atf_cache_append_paged(const void* k_new, const void* v_new, void* k_pages, void* v_pages,

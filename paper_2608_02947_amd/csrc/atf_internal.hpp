@@ -65,6 +65,12 @@ struct DecodeParams {
                               // token step); ragged batch: unused (derived on the device)
     float scale_log2;
     WindowTable win;
+    // RoPE at read time: q and the K cache hold unrotated vectors; pair r of a vector
+    // at position pos is rotated by pos * theta_r, with rho_r = theta_r / (2 pi) mod 1
+    // as a 0.64 fixed-point fraction (hi and lo words)
+    int32_t rotate;
+    uint32_t rope_rho_hi[kMaxPairs];
+    uint32_t rope_rho_lo[kMaxPairs];
 };
 
 struct AppendPagedParams {

@@ -119,7 +119,50 @@ __device__ int ragged_item(const DecodeParams& p, int item, int& t_first, int64_
     return row;
 }
 
-template <int D>
+// RoPE at read time.  The angle of pair r at position pos, in revolutions: the high
+// word of the fraction of pos * rho_r (rho_r = theta_r / (2 pi) in 0.64 fixed point),
+// exact for every position below 2^32 up to the last bit of rho_r.
+__device__ __forceinline__ float rope_revolutions(uint32_t pos, uint2 rho) {
+    return float(pos * rho.x + __umulhi(pos, rho.y)) * 2.3283064365386963e-10f;  // 2^-32
+}
+
+// Rotate one fragment: the 8 elements of half hh of pairs 8c .. 8c + 7 of a vector at
+// position pos (`own`), given the other half of the same pairs (`other`).  Half 0
+// holds the first components x_r and half 1 the second x_{r + d/2} (rotate-half):
+// x'_r = x_r cos - x_{r+d/2} sin and x'_{r+d/2} = x_{r+d/2} cos + x_r sin, in fp32,
+// rounded to bf16.  v_cos_f32 / v_sin_f32 take their argument in revolutions.
+__device__ __forceinline__ u32x4_t rope_rotate(u32x4_t own, u32x4_t other, int hh, uint32_t pos,
+                                               const uint32_t* rho_hi8, const uint32_t* rho_lo8) {
+    const float sgn = hh ? 1.f : -1.f;
+    u32x4_t r;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const float o0 = __uint_as_float(own[t] << 16), o1 = __uint_as_float(own[t] & 0xFFFF0000u);
+        const float x0 = __uint_as_float(other[t] << 16), x1 = __uint_as_float(other[t] & 0xFFFF0000u);
+        const float u0 = rope_revolutions(pos, make_uint2(rho_hi8[2 * t], rho_lo8[2 * t]));
+        const float u1 = rope_revolutions(pos, make_uint2(rho_hi8[2 * t + 1], rho_lo8[2 * t + 1]));
+        bf16x2_t two;
+        two[0] = (__bf16)__builtin_fmaf(o0, __builtin_amdgcn_cosf(u0), sgn * x0 * __builtin_amdgcn_sinf(u0));
+        two[1] = (__bf16)__builtin_fmaf(o1, __builtin_amdgcn_cosf(u1), sgn * x1 * __builtin_amdgcn_sinf(u1));
+        r[t] = __builtin_bit_cast(uint32_t, two);
+    }
+    return r;
+}
+
+// The other half of a fragment: lane l gets the registers of lane l ^ 32 (the same
+// token or head column, the other 8 dims of each pair).
+__device__ __forceinline__ u32x4_t other_half(u32x4_t x, int hh) {
+    u32x4_t r;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        // lanes 32..63 of the first copy trade places with lanes 0..31 of the second
+        const auto sw = __builtin_amdgcn_permlane32_swap(x[t], x[t], false, false);
+        r[t] = hh ? sw[0] : sw[1];
+    }
+    return r;
+}
+
+template <int D, bool kRot>
 __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const DecodeParams p) {
     constexpr int kChunks = D / 16;
     constexpr int kHalf = D / 2;
@@ -168,13 +211,18 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     const int my_w = lane < kHalf ? p.win.W[lane] : -1;
 
     // query fragments (B operand): head column `col`, dims of half hh of every chunk
+    // (rotated to the query position here when the query is given unrotated)
     u32x4_t qf[kChunks];
     {
-        const uint16_t* qrow = p.q + (int64_t(b) * p.h_q + hq0 + (head_ok ? col : 0)) * D + hh * kHalf;
+        const uint16_t* qvec = p.q + (int64_t(b) * p.h_q + hq0 + (head_ok ? col : 0)) * D;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) {
             u32x4_t z = {0u, 0u, 0u, 0u};
-            if (head_ok) z = *reinterpret_cast<const u32x4_t*>(qrow + 8 * c);
+            if (head_ok) z = *reinterpret_cast<const u32x4_t*>(qvec + hh * kHalf + 8 * c);
+            // (both lanes of a pair hold the same column, and zeros rotate to zeros)
+            if constexpr (kRot)
+                z = rope_rotate(z, other_half(z, hh), hh, uint32_t(q_pos), &p.rope_rho_hi[8 * c],
+                                &p.rope_rho_lo[8 * c]);
             qf[c] = z;
         }
     }
@@ -220,6 +268,19 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             if (kept && tok_ok)
                 z = *reinterpret_cast<const u32x4_t*>(kb + (int64_t(c) * kstride + tok - tb) * 16 + 8 * hh);
             kf[c] = z;
+        }
+        if constexpr (kRot) {
+            // the keys at their positions t0 + col, rotated here: only the kept chunks
+            // are read, so only their pairs are rotated (both lanes of a pair hold the
+            // same token).  One chunk at a time, to bound the live registers.
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
+                if (kept)
+                    kf[c] = rope_rotate(kf[c], other_half(kf[c], hh), hh, uint32_t(tok),
+                                        &p.rope_rho_hi[8 * c], &p.rope_rho_lo[8 * c]);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
         // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each
         // 16-token group).  Blocks past n_k are not read; in the block holding
@@ -552,7 +613,10 @@ hipError_t launch_decode_d(const DecodeParams& p, hipStream_t stream) {
     const bool ragged = p.n_k_rows != nullptr;
     const dim3 grid(unsigned(ragged ? p.splits + p.batch : p.splits),
                     unsigned(p.h_kv * (p.group / p.heads_per_block)), unsigned(ragged ? 1 : p.batch));
-    hipLaunchKernelGGL(decode_split_kernel<D>, grid, dim3(kWaves * 64), 0, stream, p);
+    if (p.rotate)
+        hipLaunchKernelGGL((decode_split_kernel<D, true>), grid, dim3(kWaves * 64), 0, stream, p);
+    else
+        hipLaunchKernelGGL((decode_split_kernel<D, false>), grid, dim3(kWaves * 64), 0, stream, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(decode_merge_kernel<D>, dim3(unsigned(p.batch * p.h_q), unsigned(D / 32)),

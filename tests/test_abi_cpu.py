@@ -379,6 +379,41 @@ def test_paged_validation_before_launch():
     assert "decode_paged" in atf.atf_last_error()
 
 
+def test_unrotated_validation_before_launch():
+    """Rotation frequencies are checked before launch (the window and workspace as for
+    atf_decode / atf_decode_paged); every call below fails, so nothing is launched."""
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    good = [1e4 ** (-2.0 * r / 128) for r in range(64)]
+
+    def freq(f):
+        if f is None:
+            return None
+        arr = (ctypes.c_double * len(f))(*f)
+        freq.keep = arr
+        return ctypes.cast(arr, ctypes.c_void_p)
+
+    def dec(f=None):
+        return lib.atf_decode_unrotated(16, 16, 16, 16, 16, 1, 1000, 1000, 8, 2, 1000,
+                                        ctypes.byref(w), freq(f), 0.0, 16, 16, None)
+
+    def paged(f=None):
+        return lib.atf_decode_paged_unrotated(16, 16, 16, 16, 16, 2, 1 << 12, 4, 8, 64, 1 << 13,
+                                              1 << 14, 256, 24, 8, ctypes.byref(w), freq(f), 0.0,
+                                              16, 16, None)
+
+    assert dec() == atf.ATF_EWORKSPACE               # the window's frequencies
+    assert dec(good) == atf.ATF_EWORKSPACE
+    assert paged(good) == atf.ATF_EWORKSPACE
+    for bad in (-1.0, float("inf"), float("nan")):
+        f = list(good)
+        f[5] = bad
+        assert dec(f) == atf.ATF_EINVAL
+        assert "decode_unrotated" in atf.atf_last_error()
+        assert paged(f) == atf.ATF_EINVAL
+        assert "decode_paged_unrotated" in atf.atf_last_error()
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap
