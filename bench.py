@@ -336,14 +336,14 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "4c83e6536f142e9aed990a5d762f358c708abee29e4f01e3ec7b769250f1e3b5",
-        "fetch_kib": 79575536.00, "write_kib": 933438.84,
+        "sha256": "7f4f3aef15ba0eb37498f40aed6fd6fde372a1853507dbb463b69fcb58555832",
+        "fetch_kib": 79575531.88, "write_kib": 933439.81,
     },
-    "decode_split_kernel<128>": {
+    "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "392a8b5c497079ff4f3f736e9846fc6339afcc06ebf4861a4de01bde3f14deca",
-        "fetch_kib": 737787.19, "write_kib": 4055.65,
+        "sha256": "13a29fa922ac0b0d577f7cd6f6e1b9195405c143e6c807f46677b01fbecd78aa",
+        "fetch_kib": 737817.44, "write_kib": 4062.67,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
@@ -571,7 +571,7 @@ def main():
     if tr is not None:
         roofline["traffic_fetch_bytes"] = tr["fetch_bytes"]
         roofline["traffic_write_bytes"] = tr["write_bytes"]
-    trd = recorded_traffic("decode_split_kernel<128>")
+    trd = recorded_traffic("decode_split_kernel<128, false>")
     decode_info["hbm_traffic_bytes"] = None if trd is None else trd["bytes"]
 
     cpu = None
