@@ -149,6 +149,23 @@ __device__ __forceinline__ u32x4_t rope_rotate(u32x4_t own, u32x4_t other, int h
     return r;
 }
 
+// Rotate one fragment given the cosines and sines of its 8 pairs' angles: as rope_rotate.
+__device__ __forceinline__ u32x4_t rope_rotate_cs(u32x4_t own, u32x4_t other, int hh,
+                                                  const float* cs8, const float* sn8) {
+    const float sgn = hh ? 1.f : -1.f;
+    u32x4_t r;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const float o0 = __uint_as_float(own[t] << 16), o1 = __uint_as_float(own[t] & 0xFFFF0000u);
+        const float x0 = __uint_as_float(other[t] << 16), x1 = __uint_as_float(other[t] & 0xFFFF0000u);
+        bf16x2_t two;
+        two[0] = (__bf16)__builtin_fmaf(o0, cs8[2 * t], sgn * x0 * sn8[2 * t]);
+        two[1] = (__bf16)__builtin_fmaf(o1, cs8[2 * t + 1], sgn * x1 * sn8[2 * t + 1]);
+        r[t] = __builtin_bit_cast(uint32_t, two);
+    }
+    return r;
+}
+
 // The other half of a fragment: lane l gets the registers of lane l ^ 32 (the same
 // token or head column, the other 8 dims of each pair).
 __device__ __forceinline__ u32x4_t other_half(u32x4_t x, int hh) {
@@ -170,6 +187,12 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     __shared__ float red_m[kWaves][32];
     __shared__ float red_l[kWaves][32];
     __shared__ float red_o[kDecodeMaxHeads][D + 1];
+    // rotation at read time: cos and sin of col * theta_r for the 32 token columns of a
+    // block (row col: pairs interleaved as (cos, sin)); a key's angle is the block's
+    // t0 * theta_r plus this, combined by angle addition.  Rows padded by 16 bytes so the
+    // 32 columns' reads fall in different banks.
+    constexpr int kCStride = 2 * kHalf + 4;
+    __shared__ __attribute__((aligned(16))) float s_colcs[kRot ? 32 * kCStride : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -209,6 +232,18 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * cap * 16;
     const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * ((cap + 15) / 16) * D * 16;
     const int my_w = lane < kHalf ? p.win.W[lane] : -1;
+    if constexpr (kRot) {
+        for (int e = tid; e < 32 * kHalf; e += kWaves * 64) {
+            const int cc = e / kHalf, r = e % kHalf;
+            const float u = rope_revolutions(uint32_t(cc), make_uint2(p.rope_rho_hi[r], p.rope_rho_lo[r]));
+            s_colcs[cc * kCStride + 2 * r] = __builtin_amdgcn_cosf(u);
+            s_colcs[cc * kCStride + 2 * r + 1] = __builtin_amdgcn_sinf(u);
+        }
+        __syncthreads();
+    }
+    // lane r's pair (r < d/2): its rotation fraction, for the per-block angles
+    const uint2 my_rho = kRot && lane < kHalf ? make_uint2(p.rope_rho_hi[lane], p.rope_rho_lo[lane])
+                                              : make_uint2(0u, 0u);
 
     // query fragments (B operand): head column `col`, dims of half hh of every chunk
     // (rotated to the query position here when the query is given unrotated)
@@ -272,13 +307,31 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
         if constexpr (kRot) {
             // the keys at their positions t0 + col, rotated here: only the kept chunks
             // are read, so only their pairs are rotated (both lanes of a pair hold the
-            // same token).  One chunk at a time, to bound the live registers.
+            // same token).  Angle of (t0 + col, r) by angle addition: lane r evaluates
+            // the block's t0 * theta_r once, every lane reads col * theta_r from LDS.
+            const float ub = rope_revolutions(uint32_t(t0), my_rho);
+            const float cb = __builtin_amdgcn_cosf(ub), sb = __builtin_amdgcn_sinf(ub);
 #pragma unroll
             for (int c = 0; c < kChunks; ++c) {
                 const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
-                if (kept)
-                    kf[c] = rope_rotate(kf[c], other_half(kf[c], hh), hh, uint32_t(tok),
-                                        &p.rope_rho_hi[8 * c], &p.rope_rho_lo[8 * c]);
+                if (kept) {
+                    const float* row = &s_colcs[col * kCStride + 16 * c];
+                    float cs8[8], sn8[8];
+#pragma unroll
+                    for (int q4 = 0; q4 < 4; ++q4) {
+                        const float4 v = *reinterpret_cast<const float4*>(row + 4 * q4);  // pairs 2q4, 2q4+1
+#pragma unroll
+                        for (int j = 0; j < 2; ++j) {
+                            const int e = 2 * q4 + j;
+                            const float cB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cb), 8 * c + e));
+                            const float sB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sb), 8 * c + e));
+                            const float cC = j ? v.z : v.x, sC = j ? v.w : v.y;
+                            cs8[e] = __builtin_fmaf(cB, cC, -sB * sC);
+                            sn8[e] = __builtin_fmaf(sB, cC, cB * sC);
+                        }
+                    }
+                    kf[c] = rope_rotate_cs(kf[c], other_half(kf[c], hh), hh, cs8, sn8);
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
