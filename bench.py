@@ -337,13 +337,13 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
         "sha256": "7f4f3aef15ba0eb37498f40aed6fd6fde372a1853507dbb463b69fcb58555832",
-        "fetch_kib": 79575531.88, "write_kib": 933439.81,
+        "fetch_kib": 79575533.38, "write_kib": 933439.03,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "13a29fa922ac0b0d577f7cd6f6e1b9195405c143e6c807f46677b01fbecd78aa",
-        "fetch_kib": 737817.44, "write_kib": 4062.67,
+        "sha256": "f9b39eae46306cb63404a4121fd8fee3bb8f489b2cbb9313048ffa5dbe23c3c3",
+        "fetch_kib": 737787.48, "write_kib": 4056.86,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
