@@ -342,8 +342,8 @@ TRAFFIC_RECORDS = {
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "f9b39eae46306cb63404a4121fd8fee3bb8f489b2cbb9313048ffa5dbe23c3c3",
-        "fetch_kib": 737787.48, "write_kib": 4056.86,
+        "sha256": "895b78f8b7c1e164a18ea4ae64115d473c3bbef87cca27e3969ae9fdc0652657",
+        "fetch_kib": 737786.08, "write_kib": 4058.24,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy

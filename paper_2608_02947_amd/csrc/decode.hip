@@ -27,6 +27,15 @@
 // block, and pairs kept at some distance.  Chunks with no kept pair are not
 // loaded.  Pairs whose window ends inside the block get one extra MFMA each,
 // added only to the tokens within their window.
+//
+// Batches: a uniform batch splits every row into the same token ranges; a ragged or
+// paged batch (row lengths in device arrays) cuts the batch's keys into equal spans,
+// each row into whole spans of its own keys, laid out by every workgroup from the row
+// arrays (ragged_item).
+//
+// Rotation at read time (App. B): with unrotated q and K the kernel applies RoPE to
+// the query once and to each key chunk it loads, so a pruned pair is neither read nor
+// rotated.
 #include "atf_internal.hpp"
 
 namespace atf {
@@ -126,30 +135,11 @@ __device__ __forceinline__ float rope_revolutions(uint32_t pos, uint2 rho) {
     return float(pos * rho.x + __umulhi(pos, rho.y)) * 2.3283064365386963e-10f;  // 2^-32
 }
 
-// Rotate one fragment: the 8 elements of half hh of pairs 8c .. 8c + 7 of a vector at
-// position pos (`own`), given the other half of the same pairs (`other`).  Half 0
-// holds the first components x_r and half 1 the second x_{r + d/2} (rotate-half):
-// x'_r = x_r cos - x_{r+d/2} sin and x'_{r+d/2} = x_{r+d/2} cos + x_r sin, in fp32,
-// rounded to bf16.  v_cos_f32 / v_sin_f32 take their argument in revolutions.
-__device__ __forceinline__ u32x4_t rope_rotate(u32x4_t own, u32x4_t other, int hh, uint32_t pos,
-                                               const uint32_t* rho_hi8, const uint32_t* rho_lo8) {
-    const float sgn = hh ? 1.f : -1.f;
-    u32x4_t r;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const float o0 = __uint_as_float(own[t] << 16), o1 = __uint_as_float(own[t] & 0xFFFF0000u);
-        const float x0 = __uint_as_float(other[t] << 16), x1 = __uint_as_float(other[t] & 0xFFFF0000u);
-        const float u0 = rope_revolutions(pos, make_uint2(rho_hi8[2 * t], rho_lo8[2 * t]));
-        const float u1 = rope_revolutions(pos, make_uint2(rho_hi8[2 * t + 1], rho_lo8[2 * t + 1]));
-        bf16x2_t two;
-        two[0] = (__bf16)__builtin_fmaf(o0, __builtin_amdgcn_cosf(u0), sgn * x0 * __builtin_amdgcn_sinf(u0));
-        two[1] = (__bf16)__builtin_fmaf(o1, __builtin_amdgcn_cosf(u1), sgn * x1 * __builtin_amdgcn_sinf(u1));
-        r[t] = __builtin_bit_cast(uint32_t, two);
-    }
-    return r;
-}
-
-// Rotate one fragment given the cosines and sines of its 8 pairs' angles: as rope_rotate.
+// Rotate one fragment: the 8 elements of half hh of pairs 8c .. 8c + 7 of a vector
+// (`own`), given the other half of the same pairs (`other`) and the cosines and sines
+// of the 8 pairs' angles.  Half 0 holds the first components x_r and half 1 the second
+// x_{r + d/2} (rotate-half): x'_r = x_r cos - x_{r+d/2} sin and
+// x'_{r+d/2} = x_{r+d/2} cos + x_r sin, in fp32, rounded to bf16.
 __device__ __forceinline__ u32x4_t rope_rotate_cs(u32x4_t own, u32x4_t other, int hh,
                                                   const float* cs8, const float* sn8) {
     const float sgn = hh ? 1.f : -1.f;
@@ -164,6 +154,20 @@ __device__ __forceinline__ u32x4_t rope_rotate_cs(u32x4_t own, u32x4_t other, in
         r[t] = __builtin_bit_cast(uint32_t, two);
     }
     return r;
+}
+
+// The same for a vector at position pos, its angles evaluated directly
+// (v_cos_f32 / v_sin_f32 take their argument in revolutions).
+__device__ __forceinline__ u32x4_t rope_rotate(u32x4_t own, u32x4_t other, int hh, uint32_t pos,
+                                               const uint32_t* rho_hi8, const uint32_t* rho_lo8) {
+    float cs8[8], sn8[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const float u = rope_revolutions(pos, make_uint2(rho_hi8[e], rho_lo8[e]));
+        cs8[e] = __builtin_amdgcn_cosf(u);
+        sn8[e] = __builtin_amdgcn_sinf(u);
+    }
+    return rope_rotate_cs(own, other, hh, cs8, sn8);
 }
 
 // The other half of a fragment: lane l gets the registers of lane l ^ 32 (the same
