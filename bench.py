@@ -37,6 +37,9 @@ import torch  # noqa: E402
 METRIC = ("prefill ms + effective TFLOP/s vs full-window at 32K-128K; decode GB/s at 1M")
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# dense v_mfma_f32_32x32x16_bf16 throughput measured on the device (back-to-back MFMAs on
+# every SIMD; the clock drops below its 2.4 GHz peak under this load)
+MEASURED_MFMA_BF16_TFLOPS = 2240.0
 
 
 def parse():
@@ -503,6 +506,8 @@ def main():
         "ms_max": round(max(pre_ms), 3),
         "effective_tflops": round(flops_prefill / (pre_med * 1e-3) / 1e12, 1),
         "frac_bf16_peak": round(flops_prefill / (pre_med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "frac_measured_mfma_peak": round(
+            flops_prefill / (pre_med * 1e-3) / 1e12 / MEASURED_MFMA_BF16_TFLOPS, 4),
         "retained_terms_per_head": T, "causal_cells_per_head": C,
         "qk_pruned": round(1 - T / (C * d / 2), 4),
         "ceiling_2_over_1_plus_s": round(flops_prefill_full / flops_prefill, 4),
