@@ -160,7 +160,27 @@ def _median_ms(fn, stream, warm, iters):
     return statistics.median(a.elapsed_time(b) for a, b in evs)
 
 
-def config_table(atf, W, dev, stream):
+# configurations the fp64 oracle also runs in full (every row) on the host cores, timed
+# beside the GPU (the larger ones only through the headline's sampled cpu_baseline)
+ORACLE_FULL = ("qwen05b_prefill_1k", "qwen05b_prefill_8k", "llama3b_decode_32k",
+               "llama3b_decode_128k")
+
+
+def oracle_full(wl, q, k, v, theta):
+    """Wall time of the oracle over every row of workload wl (host tensors), on the host
+    cores; the CPU leg of a configuration's line."""
+    import oracle
+    avail = len(os.sched_getaffinity(0))
+    cores = min(avail, int(os.environ.get("OMP_NUM_THREADS") or avail))
+    widths = oracle.window_widths(wl.head_dim, wl.rope_base, wl.k, theta,
+                                  n_ctx=wl.q_pos0 + wl.n_q)
+    t = time.perf_counter()
+    oracle.attend(q, k, v, wl.q_pos0, widths, threads=cores)
+    return {"seconds": round(time.perf_counter() - t, 3), "cores": cores, "kind": "oracle",
+            "sample": "every (row, head), fp64, OpenMP over rows"}
+
+
+def config_table(atf, W, dev, stream, with_oracle=True):
     """ms, effective TFLOP/s (prefill) or GB/s (decode), fraction of the roofline and
     speedup over the same kernel at k = +inf for each of the other configurations.
     Llama tables: the effective-frequency window (default) and, as a second row,
@@ -177,6 +197,9 @@ def config_table(atf, W, dev, stream):
         vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
                          device=dev)
         atf.atf_pack_vcache(inp["v"], vp)
+        host = None
+        if with_oracle and name in ORACLE_FULL:
+            host = (inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu())
         del inp["k"], inp["v"]
         o = torch.empty_like(inp["q"])
         lse = torch.empty((wl.batch, wl.h_q, wl.n_q), dtype=torch.float32, device=dev)
@@ -201,6 +224,10 @@ def config_table(atf, W, dev, stream):
                 "frac_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
                 "full_window_ms": round(t_off, 4), "speedup_vs_full_window": round(t_off / t, 4),
                 "qk_pruned": round(1 - T / (C * d / 2), 4)}
+        if host is not None:
+            cpu = oracle_full(wl, *host, tables[""])
+            cpu["gpu_speedup"] = round(cpu["seconds"] * 1e3 / out[name]["ms"], 1)
+            out[name]["oracle"] = cpu
         del inp, kp, vp, o, lse
         torch.cuda.empty_cache()
     for name in DECODE_CONFIGS:
@@ -218,6 +245,9 @@ def config_table(atf, W, dev, stream):
             atf.atf_pack_kcache(inp["k"], kp)
             atf.atf_pack_vcache(inp["v"], vp)
             sets.append((kp, vp))
+        host = None
+        if with_oracle and name in ORACLE_FULL:
+            host = (inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu())
         del inp["k"], inp["v"]
         qd = inp["q"][:, 0].contiguous()
         od = torch.empty_like(qd)
@@ -249,6 +279,10 @@ def config_table(atf, W, dev, stream):
                 "ms": round(t, 4), "GBps": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
                 "algorithmic_bytes": nbytes, "full_window_ms": round(t_off, 4),
                 "speedup_vs_full_window": round(t_off / t, 4), "cache_sets": nset}
+        if host is not None:
+            cpu = oracle_full(wl, *host, tables[""])
+            cpu["gpu_speedup"] = round(cpu["seconds"] * 1e3 / out[name]["ms"], 1)
+            out[name]["oracle"] = cpu
         del sets, qd, od, lsed, ws
         torch.cuda.empty_cache()
     out.update(ragged_decode_config(atf, W, dev, stream))
@@ -584,7 +618,8 @@ def main():
         cpu = cpu_baseline(inp, pf, args.cpu_rows)
     del inp, q, k, v, kp, vp, o, lse
     torch.cuda.empty_cache()
-    configs = None if args.no_configs else config_table(atf, W, dev, stream)
+    configs = None if args.no_configs else config_table(atf, W, dev, stream,
+                                                        not args.no_cpu_baseline)
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
