@@ -348,7 +348,10 @@ def ragged_decode_config(atf, W, dev, stream):
     kpool = torch.empty(atf.kpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
     vpool = torch.empty(atf.vpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=dev)
     inp = W.make_inputs(wl, device=dev)
-    atf.atf_cache_append_paged(inp["k"], inp["v"], kpool, vpool, btd, 0, stream=stream)
+    for b, c in enumerate(counts):  # each row writes only its own pages
+        atf.atf_cache_append_paged(inp["k"][b:b + 1, :c * pt].contiguous(),
+                                   inp["v"][b:b + 1, :c * pt].contiguous(), kpool, vpool,
+                                   btd[b:b + 1], 0, stream=stream)
     del inp
     runp = lambda w: atf.atf_decode_paged(qd, kpool, vpool, od, lsed, btd, rows, rows, wl.n_k, w, ws,
                                           stream=stream)

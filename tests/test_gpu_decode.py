@@ -535,3 +535,45 @@ def test_decode_paged_rows(case):
         _, widths = windows_for(d, base, kwin, None, n_ctx=qp + 1)
         o_ref, lse_ref, _ = oracle.attend(q[b:b + 1], kc[b:b + 1, :nk], vc[b:b + 1, :nk], qp, widths)
         compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"paged row {b}")
+
+
+def test_decode_paged_llama_128k_bench_layout():
+    """The benchmark's paged batch at full size: Llama-3.2-3B-shaped rows of 131072 ..
+    4096 keys in 128-token pages, each row's pages shuffled in one pool and written row by
+    row with atf_cache_append_paged.  Equal bits with atf_decode_ragged on contiguous
+    caches, and the longest and the shortest row against the oracle."""
+    import paper_2608_02947_amd as atf
+    wl = W.WORKLOADS["llama3b_decode_128k"]
+    d, B, pt = wl.head_dim, wl.batch, 128
+    rows_l = [131072, 98304, 65536, 32768, 16384, 8192, 120000, 4096]
+    note("decode paged llama 128K, benchmark layout")
+    inp = W.make_inputs(wl, device=DEV)
+    counts = [-(-n // pt) for n in rows_l]
+    perm = np.random.default_rng(20260099).permutation(sum(counts))
+    bt = np.full((B, wl.n_k // pt), -1, dtype=np.int32)
+    at = 0
+    for b, c in enumerate(counts):
+        bt[b, :c] = perm[at:at + c]
+        at += c
+    btd = torch.from_numpy(bt).to(DEV)
+    kpool = torch.empty(atf.kpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=DEV)
+    vpool = torch.empty(atf.vpages_shape(sum(counts), pt, wl.h_kv, d), dtype=torch.bfloat16, device=DEV)
+    for b, c in enumerate(counts):
+        atf.atf_cache_append_paged(inp["k"][b:b + 1, :c * pt].contiguous(),
+                                   inp["v"][b:b + 1, :c * pt].contiguous(), kpool, vpool,
+                                   btd[b:b + 1], 0)
+    th = W.workload_theta(wl)
+    win, _ = windows_for(d, wl.rope_base, wl.k, th, n_ctx=wl.n_k + 1)
+    qd = inp["q"][:, 0].contiguous()
+    o, lse = _gpu_decode_paged(qd, kpool, vpool, btd, rows_l, rows_l, wl.n_k, win)
+    del kpool, vpool
+    o_c, lse_c = _gpu_decode_ragged(qd, inp["k"], inp["v"], rows_l, rows_l, wl.n_k, win)
+    assert torch.equal(o, o_c) and torch.equal(lse, lse_c)
+    o, lse = to_f64(o), to_f64(lse)
+    for b in (0, 7):
+        nk = rows_l[b]
+        _, widths = windows_for(d, wl.rope_base, wl.k, th, n_ctx=nk + 1)
+        q = inp["q"][b:b + 1].cpu()
+        o_ref, lse_ref, _ = oracle.attend(q, inp["k"][b:b + 1, :nk].cpu(), inp["v"][b:b + 1, :nk].cpu(),
+                                          nk, widths)
+        compare(o[b:b + 1], lse[b:b + 1], o_ref[:, 0], lse_ref[:, :, 0], f"paged bench row {b}")
