@@ -320,7 +320,8 @@ int atf_decode_paged(const void *q, const void *k_pages, const void *v_pages, vo
  * position (theta_r / (2 pi) held as a 0.64 fixed-point fraction).
  *   rope_inv_freq  host double [d/2] of the rotation's theta_r, or NULL: the window's
  *                  frequencies (w->inv_freq if set, else rope_base^(-2r/d))
- * Everything else is atf_decode (atf_decode_unrotated) or atf_decode_paged
+ * Everything else is atf_decode (atf_decode_unrotated), atf_decode_ragged
+ * (atf_decode_ragged_unrotated: row b's key t at position t) or atf_decode_paged
  * (atf_decode_paged_unrotated): same layouts, window, workspace, errors, plus
  * ATF_EINVAL for a rotation frequency that is negative, infinite or NaN.  V is never
  * rotated.  Deterministic: equal inputs give equal bits. */
@@ -329,6 +330,12 @@ int atf_decode_unrotated(const void *q, const void *k_cache, const void *v_cache
                          int32_t h_kv, int64_t cache_tokens, const atf_window *w,
                          const double *rope_inv_freq, float softmax_scale, void *workspace,
                          size_t workspace_bytes, void *hip_stream);
+int atf_decode_ragged_unrotated(const void *q, const void *k_cache, const void *v_cache, void *o,
+                                float *lse, int32_t batch, const int32_t *n_k_rows,
+                                const int32_t *q_pos_rows, int64_t max_n_k, int32_t h_q,
+                                int32_t h_kv, int64_t cache_tokens, const atf_window *w,
+                                const double *rope_inv_freq, float softmax_scale,
+                                void *workspace, size_t workspace_bytes, void *hip_stream);
 int atf_decode_paged_unrotated(const void *q, const void *k_pages, const void *v_pages, void *o,
                                float *lse, int32_t batch, const int32_t *block_table,
                                int32_t max_pages_per_row, int32_t num_pages, int32_t page_tokens,

@@ -82,6 +82,8 @@ def _load():
                                             i32, W, f32, P, ctypes.c_size_t, P]),
         "atf_decode_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, P,
                                                 f32, P, ctypes.c_size_t, P]),
+        "atf_decode_ragged_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, P, P, i64, i32, i32, i64,
+                                                       W, P, f32, P, ctypes.c_size_t, P]),
         "atf_decode_paged_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, P, i32, i32, i32, P, P,
                                                       i64, i32, i32, W, P, f32, P, ctypes.c_size_t,
                                                       P]),
@@ -98,7 +100,8 @@ _lib = _load()
 EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
             "atf_decode_workspace_bytes", "atf_decode", "atf_decode_ragged", "atf_cache_append_paged",
-            "atf_decode_paged", "atf_decode_unrotated", "atf_decode_paged_unrotated", "atf_last_error")
+            "atf_decode_paged", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
+            "atf_decode_paged_unrotated", "atf_last_error")
 
 
 def library():
@@ -456,6 +459,33 @@ def atf_decode_paged(q, k_pages, v_pages, o, lse, block_table, n_k_rows, q_pos_r
         block_table.shape[1], num_pages, pt, _dev_ptr(n_k_rows, torch.int32, "n_k_rows"),
         _dev_ptr(q_pos_rows, torch.int32, "q_pos_rows"), int(max_n_k), h_q, h_kv,
         ctypes.byref(cw), float(softmax_scale), _dev_ptr(workspace, torch.uint8, "workspace"),
+        workspace.numel(), _stream_ptr(stream))
+    _check(rc)
+
+
+def atf_decode_ragged_unrotated(q, k_pcm, v_pack, o, lse, n_k_rows, q_pos_rows, max_n_k: int,
+                                window: Window, workspace, softmax_scale: float = 0.0,
+                                stream=None, rope_inv_freq=None):
+    """atf_decode_ragged with q and the K cache UNROTATED (row b's key t at position t,
+    its query at q_pos_rows[b]); rope_inv_freq as atf_decode_unrotated."""
+    torch = _torch()
+    B, h_q, d = q.shape
+    if k_pcm.dim() != 5:
+        raise ValueError("atf_decode_ragged_unrotated: k_pcm must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_pcm.shape
+    if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
+            tuple(k_pcm.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_pack.shape) != vcache_shape(B, cap, h_kv, d) or \
+            tuple(n_k_rows.shape) != (B,) or tuple(q_pos_rows.shape) != (B,):
+        raise ValueError("atf_decode_ragged_unrotated: inconsistent shapes")
+    cw, keep = window.as_c()
+    fp, keep2 = _rope_freq(rope_inv_freq, d)
+    rc = _lib.atf_decode_ragged_unrotated(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_pcm, torch.bfloat16, "k"),
+        _dev_ptr(v_pack, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+        _dev_ptr(lse, torch.float32, "lse"), B, _dev_ptr(n_k_rows, torch.int32, "n_k_rows"),
+        _dev_ptr(q_pos_rows, torch.int32, "q_pos_rows"), int(max_n_k), h_q, h_kv, cap,
+        ctypes.byref(cw), fp, float(softmax_scale), _dev_ptr(workspace, torch.uint8, "workspace"),
         workspace.numel(), _stream_ptr(stream))
     _check(rc)
 

@@ -636,6 +636,22 @@ int atf_decode_unrotated(const void* q, const void* k_cache, const void* v_cache
                        workspace_bytes, hip_stream, PagedArgs(), rope);
 }
 
+int atf_decode_ragged_unrotated(const void* q, const void* k_cache, const void* v_cache, void* o,
+                                float* lse, int32_t batch, const int32_t* n_k_rows,
+                                const int32_t* q_pos_rows, int64_t max_n_k, int32_t h_q,
+                                int32_t h_kv, int64_t cache_tokens, const atf_window* w,
+                                const double* rope_inv_freq, float softmax_scale,
+                                void* workspace, size_t workspace_bytes, void* hip_stream) {
+    if (!n_k_rows || !q_pos_rows)
+        return fail(ATF_EINVAL, "decode_ragged_unrotated: NULL row-length or row-position array");
+    RopeArgs rope;
+    rope.rotate = true;
+    rope.inv_freq = rope_inv_freq;
+    return decode_impl("decode_ragged_unrotated", q, k_cache, v_cache, o, lse, batch, max_n_k, 0,
+                       n_k_rows, q_pos_rows, h_q, h_kv, cache_tokens, w, softmax_scale, workspace,
+                       workspace_bytes, hip_stream, PagedArgs(), rope);
+}
+
 int atf_decode_ragged(const void* q, const void* k_cache, const void* v_cache, void* o, float* lse,
                       int32_t batch, const int32_t* n_k_rows, const int32_t* q_pos_rows,
                       int64_t max_n_k, int32_t h_q, int32_t h_kv, int64_t cache_tokens,

@@ -402,6 +402,15 @@ def test_unrotated_validation_before_launch():
                                               1 << 14, 256, 24, 8, ctypes.byref(w), freq(f), 0.0,
                                               16, 16, None)
 
+    def ragged(f=None):
+        return lib.atf_decode_ragged_unrotated(16, 16, 16, 16, 16, 2, 1 << 13, 1 << 14, 1000, 8,
+                                               2, 1000, ctypes.byref(w), freq(f), 0.0, 16, 16,
+                                               None)
+
+    assert ragged(good) == atf.ATF_EWORKSPACE
+    bad = list(good)
+    bad[0] = -2.0
+    assert ragged(bad) == atf.ATF_EINVAL and "decode_ragged_unrotated" in atf.atf_last_error()
     assert dec() == atf.ATF_EWORKSPACE               # the window's frequencies
     assert dec(good) == atf.ATF_EWORKSPACE
     assert paged(good) == atf.ATF_EWORKSPACE

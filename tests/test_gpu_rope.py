@@ -1,7 +1,8 @@
 """GPU parity of decode from UNROTATED caches (RoPE applied at read time, App. B)
 through the C ABI: atf_decode_unrotated and atf_decode_paged_unrotated against the
 oracle, which rotates the same bf16 query and keys in fp64 (oracle.rope_rotate, pinned
-in test_oracle_rope.py) and attends the rotated vectors exactly."""
+in test_oracle_rope.py), stores them in bf16 as a pre-rotated cache would, and attends
+them in fp64."""
 import math
 
 import numpy as np
@@ -29,10 +30,12 @@ def _inputs(B, n_k, h_q, h_kv, d, seed):
 
 
 def _oracle(q, k, v, q_pos, theta, widths):
-    """Rotate in fp64 (query at q_pos, key j at j), then windowed attention."""
-    qr = oracle.rope_rotate(q, [q_pos], theta)
-    kr = oracle.rope_rotate(k, np.arange(k.shape[1]), theta)
-    o, lse, _ = oracle.attend(qr, kr, v.to(torch.float64).numpy(), q_pos, widths)
+    """Rotate in fp64 (query at q_pos, key j at j), store the rotated vectors in bf16
+    (round to nearest even) as a pre-rotated cache would hold them, then windowed
+    attention: the result an unrotated cache read with RoPE at read time must give."""
+    qr = torch.from_numpy(oracle.rope_rotate(q, [q_pos], theta)).to(torch.bfloat16)
+    kr = torch.from_numpy(oracle.rope_rotate(k, np.arange(k.shape[1]), theta)).to(torch.bfloat16)
+    o, lse, _ = oracle.attend(qr, kr, v, q_pos, widths)
     return o[:, 0], lse[:, :, 0]
 
 
@@ -166,3 +169,34 @@ def test_decode_unrotated_qwen7b1m_every_head():
     o, lse = _gpu(q, k, v, wl.q_pos0, win)
     o_ref, lse_ref = _oracle(q, k, v, wl.q_pos0, W.rope_theta(d, wl.rope_base).numpy(), widths)
     compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "unrotated qwen7b1m")
+
+
+def test_decode_ragged_unrotated():
+    """Ragged batch from unrotated contiguous caches: row b's key t at position t, its
+    query at q_pos_rows[b] (inside, at and past its cache end; an empty row)."""
+    import paper_2608_02947_amd as atf
+    n_ks, q_poss = [3000, 1, 1200, 0, 2500], [3000, 1, 1900, 0, 2000]
+    B, h_q, h_kv, d, base, cap = 5, 8, 2, 128, 1e4, 3000
+    q, k, v = _inputs(B, cap, h_q, h_kv, d, seed=91)
+    note("decode ragged unrotated")
+    win, _ = windows_for(d, base, 2.0, None, n_ctx=max(q_poss) + 1)
+    qd = q[:, 0].contiguous().to(DEV)
+    kp, vp = pack_kcache(k.to(DEV)), pack_vcache(v.to(DEV))
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, cap, d), dtype=torch.uint8,
+                     device=DEV)
+    o = torch.empty_like(qd)
+    lse = torch.empty((B, h_q), dtype=torch.float32, device=DEV)
+    atf.atf_decode_ragged_unrotated(qd, kp, vp, o, lse,
+                                    torch.tensor(n_ks, dtype=torch.int32, device=DEV),
+                                    torch.tensor(q_poss, dtype=torch.int32, device=DEV), cap, win, ws)
+    torch.cuda.synchronize()
+    o, lse = to_f64(o), to_f64(lse)
+    th = W.rope_theta(d, base).numpy()
+    for b, (nk, qp) in enumerate(zip(n_ks, q_poss)):
+        if nk == 0:
+            assert np.all(o[b] == 0.0) and np.all(lse[b] == -np.inf)
+            continue
+        n_used = min(nk, qp + 1)
+        _, widths = windows_for(d, base, 2.0, None, n_ctx=qp + 1)
+        o_ref, lse_ref = _oracle(q[b:b + 1], k[b:b + 1, :n_used], v[b:b + 1, :n_used], qp, th, widths)
+        compare(o[b:b + 1], lse[b:b + 1], o_ref, lse_ref, f"ragged unrotated row {b}")
