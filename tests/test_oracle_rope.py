@@ -85,3 +85,66 @@ def test_rope_bf16_input_is_its_exact_value():
     y1 = oracle.rope_rotate(x, [0, 9, 4000], th)
     y2 = oracle.rope_rotate(x.to(torch.float64).numpy(), [0, 9, 4000], th)
     assert np.array_equal(y1, y2)
+
+
+# ---------------------------------------------------------------------------
+# planted mistakes: each plausible slip in a rotation routine fails at least one of
+# the checks above (written again here against a rotation passed in)
+# ---------------------------------------------------------------------------
+def _rot_variant(kind):
+    def rot(x, positions, theta):
+        x = np.asarray(x, dtype=np.float64)
+        d = x.shape[-1]
+        h = d // 2
+        pos = np.asarray(positions, dtype=np.float64)
+        th = np.asarray(theta, dtype=np.float64)
+        if kind == "position_off_by_one":
+            pos = pos + 1
+        if kind == "theta_reversed":
+            th = th[::-1]
+        ang = pos[:, None] * th[None, :]
+        c, s_ = np.cos(ang)[:, None, :], np.sin(ang)[:, None, :]
+        if kind == "interleaved_pairs":
+            a, b = x[..., 0::2], x[..., 1::2]
+        else:
+            a, b = x[..., :h], x[..., h:]
+        sgn = -1.0 if kind == "sine_sign" else 1.0
+        first = a * c - sgn * b * s_
+        second = b * c + sgn * a * s_
+        if kind == "cos_sin_swapped":
+            first, second = a * s_ - b * c, b * s_ + a * c
+        out = np.empty_like(x)
+        if kind == "interleaved_pairs":
+            out[..., 0::2], out[..., 1::2] = first, second
+        else:
+            out[..., :h], out[..., h:] = first, second
+        return out
+    return rot
+
+
+def _passes_pins(rot):
+    d = 16
+    th = _theta(d, 1e4)
+    x = _x((2, 7, 3, d), 1)
+    pos = np.array([0, 1, 5, 100, 4097, 131071, 1048575])
+    y = rot(x, pos, th)
+    z = (x[..., : d // 2] + 1j * x[..., d // 2:]) * np.exp(1j * pos[:, None] * th)[None, :, None, :]
+    if np.abs(y[..., : d // 2] - z.real).max() > 1e-12 or np.abs(y[..., d // 2:] - z.imag).max() > 1e-12:
+        return False
+    hand = rot(np.array([[[1.0, 0.0]]] * 4)[None], np.arange(4), np.array([math.pi / 2]))
+    if np.abs(hand[0, :, 0, :] - np.array([[1, 0], [0, 1], [-1, 0], [0, -1]])).max() > 1e-15:
+        return False
+    if not np.array_equal(rot(x, np.zeros(7), th), x):
+        return False
+    return True
+
+
+def test_pins_accept_the_oracle():
+    assert _passes_pins(oracle.rope_rotate)
+    assert _passes_pins(_rot_variant("none"))
+
+
+@pytest.mark.parametrize("kind", ["sine_sign", "interleaved_pairs", "position_off_by_one",
+                                  "theta_reversed", "cos_sin_swapped"])
+def test_pins_reject_planted_mistake(kind):
+    assert not _passes_pins(_rot_variant(kind))
