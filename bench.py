@@ -55,8 +55,6 @@ def parse():
                     help="skip the per-configuration table (the other workloads)")
     ap.add_argument("--no-family", action="store_true",
                     help="skip the other windows (variable-k profile, uniform k=64, rounded slice)")
-    ap.add_argument("--cpu-rows", type=int, default=512,
-                    help="(row, head) pairs of the prefill chunk the oracle recomputes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for scaling rocprof byte counters)")
     ap.add_argument("--profile-workload", default=None,
@@ -136,6 +134,37 @@ DECODE_CONFIGS = ["llama3b_decode_32k", "llama3b_decode_128k"]
 FAMILY_CONFIGS = ("qwen05b_prefill_32k", "llama3b_prefill_128k", "llama3b_decode_128k")
 
 
+FAMILY_TAGS = ("var16to2", "k64", "rounded8")
+
+
+def timed_tables():
+    """{workload: [window tags]} of every call this benchmark times; the GPU parity tests
+    check each entry at the same size (tests/parity.py BENCH_TABLE_TESTS)."""
+    import workloads as W
+    t = {"qwen7b1m_prefill_chunk": ["default", "kinf", *FAMILY_TAGS],
+         "qwen7b1m_decode": ["default", "kinf", *FAMILY_TAGS, "unrotated", "unrotated_kinf"]}
+    for name in PREFILL_CONFIGS + DECODE_CONFIGS:
+        tags = ["default", "kinf"]
+        if W.WORKLOADS[name].llama3:
+            tags.append("raw_base")
+        if name in FAMILY_CONFIGS:
+            tags += list(FAMILY_TAGS)
+        t[name] = tags
+    t["llama3b_decode_128k"] += ["ragged", "ragged_kinf", "paged", "paged_kinf"]
+    return t
+
+
+def sample_rows(wl, widths):
+    """The stratified (b, hq, i) sample of a full-size prefill that the oracle times here
+    and the GPU parity tests check: >= 256 rows over all heads (workloads.stratified_rows),
+    with the prefill workgroup's position tiles floor(rows / G) (rows = 256 at d = 128;
+    128 for the windowed and 256 for the window-off kernel at d = 64)."""
+    import workloads as W
+    G = wl.group
+    tiles = (256 // G,) if wl.head_dim == 128 else (128 // G, 256 // G)
+    return W.stratified_rows(wl.batch, wl.n_q, wl.h_q, wl.q_pos0, G, tiles, widths, seed=wl.seed)
+
+
 def family_windows(atf, d, base, theta, k=2.0):
     """Windows timed beside the default one: two members of the window family of
     App. A, and the default window with the rounded slice of Sec. 3.3 (8-pair steps)."""
@@ -160,24 +189,51 @@ def _median_ms(fn, stream, warm, iters):
     return statistics.median(a.elapsed_time(b) for a, b in evs)
 
 
-# configurations the fp64 oracle also runs in full (every row) on the host cores, timed
-# beside the GPU (the larger ones only through the headline's sampled cpu_baseline)
+# configurations the fp64 oracle runs in full (every row) on the host cores, timed beside
+# the GPU; the others it runs on the stratified row sample and the time is extrapolated
 ORACLE_FULL = ("qwen05b_prefill_1k", "qwen05b_prefill_8k", "llama3b_decode_32k",
                "llama3b_decode_128k")
+ORACLE_SAMPLED = ("qwen05b_prefill_32k", "llama3b_prefill_32k", "llama3b_prefill_128k")
+
+
+def host_cores():
+    avail = len(os.sched_getaffinity(0))
+    return min(avail, int(os.environ.get("OMP_NUM_THREADS") or avail))
 
 
 def oracle_full(wl, q, k, v, theta):
     """Wall time of the oracle over every row of workload wl (host tensors), on the host
     cores; the CPU leg of a configuration's line."""
     import oracle
-    avail = len(os.sched_getaffinity(0))
-    cores = min(avail, int(os.environ.get("OMP_NUM_THREADS") or avail))
+    cores = host_cores()
     widths = oracle.window_widths(wl.head_dim, wl.rope_base, wl.k, theta,
                                   n_ctx=wl.q_pos0 + wl.n_q)
     t = time.perf_counter()
     oracle.attend(q, k, v, wl.q_pos0, widths, threads=cores)
     return {"seconds": round(time.perf_counter() - t, 3), "cores": cores, "kind": "oracle",
             "sample": "every (row, head), fp64, OpenMP over rows"}
+
+
+def oracle_sampled(wl, q, k, v, theta):
+    """The oracle on the stratified row sample of workload wl (the GPU parity sample),
+    timed on the host cores; the whole workload's time extrapolated by causal cells
+    (the oracle's work per row is proportional to the keys it visits)."""
+    import oracle
+    cores = host_cores()
+    widths = oracle.window_widths(wl.head_dim, wl.rope_base, wl.k, theta,
+                                  n_ctx=wl.q_pos0 + wl.n_q)
+    rows = sample_rows(wl, widths)
+    t = time.perf_counter()
+    oracle.attend(q, k, v, wl.q_pos0, widths, rows=rows, threads=cores)
+    dt = time.perf_counter() - t
+    pos = wl.q_pos0 + np.arange(wl.n_q, dtype=np.float64)
+    cells_all = wl.batch * wl.h_q * float(np.sum(np.minimum(pos, wl.n_k - 1) + 1))
+    cells_sample = float(np.sum(np.minimum(wl.q_pos0 + rows[:, 2], wl.n_k - 1) + 1))
+    return {"seconds_extrapolated": round(dt * cells_all / cells_sample, 1),
+            "label": "extrapolated", "sample_seconds": round(dt, 3),
+            "sample_rows": int(len(rows)), "cores": cores, "kind": "oracle",
+            "sample": f"{len(rows)} stratified (row, head) pairs over all heads, fp64, OpenMP "
+                      "over rows; extrapolated to every row by causal-cell count"}
 
 
 def config_table(atf, W, dev, stream, with_oracle=True):
@@ -198,7 +254,7 @@ def config_table(atf, W, dev, stream, with_oracle=True):
                          device=dev)
         atf.atf_pack_vcache(inp["v"], vp)
         host = None
-        if with_oracle and name in ORACLE_FULL:
+        if with_oracle and (name in ORACLE_FULL or name in ORACLE_SAMPLED):
             host = (inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu())
         del inp["k"], inp["v"]
         o = torch.empty_like(inp["q"])
@@ -225,10 +281,15 @@ def config_table(atf, W, dev, stream, with_oracle=True):
                 "full_window_ms": round(t_off, 4), "speedup_vs_full_window": round(t_off / t, 4),
                 "qk_pruned": round(1 - T / (C * d / 2), 4)}
         if host is not None:
-            cpu = oracle_full(wl, *host, tables[""])
-            cpu["gpu_speedup"] = round(cpu["seconds"] * 1e3 / out[name]["ms"], 1)
+            if name in ORACLE_FULL:
+                cpu = oracle_full(wl, *host, tables[""])
+                cpu["gpu_speedup"] = round(cpu["seconds"] * 1e3 / out[name]["ms"], 1)
+            else:
+                cpu = oracle_sampled(wl, *host, tables[""])
+                cpu["gpu_speedup_extrapolated"] = round(
+                    cpu["seconds_extrapolated"] * 1e3 / out[name]["ms"], 1)
             out[name]["oracle"] = cpu
-        del inp, kp, vp, o, lse
+        del inp, kp, vp, o, lse, host
         torch.cuda.empty_cache()
     for name in DECODE_CONFIGS:
         wl = W.WORKLOADS[name]
@@ -618,7 +679,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(inp, pf, args.cpu_rows)
+        cpu = cpu_baseline(inp, pf, qd, dc, dec_med)
     del inp, q, k, v, kp, vp, o, lse
     torch.cuda.empty_cache()
     configs = None if args.no_configs else config_table(atf, W, dev, stream,
@@ -653,26 +714,32 @@ def cpu_model() -> str:
     return platform.machine()
 
 
-def cpu_baseline(inp, pf, n_rows):
-    """The fp64 oracle on a bounded sample of the same prefill chunk, on the host cores."""
+def cpu_baseline(inp, pf, qd, dc, decode_ms):
+    """The fp64 oracle on the host cores: the stratified row sample of the same prefill
+    chunk (the rows the GPU parity test checks; the headline leg, in the metric's unit),
+    and the whole decode at 1M (every head)."""
     import oracle
-    avail = len(os.sched_getaffinity(0))
-    cores = min(avail, int(os.environ.get("OMP_NUM_THREADS") or avail))
-    rng = np.random.default_rng(pf.seed)
-    rows = np.stack([np.zeros(n_rows, dtype=np.int64),
-                     rng.integers(0, pf.h_q, n_rows),
-                     rng.integers(0, pf.n_q, n_rows)], axis=1).astype(np.int64)
+    cores = host_cores()
     qc, kc, vc = inp["q"].cpu(), inp["k"].cpu(), inp["v"].cpu()
     widths = oracle.window_widths(pf.head_dim, pf.rope_base, pf.k, n_ctx=pf.n_k)
+    rows = sample_rows(pf, widths)
     t = time.perf_counter()
     _, _, terms = oracle.attend(qc, kc, vc, pf.q_pos0, widths, rows=rows, threads=cores)
     dt = time.perf_counter() - t
     causal = np.minimum(pf.q_pos0 + rows[:, 2], pf.n_k - 1) + 1
     flops = float(np.sum(4.0 * terms.astype(np.float64) + 2.0 * pf.head_dim * causal))
+    widths_d = oracle.window_widths(dc.head_dim, dc.rope_base, dc.k, n_ctx=dc.q_pos0 + 1)
+    td = time.perf_counter()
+    oracle.attend(qd.cpu()[:, None], kc, vc, dc.q_pos0, widths_d, threads=cores)
+    td = time.perf_counter() - td
     return {"value": float(f"{flops / dt / 1e12:.6g}"), "unit": "TFLOP/s", "cores": cores,
             "kind": "oracle", "seconds": round(dt, 2), "cpu": cpu_model(),
-            "sample": f"{n_rows} random (query row, head) pairs of the 131072-row chunk, "
-                      f"each over its ~1M causal keys, fp64, OpenMP over rows"}
+            "sample": f"{len(rows)} stratified (query row, head) pairs of the 131072-row chunk "
+                      "over all heads (the GPU parity sample), each over its ~1M causal keys, "
+                      "fp64, OpenMP over rows",
+            "decode_1m_full": {"seconds": round(td, 3), "cores": cores,
+                               "sample": "every head of the decode at 1,048,576, fp64",
+                               "gpu_speedup": round(td * 1e3 / decode_ms, 1)}}
 
 
 if __name__ == "__main__":

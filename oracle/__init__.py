@@ -54,11 +54,14 @@ _lib = None
 
 
 def _load():
+    """Load liboracle.so, or the library named by ORACLE_LIB (the mutation test of the
+    pins loads deliberately broken builds of oracle.c this way)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
+        path = os.environ.get("ORACLE_LIB") or _LIB_PATH
+        if path == _LIB_PATH and not os.path.exists(_LIB_PATH):
             build(force=False)
-        lib = ctypes.CDLL(_LIB_PATH)
+        lib = ctypes.CDLL(path)
         p = ctypes.c_void_p
         i64 = ctypes.c_int64
         dbl = ctypes.c_double

@@ -157,15 +157,17 @@ def test_decode_paged_unrotated():
         compare(o[b:b + 1], lse[b:b + 1], o_ref, lse_ref, f"paged unrotated row {b}")
 
 
-def test_decode_unrotated_qwen7b1m_every_head():
+@pytest.mark.parametrize("kwin", [2.0, math.inf], ids=["default", "kinf"])
+def test_decode_unrotated_qwen7b1m_every_head(kwin):
     """The benchmark's 1M decode shape (28 query heads / 4 KV heads, d = 128, base 1e7,
-    k = 2, query at 1,048,576 over keys 0 .. 1,048,575) from unrotated caches: every
-    head against the oracle's fp64 rotation and attention."""
+    query at 1,048,576 over keys 0 .. 1,048,575) from unrotated caches, at k = 2 and with
+    the window off (both timed): every head against the oracle's fp64 rotation and
+    attention."""
     wl = W.WORKLOADS["qwen7b1m_decode"]
     d = wl.head_dim
-    note("decode unrotated qwen7b1m, every head")
+    note(f"decode unrotated qwen7b1m, every head, k={kwin}")
     q, k, v = _inputs(wl.batch, wl.n_k, wl.h_q, wl.h_kv, d, seed=wl.seed + 101)
-    win, widths = windows_for(d, wl.rope_base, wl.k, None, n_ctx=wl.q_pos0 + 1)
+    win, widths = windows_for(d, wl.rope_base, kwin, None, n_ctx=wl.q_pos0 + 1)
     o, lse = _gpu(q, k, v, wl.q_pos0, win)
     o_ref, lse_ref = _oracle(q, k, v, wl.q_pos0, W.rope_theta(d, wl.rope_base).numpy(), widths)
     compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "unrotated qwen7b1m")

@@ -193,3 +193,72 @@ def random_bf16(shape, seed: int, device="cpu", scale: float = 1.0) -> torch.Ten
     g = _gen(seed, device)
     return (torch.randn(shape, generator=g, device=device, dtype=torch.float32) * scale).to(
         torch.bfloat16)
+
+
+def stratified_rows(batch: int, n_q: int, h_q: int, q_pos0: int, group: int, pos_tiles,
+                    widths, seed: int, n_random: int = 64, wave_rows: int = 32,
+                    n_threshold_pairs: int = 24):
+    """A stratified sample of (b, hq, i) query rows of a prefill, over all query heads,
+    for checking full-size outputs row by row.  Returns an int64 array [n, 3] of
+    (batch, query head, query row), sorted, without repeats.
+
+    Strata (positions are q_pos0 + i; a workgroup of the prefill packs
+    P = pos_tiles[k] consecutive positions x the `group` heads of one KV head into
+    rows f -> (position f // group, head f % group), in blocks of `wave_rows` rows):
+      - the first and the last 64 query rows, the head advancing by one per row, so
+        that every head appears at both ends;
+      - the first and the last row of 8 randomly chosen position tiles, for every
+        tile size in pos_tiles;
+      - the rows on either side of each seam between two `wave_rows`-row blocks
+        (f = wave_rows*w - 1 and wave_rows*w) of 3 randomly chosen tiles per tile size;
+      - for up to n_threshold_pairs pairs r whose width W_r = floor(widths[r]) is below
+        the largest distance: positions p at which the first key the pair still
+        reaches, p - W_r, is the first or last key of a 32-key block or of a 64-key
+        tile (residues 0, 31, 32, 63 mod 64), two residues per pair;
+      - n_random seeded random rows.
+    This module holds no arithmetic of the method: `widths` and `pos_tiles` are inputs.
+    """
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    picks = set()
+
+    def add(i, h=None, b=None):
+        if 0 <= i < n_q:
+            picks.add((int(rng.integers(0, batch)) if b is None else int(b),
+                       int(rng.integers(0, h_q)) if h is None else int(h) % h_q, int(i)))
+
+    for t in range(min(64, n_q)):
+        add(t, h=t)
+        add(n_q - 1 - t, h=t)
+    for P in pos_tiles:
+        P = int(P)
+        n_tiles = (n_q + P - 1) // P
+        for t in rng.integers(0, n_tiles, size=8):
+            add(int(t) * P)
+            add(min(n_q, int(t) * P + P) - 1)
+        rows = P * group
+        n_kv = max(1, h_q // group)
+        for t in rng.integers(0, n_tiles, size=3):
+            g = int(rng.integers(0, n_kv))
+            for w in range(1, (rows + wave_rows - 1) // wave_rows):
+                for f in (wave_rows * w - 1, wave_rows * w):
+                    if f < rows:
+                        add(int(t) * P + f // group, h=g * group + f % group)
+    w = np.asarray(widths, dtype=np.float64)
+    p_lo, p_hi = q_pos0, q_pos0 + n_q - 1
+    cand = [r for r in range(w.shape[0]) if np.isfinite(w[r]) and np.floor(w[r]) + 1 <= p_hi]
+    if len(cand) > n_threshold_pairs:
+        cand = sorted(rng.choice(cand, size=n_threshold_pairs, replace=False).tolist())
+    for r in cand:
+        W_r = int(np.floor(w[r]))
+        lo = max(p_lo, W_r + 1)
+        for res in rng.choice([0, 31, 32, 63], size=2, replace=False):
+            p0 = int(rng.integers(lo, p_hi + 1))
+            p = p0 - ((p0 - W_r - int(res)) % 64)
+            if p < lo:
+                p += 64
+            if p <= p_hi:
+                add(p - q_pos0)
+    for i in rng.integers(0, n_q, size=n_random):
+        add(int(i))
+    return np.array(sorted(picks), dtype=np.int64).reshape(-1, 3)
