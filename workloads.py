@@ -197,7 +197,7 @@ def random_bf16(shape, seed: int, device="cpu", scale: float = 1.0) -> torch.Ten
 
 def stratified_rows(batch: int, n_q: int, h_q: int, q_pos0: int, group: int, pos_tiles,
                     widths, seed: int, n_random: int = 64, wave_rows: int = 32,
-                    n_threshold_pairs: int = 24):
+                    n_threshold_pairs: int = 24, min_rows: int = 256):
     """A stratified sample of (b, hq, i) query rows of a prefill, over all query heads,
     for checking full-size outputs row by row.  Returns an int64 array [n, 3] of
     (batch, query head, query row), sorted, without repeats.
@@ -215,7 +215,7 @@ def stratified_rows(batch: int, n_q: int, h_q: int, q_pos0: int, group: int, pos
         the largest distance: positions p at which the first key the pair still
         reaches, p - W_r, is the first or last key of a 32-key block or of a 64-key
         tile (residues 0, 31, 32, 63 mod 64), two residues per pair;
-      - n_random seeded random rows.
+      - n_random seeded random rows, and more until there are at least min_rows.
     This module holds no arithmetic of the method: `widths` and `pos_tiles` are inputs.
     """
     import numpy as np
@@ -259,6 +259,7 @@ def stratified_rows(batch: int, n_q: int, h_q: int, q_pos0: int, group: int, pos
                 p += 64
             if p <= p_hi:
                 add(p - q_pos0)
-    for i in rng.integers(0, n_q, size=n_random):
-        add(int(i))
+    target = max(min_rows, len(picks) + n_random) if n_q * h_q * batch >= min_rows else 0
+    while len(picks) < target:
+        add(int(rng.integers(0, n_q)))
     return np.array(sorted(picks), dtype=np.int64).reshape(-1, 3)
