@@ -237,6 +237,32 @@ int atf_decode(const void *q, const void *k_cache, const void *v_cache, void *o,
                int64_t cache_tokens, const atf_window *w, float softmax_scale,
                void *workspace, size_t workspace_bytes, void *hip_stream);
 
+/* Size in bytes of the library's own decode scratch array (atf_decode_noalloc). */
+#define ATF_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+
+/* atf_decode without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, allocation-free serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, layouts, window, kernels and
+ * results as atf_decode, bit for bit; the split partial states go to a
+ * file-scope device array of ATF_DECODE_NOALLOC_SCRATCH_BYTES (16 MiB) inside the
+ * library instead of a caller workspace.  The call allocates nothing (no
+ * hipMalloc, hipFree or allocating library routine); the first call on a device
+ * resolves that device's copy of the array.
+ * Limit: the partial states of these sizes, atf_decode_workspace_bytes(batch,
+ * h_q, h_kv, n_k, head_dim) for the uniform plan (about batch * splits * h_q *
+ * (4 head_dim + 8) bytes; 3.7 MB for 28 query heads / 4 KV heads, d = 128, at 1M
+ * keys), must fit in the array, else ATF_EWORKSPACE and nothing is launched.
+ * Sharing: every device holds its own copy for the life of the process, and all
+ * calls on one device share it and leave their partial states in it, so two
+ * calls that may run at the same time on one device (different streams, host
+ * threads) race: serialise them.  Nothing needs to be cleared between calls.
+ * Errors: as atf_decode (ATF_EWORKSPACE only for the limit above; ATF_EHIP also
+ * when the array's address cannot be resolved). */
+int atf_decode_noalloc(const void *q, const void *k_cache, const void *v_cache, void *o,
+                       float *lse, int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q,
+                       int32_t h_kv, int64_t cache_tokens, const atf_window *w,
+                       float softmax_scale, void *hip_stream);
+
 /* Decode of a ragged batch: row b holds one query token at position q_pos_rows[b]
  * against keys 0 .. min(q_pos_rows[b], n_k_rows[b] - 1) of its own cache entry
  * (Sec. 5: the last query row of each sequence, for a batch of sequences of

@@ -15,6 +15,7 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_pack_vcache`, :func:`atf_vcache_bytes` -- V-cache layout.
 - :func:`atf_cache_append` -- write new tokens into both caches at a position.
 - :func:`atf_decode_workspace_bytes`, :func:`atf_decode` -- split-KV decode.
+- :func:`atf_decode_noalloc` -- the same without a workspace (library scratch array).
 - :func:`atf_decode_ragged` -- the same for a batch of sequences of different lengths.
 - :func:`atf_cache_append_paged`, :func:`atf_decode_paged` -- paged caches (block tables).
 """
@@ -74,6 +75,8 @@ def _load():
         "atf_decode_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i64, i32]),
         "atf_decode": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, f32, P,
                                       ctypes.c_size_t, P]),
+        "atf_decode_noalloc": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, f32,
+                                              P]),
         "atf_decode_ragged": (ctypes.c_int, [P, P, P, P, P, i32, P, P, i64, i32, i32, i64, W, f32,
                                              P, ctypes.c_size_t, P]),
         "atf_cache_append_paged": (ctypes.c_int, [P, P, P, P, P, i32, i32, i32, i32, i64, i64,
@@ -99,7 +102,8 @@ def _load():
 _lib = _load()
 EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf_prefill", "atf_kcache_chunk_pairs",
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
-            "atf_decode_workspace_bytes", "atf_decode", "atf_decode_ragged", "atf_cache_append_paged",
+            "atf_decode_workspace_bytes", "atf_decode", "atf_decode_noalloc", "atf_decode_ragged",
+            "atf_cache_append_paged",
             "atf_decode_paged", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
             "atf_decode_paged_unrotated", "atf_last_error")
 
@@ -332,6 +336,34 @@ def atf_decode(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window, workspace,
                          ctypes.byref(cw), float(softmax_scale),
                          _dev_ptr(workspace, torch.uint8, "workspace"), workspace.numel(),
                          _stream_ptr(stream))
+    _check(rc)
+
+
+# Size of the library's decode scratch array (ATF_DECODE_NOALLOC_SCRATCH_BYTES)
+DECODE_NOALLOC_SCRATCH_BYTES = 16 << 20
+
+
+def atf_decode_noalloc(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window,
+                       softmax_scale: float = 0.0, stream=None, n_k: Optional[int] = None):
+    """atf_decode without a workspace: the split partials go to the library's own
+    device scratch array (no allocation; calls on one device must not overlap)."""
+    torch = _torch()
+    B, h_q, d = q.shape
+    if k_pcm.dim() != 5:
+        raise ValueError("atf_decode_noalloc: k_pcm must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_pcm.shape
+    n_k = cap if n_k is None else int(n_k)
+    if tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q) or \
+            tuple(k_pcm.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_pack.shape) != vcache_shape(B, cap, h_kv, d):
+        raise ValueError("atf_decode_noalloc: inconsistent shapes")
+    cw, keep = window.as_c()
+    rc = _lib.atf_decode_noalloc(_dev_ptr(q, torch.bfloat16, "q"),
+                                 _dev_ptr(k_pcm, torch.bfloat16, "k"),
+                                 _dev_ptr(v_pack, torch.bfloat16, "v"),
+                                 _dev_ptr(o, torch.bfloat16, "o"),
+                                 _dev_ptr(lse, torch.float32, "lse"), B, n_k, q_pos, h_q, h_kv,
+                                 cap, ctypes.byref(cw), float(softmax_scale), _stream_ptr(stream))
     _check(rc)
 
 

@@ -623,6 +623,33 @@ int atf_decode(const void* q, const void* k_cache, const void* v_cache, void* o,
                        hip_stream);
 }
 
+int atf_decode_noalloc(const void* q, const void* k_cache, const void* v_cache, void* o,
+                       float* lse, int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q,
+                       int32_t h_kv, int64_t cache_tokens, const atf_window* w,
+                       float softmax_scale, void* hip_stream) {
+    static_assert(atf::kNoAllocScratchBytes == ATF_DECODE_NOALLOC_SCRATCH_BYTES,
+                  "scratch size of the header and of the library differ");
+    if (w == nullptr) return fail(ATF_EINVAL, "decode_noalloc: NULL window");
+    const int d = w->head_dim;
+    if (batch >= 1 && h_q >= 1 && h_kv >= 1 && h_q % h_kv == 0 && n_k >= 1 && n_k < kPosLimit &&
+        (d == 64 || d == 128)) {
+        const size_t need = uniform_layout(batch, h_q, h_kv, n_k, d).total;
+        if (need > atf::kNoAllocScratchBytes)
+            return fail(ATF_EWORKSPACE,
+                        "decode_noalloc: these sizes need %zu bytes of partial states, above the "
+                        "%zu-byte scratch array (use atf_decode with a workspace)",
+                        need, atf::kNoAllocScratchBytes);
+    }
+    void* ws = nullptr;
+    const hipError_t e = atf::noalloc_scratch(&ws);
+    if (e != hipSuccess)
+        return fail(ATF_EHIP, "decode_noalloc: scratch address: %s", hipGetErrorString(e));
+    // every other argument is checked as atf_decode checks it
+    return decode_impl("decode_noalloc", q, k_cache, v_cache, o, lse, batch, n_k, q_pos, nullptr,
+                       nullptr, h_q, h_kv, cache_tokens, w, softmax_scale, ws,
+                       atf::kNoAllocScratchBytes, hip_stream);
+}
+
 int atf_decode_unrotated(const void* q, const void* k_cache, const void* v_cache, void* o,
                          float* lse, int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q,
                          int32_t h_kv, int64_t cache_tokens, const atf_window* w,

@@ -109,5 +109,11 @@ constexpr int32_t kDecodeTokenStep = 128;
 constexpr int32_t kDecodeMaxSplits = 4096;
 // Query heads one decode workgroup handles at most (columns of its MFMA tiles).
 constexpr int32_t kDecodeMaxHeads = 32;
+// Size of the library's own decode scratch array (decode.hip), the workspace of
+// atf_decode_noalloc; equal to ATF_DECODE_NOALLOC_SCRATCH_BYTES of atf.h.
+constexpr size_t kNoAllocScratchBytes = size_t(16) << 20;
+// Device address of that array on the current device, resolved once per device
+// (hipGetSymbolAddress) and kept for the life of the process.
+hipError_t noalloc_scratch(void** out);
 
 }  // namespace atf

@@ -38,6 +38,8 @@
 // rotated.
 #include "atf_internal.hpp"
 
+#include <mutex>
+
 namespace atf {
 namespace {
 
@@ -701,6 +703,38 @@ hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream
         return hipErrorInvalidValue;
     (void)hipGetLastError();
     return head_dim == 64 ? launch_decode_d<64>(p, stream) : launch_decode_d<128>(p, stream);
+}
+
+// The decode workspace of atf_decode_noalloc: a file-scope device array, so that
+// callers that cannot allocate (graph capture, allocation-free serving loops) need
+// no workspace.  Every device the library runs on holds its own copy for the life
+// of the process; calls on one device share it (the last call's partial states stay
+// in it), so such calls must not overlap.  In host code `scratch` names a host-side
+// stand-in, never the device memory: its device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxScratchDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_addr[dev] == nullptr) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (ptr == nullptr) return hipErrorInvalidSymbol;
+        g_scratch_addr[dev] = ptr;
+    }
+    *out = g_scratch_addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream) {

@@ -306,6 +306,20 @@ def test_decode_validation_before_launch():
     assert call(ws_bytes=need, cache_tokens=131071) == atf.ATF_EINVAL   # below n_k
 
 
+def test_decode_noalloc_validation_before_launch():
+    """atf_decode_noalloc: sizes whose partial states exceed the library's scratch array
+    fail with ATF_EWORKSPACE, and a NULL window with ATF_EINVAL, before any device call
+    (the pointers below are not device memory)."""
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    assert atf.atf_decode_workspace_bytes(64, 64, 1, 4096, 128) > atf.DECODE_NOALLOC_SCRATCH_BYTES
+    rc = lib.atf_decode_noalloc(16, 16, 16, 16, 16, 64, 4096, 4096, 64, 1, 0, ctypes.byref(w),
+                                0.0, None)
+    assert rc == atf.ATF_EWORKSPACE and "scratch" in atf.atf_last_error()
+    rc = lib.atf_decode_noalloc(16, 16, 16, 16, 16, 1, 4096, 4096, 28, 4, 0, None, 0.0, None)
+    assert rc == atf.ATF_EINVAL
+
+
 def test_decode_ragged_validation_before_launch():
     """Every call below fails validation, so nothing is launched (the pointers are
     placeholders)."""
