@@ -37,9 +37,10 @@ import torch  # noqa: E402
 METRIC = ("prefill ms + effective TFLOP/s vs full-window at 32K-128K; decode GB/s at 1M")
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-# dense v_mfma_f32_32x32x16_bf16 throughput measured on the device (back-to-back MFMAs on
-# every SIMD; the clock drops below its 2.4 GHz peak under this load)
-MEASURED_MFMA_BF16_TFLOPS = 2240.0
+# dense v_mfma_f32_32x32x16_bf16 throughput measured on the device by `bench.py --peaks`
+# (back-to-back MFMAs on one wave per SIMD; the clock drops below its 2.4 GHz peak under
+# this load); a reference figure beside the published peak, which the roofline uses
+MEASURED_MFMA_BF16_TFLOPS = 1965.9
 
 
 def parse():
@@ -55,6 +56,9 @@ def parse():
                     help="skip the per-configuration table (the other workloads)")
     ap.add_argument("--no-family", action="store_true",
                     help="skip the other windows (variable-k profile, uniform k=64, rounded slice)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="only time the device-limit microbenchmarks (libatf_peaks.so): dense "
+                         "bf16 MFMA, v_exp_f32 and HBM read rates")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for scaling rocprof byte counters)")
     ap.add_argument("--profile-workload", default=None,
@@ -113,6 +117,67 @@ def profile_driver(name, iters, kinf, raw_base=False):
     torch.cuda.synchronize()
     print(json.dumps({"profile_workload": name, "k": "inf" if kinf else wl.k,
                       "ms": [round(a.elapsed_time(b), 4) for a, b in ms]}))
+
+
+def measure_peaks():
+    """Dense bf16 MFMA rate (back-to-back v_mfma_f32_32x32x16_bf16 on 1, 2 and 4 waves per SIMD),
+    v_exp_f32 rate (16 independent chains per thread) and HBM read rate (16-byte loads
+    streaming an 8 GiB buffer, and a torch device copy), timed with HIP events on the
+    current stream; the median of 5 launches after one warm-up."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2608_02947_amd", "libatf_peaks.so"))
+    P, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.atf_probe_mfma_bf16.argtypes = [P, i32, i32, P]
+    lib.atf_probe_exp2.argtypes = [P, i32, i32, P]
+    lib.atf_probe_read.argtypes = [P, i64, P, i32, P]
+    stream = torch.cuda.current_stream()
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    blocks = 1024  # 4096 waves: four per SIMD on 256 CUs
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        fn()
+        evs = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            rc = fn()
+            b.record(stream)
+            assert rc in (0, None), rc
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return statistics.median(a.elapsed_time(b) for a, b in evs) * 1e-3
+
+    it_m = 2000
+    mfma = {}
+    for waves_per_simd in (1, 2, 4):
+        nb = 256 * waves_per_simd
+        t = timed(lambda: lib.atf_probe_mfma_bf16(ctypes.c_void_p(out.data_ptr()), nb, it_m, sp))
+        mfma[waves_per_simd] = nb * 4 * 4 * it_m * 32768 / t / 1e12
+    mfma_tflops = max(mfma.values())
+    it_e = 20000
+    t = timed(lambda: lib.atf_probe_exp2(ctypes.c_void_p(out.data_ptr()), blocks, it_e, sp))
+    exps = blocks * 256 * 16 * it_e / t
+    nbytes = 8 << 30
+    src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    words = torch.empty(2048 * 256, dtype=torch.int32, device="cuda")
+    t = timed(lambda: lib.atf_probe_read(ctypes.c_void_p(src.data_ptr()), nbytes,
+                                         ctypes.c_void_p(words.data_ptr()), 2048, sp))
+    read_gbs = nbytes / t / 1e9
+    dst = torch.empty_like(src)
+
+    def copy_once():
+        dst.copy_(src)
+    t = timed(copy_once)
+    copy_gbs = 2 * nbytes / t / 1e9
+    print(json.dumps({"peaks": {
+        "mfma_bf16_dense_tflops": round(mfma_tflops, 1),
+        "mfma_bf16_dense_tflops_by_waves_per_simd": {str(k): round(v, 1) for k, v in mfma.items()},
+        "frac_of_2500": round(mfma_tflops / PEAK_BF16_TFLOPS, 4),
+        "v_exp_f32_per_s": float(f"{exps:.4g}"),
+        "v_exp_f32_lanes_per_clk_per_simd_at_2.4GHz": round(exps / (1024 * 2.4e9), 2),
+        "hbm_read_GBps": round(read_gbs, 1), "hbm_copy_read_plus_write_GBps": round(copy_gbs, 1),
+        "frac_read_of_8000": round(read_gbs / PEAK_HBM_GBS, 4)}}))
 
 
 def copy_calibration():
@@ -437,17 +502,17 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "7f4f3aef15ba0eb37498f40aed6fd6fde372a1853507dbb463b69fcb58555832",
-        "fetch_kib": 79575533.38, "write_kib": 933439.03,
+        "sha256": "82e58e8625b1914b9ae8e75c7e7127195874328eb333d3e0bdd24982f0f554f2",
+        "fetch_kib": 79575541.13, "write_kib": 933440.66,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "895b78f8b7c1e164a18ea4ae64115d473c3bbef87cca27e3969ae9fdc0652657",
-        "fetch_kib": 737786.08, "write_kib": 4058.24,
+        "sha256": "c7e0b6301f7df87c1625e7a5745c39fb73abb1d041a8afa89517312e1078ca6f",
+        "fetch_kib": 737787.13, "write_kib": 4060.30,
     },
 }
-COPY_CALIBRATION_KIB = {"fetch": 524299.5, "write": 1048576.0}  # counters for a 1 GiB copy
+COPY_CALIBRATION_KIB = {"fetch": 524302.04, "write": 1048576.0}  # counters for a 1 GiB copy
 
 
 def recorded_traffic(kernel):
@@ -475,6 +540,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.peaks:
+        measure_peaks()
         return
     if args.profile_workload:
         profile_driver(args.profile_workload, args.profile_iters, args.profile_kinf,
