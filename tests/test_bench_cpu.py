@@ -21,7 +21,9 @@ def test_recorded_traffic_scaling_and_source_check(monkeypatch):
     KiB); a record whose sources no longer hash to its sha256 gives None."""
     src = "paper_2608_02947_amd/csrc/atf_internal.hpp"
     h = hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest()
-    fake = {"k": {"sources": [src], "sha256": h, "fetch_kib": 524299.5 * 3, "write_kib": 1048576.0}}
+    cal = bench.COPY_CALIBRATION_KIB
+    fake = {"k": {"sources": [src], "sha256": h, "fetch_kib": cal["fetch"] * 3,
+                  "write_kib": cal["write"]}}
     monkeypatch.setattr(bench, "TRAFFIC_RECORDS", fake)
     t = bench.recorded_traffic("k")
     assert t["fetch_bytes"] == 3 << 30 and t["write_bytes"] == 1 << 30
