@@ -30,7 +30,9 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libatf.so")
+# ATF_LIB names another build of the same library (the sanitizer test of the host code
+# loads one built with AddressSanitizer this way); by default the in-package libatf.so
+LIB_PATH = os.environ.get("ATF_LIB") or os.path.join(_HERE, "libatf.so")
 
 ATF_OK = 0
 ATF_EINVAL = -1
