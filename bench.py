@@ -129,6 +129,7 @@ def measure_peaks():
     P, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
     lib.atf_probe_mfma_bf16.argtypes = [P, i32, i32, P]
     lib.atf_probe_exp2.argtypes = [P, i32, i32, P]
+    lib.atf_probe_mfma_bf16_k8.argtypes = [P, i32, i32, P]
     lib.atf_probe_read.argtypes = [P, i64, P, i32, P]
     stream = torch.cuda.current_stream()
     sp = ctypes.c_void_p(stream.cuda_stream)
@@ -155,6 +156,10 @@ def measure_peaks():
         t = timed(lambda: lib.atf_probe_mfma_bf16(ctypes.c_void_p(out.data_ptr()), nb, it_m, sp))
         mfma[waves_per_simd] = nb * 4 * 4 * it_m * 32768 / t / 1e12
     mfma_tflops = max(mfma.values())
+    # the 16-deep MFMA (4 rotary pairs per K-step) on one wave per SIMD: time per
+    # instruction relative to the 32-deep one
+    t8 = timed(lambda: lib.atf_probe_mfma_bf16_k8(ctypes.c_void_p(out.data_ptr()), 256, it_m, sp))
+    t16 = timed(lambda: lib.atf_probe_mfma_bf16(ctypes.c_void_p(out.data_ptr()), 256, it_m, sp))
     it_e = 20000
     t = timed(lambda: lib.atf_probe_exp2(ctypes.c_void_p(out.data_ptr()), blocks, it_e, sp))
     exps = blocks * 256 * 16 * it_e / t
@@ -173,6 +178,7 @@ def measure_peaks():
     print(json.dumps({"peaks": {
         "mfma_bf16_dense_tflops": round(mfma_tflops, 1),
         "mfma_bf16_dense_tflops_by_waves_per_simd": {str(k): round(v, 1) for k, v in mfma.items()},
+        "mfma_32x32x8_time_per_instr_vs_32x32x16": round(t8 / t16, 3),
         "frac_of_2500": round(mfma_tflops / PEAK_BF16_TFLOPS, 4),
         "v_exp_f32_per_s": float(f"{exps:.4g}"),
         "v_exp_f32_lanes_per_clk_per_simd_at_2.4GHz": round(exps / (1024 * 2.4e9), 2),

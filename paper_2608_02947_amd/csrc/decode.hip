@@ -199,6 +199,9 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     // 32 columns' reads fall in different banks.
     constexpr int kCStride = 2 * kHalf + 4;
     __shared__ __attribute__((aligned(16))) float s_colcs[kRot ? 32 * kCStride : 1];
+    // per wave: (cos, sin) of the current block's t0 * theta_r for every pair r, written by
+    // lane r and read back by all lanes (broadcast reads of the chunk's 8 pairs)
+    __shared__ __attribute__((aligned(16))) float s_blkcs[kRot ? kWaves * 2 * kHalf : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -314,23 +317,34 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             // the keys at their positions t0 + col, rotated here: only the kept chunks
             // are read, so only their pairs are rotated (both lanes of a pair hold the
             // same token).  Angle of (t0 + col, r) by angle addition: lane r evaluates
-            // the block's t0 * theta_r once, every lane reads col * theta_r from LDS.
+            // the block's t0 * theta_r once and leaves its cosine and sine in the wave's
+            // LDS row; every lane reads those of its chunk's 8 pairs and col * theta_r from LDS.
             const float ub = rope_revolutions(uint32_t(t0), my_rho);
-            const float cb = __builtin_amdgcn_cosf(ub), sb = __builtin_amdgcn_sinf(ub);
+            float* blk = &s_blkcs[wave * 2 * kHalf];
+            if (lane < kHalf) {
+                blk[2 * lane] = __builtin_amdgcn_cosf(ub);
+                blk[2 * lane + 1] = __builtin_amdgcn_sinf(ub);
+            }
+            // the wave's own LDS writes complete before its later LDS reads; the fence keeps
+            // the compiler from moving the reads above the writes
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
             for (int c = 0; c < kChunks; ++c) {
                 const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
                 if (kept) {
                     const float* row = &s_colcs[col * kCStride + 16 * c];
+                    const float* brow = blk + 16 * c;
                     float cs8[8], sn8[8];
 #pragma unroll
                     for (int q4 = 0; q4 < 4; ++q4) {
                         const float4 v = *reinterpret_cast<const float4*>(row + 4 * q4);  // pairs 2q4, 2q4+1
+                        const float4 w = *reinterpret_cast<const float4*>(brow + 4 * q4);
 #pragma unroll
                         for (int j = 0; j < 2; ++j) {
                             const int e = 2 * q4 + j;
-                            const float cB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cb), 8 * c + e));
-                            const float sB = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sb), 8 * c + e));
+                            const float cB = j ? w.z : w.x, sB = j ? w.w : w.y;
                             const float cC = j ? v.z : v.x, sC = j ? v.w : v.y;
                             cs8[e] = __builtin_fmaf(cB, cC, -sB * sC);
                             sn8[e] = __builtin_fmaf(sB, cC, cB * sC);

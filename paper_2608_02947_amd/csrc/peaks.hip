@@ -33,6 +33,27 @@ __global__ __launch_bounds__(256) void mfma_loop(float* out, int iters, float se
     out[blockIdx.x * blockDim.x + threadIdx.x] = r;
 }
 
+// The same with v_mfma_f32_32x32x8_bf16 (half the depth, 16384 flops): what a K-step
+// of 4 rotary pairs would cost against the 8-pair step above.
+__global__ __launch_bounds__(256) void mfma8_loop(float* out, int iters, float seed) {
+    typedef short s16x4_t __attribute__((ext_vector_type(4)));
+    s16x4_t a, b;
+    for (int i = 0; i < 4; ++i) {
+        a[i] = short(threadIdx.x + i);
+        b[i] = short(i + 1) + short(seed);
+    }
+    f32x16_t c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    for (int it = 0; it < iters; ++it) {
+        c0 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, b, c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, b, c1, 0, 0, 0);
+        c2 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, b, c2, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x8bf16_1k(a, b, c3, 0, 0, 0);
+    }
+    float r = 0.f;
+    for (int i = 0; i < 16; ++i) r += c0[i] + c1[i] + c2[i] + c3[i];
+    out[blockIdx.x * blockDim.x + threadIdx.x] = r;
+}
+
 // v_exp_f32 on 16 independent chains per thread (throughput, not latency, bound).
 __global__ __launch_bounds__(256) void exp_loop(float* out, int iters, float seed) {
     float x[16];
@@ -71,6 +92,14 @@ int atf_probe_mfma_bf16(float* out, int blocks, int iters, void* stream) {
     if (out == nullptr || blocks < 1 || iters < 1) return -1;
     hipLaunchKernelGGL(mfma_loop, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream), out,
                        iters, 0.001f);
+    return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+// MFMA 32x32x8 (16384 flops each), as atf_probe_mfma_bf16.
+int atf_probe_mfma_bf16_k8(float* out, int blocks, int iters, void* stream) {
+    if (out == nullptr || blocks < 1 || iters < 1) return -1;
+    hipLaunchKernelGGL(mfma8_loop, dim3(blocks), dim3(256), 0, static_cast<hipStream_t>(stream),
+                       out, iters, 0.001f);
     return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
