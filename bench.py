@@ -514,8 +514,8 @@ TRAFFIC_RECORDS = {
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "c7e0b6301f7df87c1625e7a5745c39fb73abb1d041a8afa89517312e1078ca6f",
-        "fetch_kib": 737787.13, "write_kib": 4060.30,
+        "sha256": "6cb6444d1238a6a4e718635259d094499ba103d4dcc8b93a02c9cbd716db53fb",
+        "fetch_kib": 737792.92, "write_kib": 4057.19,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.04, "write": 1048576.0}  # counters for a 1 GiB copy
