@@ -237,6 +237,12 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
         t_end = min(n_valid, t_begin + p.split_tokens);
         slot0 = (int64_t(b) * p.h_q + hq0) * p.splits + split;
     }
+    // the split's bounds are the same for every lane; saying so keeps the block loop's
+    // exit, and the window ballots carried from one block to the next, in scalar
+    // registers, so that each MFMA below is skipped by a scalar branch (an MFMA issued
+    // under an all-zero EXEC mask still accumulates)
+    t_begin = __builtin_amdgcn_readfirstlane(t_begin);
+    t_end = __builtin_amdgcn_readfirstlane(t_end);
     const int64_t cap = p.cache_tokens;  // stream length of the caches
     const uint16_t* kstream = p.kpcm + (int64_t(b) * p.h_kv + g) * kChunks * cap * 16;
     const uint16_t* vblocks = p.vpk + (int64_t(b) * p.h_kv + g) * ((cap + 15) / 16) * D * 16;
@@ -278,41 +284,118 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     float l_run = 0.f;
     const float sc = p.scale_log2;
 
-    for (int t0 = t_begin + 32 * wave; t0 < t_end; t0 += 32 * kWaves) {
-        const int t_last = min(t0 + 31, t_end - 1);
-        // where the block's 32 tokens live: the row's contiguous cache, or the page the
-        // block table names (a page holds a whole number of 32-token blocks)
-        const uint16_t* kb = kstream;   // chunk c of token t at kb + (c * kstride + t - tb) * 16
-        const uint16_t* vb = vblocks;   // 16-token block j at vb + (j - tb / 16) * D * 16
-        int64_t kstride = cap;
-        int tb = 0;
+    // a block's place in the caches (the row's contiguous cache, or the page the block
+    // table names; a page holds a whole number of 32-token blocks) and its window
+    // classification: `full` = pairs kept at every token of the block, `keep` = pairs
+    // kept at one or more
+    struct Blk {
+        const uint16_t* kb;  // chunk c of token t at kb + (c * kstride + t - tb) * 16
+        const uint16_t* vb;  // 16-token block j at vb + (j - tb / 16) * D * 16
+        int64_t kstride;
+        int tb;
+        uint64_t full, keep;
+    };
+    auto locate = [&](int t0) {
+        Blk B = {kstream, vblocks, cap, 0, 0ull, 0ull};
         if (p.block_table != nullptr) {
             const int pt = p.page_tokens;
             const int page = min(max(p.block_table[int64_t(b) * p.max_pages + t0 / pt], 0),
                                  p.num_pages - 1);
-            kb = p.kpcm + (int64_t(page) * p.h_kv + g) * kChunks * int64_t(pt) * 16;
-            vb = p.vpk + (int64_t(page) * p.h_kv + g) * (pt / 16) * int64_t(D) * 16;
-            kstride = pt;
-            tb = t0 - t0 % pt;
+            B.kb = p.kpcm + (int64_t(page) * p.h_kv + g) * kChunks * int64_t(pt) * 16;
+            B.vb = p.vpk + (int64_t(page) * p.h_kv + g) * (pt / 16) * int64_t(D) * 16;
+            B.kstride = pt;
+            B.tb = t0 - t0 % pt;
         }
-        const int zhi = q_pos - t0;
-        const int zlo = max(0, q_pos - t_last);
-        const uint64_t full = __ballot(my_w >= zhi);
-        const uint64_t keep = __ballot(my_w >= zlo);
-
-        // K fragments of the kept chunks (A operand: token t0 + col, dims of half hh);
-        // the last chunk is always fetched because the first MFMA multiplies it
-        const int tok = t0 + col;
-        const bool tok_ok = tok < t_end;
-        u32x4_t kf[kChunks];
+        const int t_last = min(t0 + 31, t_end - 1);
+        B.full = __ballot(my_w >= q_pos - t0);
+        B.keep = __ballot(my_w >= max(0, q_pos - t_last));
+        return B;
+    };
+    // K fragments of the kept chunks (A operand: token t0 + col, dims of half hh); the
+    // last chunk is always fetched because the first MFMA multiplies it.
+    //
+    // With rotation at read time the next block's K is loaded while the current block is
+    // rotated, multiplied and accumulated (its registers are free once the block's QK
+    // products are issued), and the current block's V is loaded before its K is rotated.
+    // The waits then have to count the loads in flight, so that count must not depend on
+    // the window: a chunk no token of the block keeps re-reads the always-fetched last
+    // chunk (a cache hit; its fragment is never multiplied), and a token past the split's
+    // end reads the split's last token (its score is masked).  Without rotation the
+    // loads are few enough in time to be issued with the block's own V, and pruned
+    // chunks are not loaded at all.
+    u32x4_t kf[kChunks];
+    auto load_k = [&](const Blk& B, int t0) {
+        if constexpr (kRot) {
+            const int tok = min(t0 + col, t_end - 1);
+            const uint16_t* base = B.kb + (int64_t(tok) - B.tb) * 16 + 8 * hh;
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) {
-            u32x4_t z = {0u, 0u, 0u, 0u};
-            const bool kept = c == kChunks - 1 || ((keep >> (8 * c)) & 0xFFull) != 0;
-            if (kept && tok_ok)
-                z = *reinterpret_cast<const u32x4_t*>(kb + (int64_t(c) * kstride + tok - tb) * 16 + 8 * hh);
-            kf[c] = z;
+            for (int c = 0; c < kChunks; ++c) {
+                const bool kept = c == kChunks - 1 || ((B.keep >> (8 * c)) & 0xFFull) != 0;
+                kf[c] = *reinterpret_cast<const u32x4_t*>(base + int64_t(kept ? c : kChunks - 1) * B.kstride * 16);
+            }
+        } else {
+            const int tok = t0 + col;
+            const bool tok_ok = tok < t_end;
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                u32x4_t z = {0u, 0u, 0u, 0u};
+                const bool kept = c == kChunks - 1 || ((B.keep >> (8 * c)) & 0xFFull) != 0;
+                if (kept && tok_ok)
+                    z = *reinterpret_cast<const u32x4_t*>(B.kb + (int64_t(c) * B.kstride + tok - B.tb) * 16 + 8 * hh);
+                kf[c] = z;
+            }
         }
+    };
+
+    int t0 = t_begin + 32 * wave;
+    Blk B = {kstream, vblocks, cap, 0, 0ull, 0ull};
+    if constexpr (kRot) {
+        if (t0 < t_end) {
+            B = locate(t0);
+            load_k(B, t0);
+        }
+    }
+    for (; t0 < t_end; t0 += 32 * kWaves) {
+        if constexpr (!kRot) {
+            B = locate(t0);
+            load_k(B, t0);
+        }
+        const uint64_t full = B.full;
+        const uint64_t keep = B.keep;
+        const uint16_t* vb = B.vb;
+        const int tb = B.tb;
+
+        // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each
+        // 16-token group).  A block past n_k re-reads the last block holding keys and is
+        // zeroed (so that both blocks always issue their loads); in the block holding
+        // token n_k the slots of later tokens are zeroed (the cache past n_k need not
+        // hold finite values, and their probabilities are 0).
+        u32x4_t vf[2][kDB];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int blk = t0 / 16 + ks;
+            const int blk_rd = min(blk, (n_k - 1) / 16);
+#pragma unroll
+            for (int i = 0; i < kDB; ++i)
+                vf[ks][i] = *reinterpret_cast<const u32x4_t*>(vb + (int64_t(blk_rd - tb / 16) * D + 32 * i + col) * 16 + 8 * hh);
+            if (16 * blk >= n_k) {
+#pragma unroll
+                for (int i = 0; i < kDB; ++i) vf[ks][i] = u32x4_t{0u, 0u, 0u, 0u};
+            }
+            if (16 * blk < n_k && 16 * blk + 16 > n_k) {
+                const int lim = n_k - 16 * blk - 4 * hh;  // slot e valid iff 8(e/4) + e%4 < lim
+#pragma unroll
+                for (int i = 0; i < kDB; ++i)
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const int e0 = 2 * t, e1 = 2 * t + 1;
+                        const uint32_t m = (8 * (e0 / 4) + e0 % 4 < lim ? 0x0000FFFFu : 0u) |
+                                           (8 * (e1 / 4) + e1 % 4 < lim ? 0xFFFF0000u : 0u);
+                        vf[ks][i][t] &= m;
+                    }
+            }
+        }
+
         if constexpr (kRot) {
             // the keys at their positions t0 + col, rotated here: only the kept chunks
             // are read, so only their pairs are rotated (both lanes of a pair hold the
@@ -355,35 +438,6 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-        // V^T fragments (A operand: dim 32 i + col, 8 tokens of half hh of each
-        // 16-token group).  Blocks past n_k are not read; in the block holding
-        // token n_k the slots of later tokens are zeroed (the cache past n_k need
-        // not hold finite values, and their probabilities are 0).
-        u32x4_t vf[2][kDB];
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int blk = t0 / 16 + ks;
-#pragma unroll
-            for (int i = 0; i < kDB; ++i) {
-                u32x4_t z = {0u, 0u, 0u, 0u};
-                if (16 * blk < n_k)
-                    z = *reinterpret_cast<const u32x4_t*>(vb + (int64_t(blk - tb / 16) * D + 32 * i + col) * 16 + 8 * hh);
-                vf[ks][i] = z;
-            }
-            if (16 * blk < n_k && 16 * blk + 16 > n_k) {
-                const int lim = n_k - 16 * blk - 4 * hh;  // slot e valid iff 8(e/4) + e%4 < lim
-#pragma unroll
-                for (int i = 0; i < kDB; ++i)
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const int e0 = 2 * t, e1 = 2 * t + 1;
-                        const uint32_t m = (8 * (e0 / 4) + e0 % 4 < lim ? 0x0000FFFFu : 0u) |
-                                           (8 * (e1 / 4) + e1 % 4 < lim ? 0xFFFF0000u : 0u);
-                        vf[ks][i][t] &= m;
-                    }
-            }
-        }
-
         // QK (lowest frequencies first; one MFMA site per chunk)
         f32x16_t sacc;
 #pragma unroll
@@ -403,7 +457,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
         while (part) {
             const int r = __builtin_ctzll(part);
             const int c = r >> 3;
-            const int wr = p.win.W[r];
+            const int wr = __builtin_amdgcn_readlane(my_w, r);
             const uint64_t grp = __ballot(my_w == wr) & part & (0xFFull << (8 * c));
             part &= ~grp;
             u32x4_t kfc = kf[0], qfc = qf[0];
@@ -420,6 +474,13 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                 const int off = 8 * (v / 4) + (v % 4);
                 sacc[v] += off >= thr ? t[v] : 0.f;
             }
+        }
+        if constexpr (kRot) {
+            // the next block's K (past the split's last block the current block is loaded
+            // again, so that the loads in flight do not depend on the path)
+            const int tn = t0 + 32 * kWaves < t_end ? t0 + 32 * kWaves : t0;
+            B = locate(tn);
+            load_k(B, tn);
         }
         // tokens past the split's end
         if (t0 + 32 > t_end) {

@@ -1,10 +1,15 @@
-"""Checks on the gfx950 assembly of the prefill kernels (CPU: hipcc cross-compiles).
+"""Checks on the gfx950 assembly of the kernels (CPU: hipcc cross-compiles).
 
 The direct global->LDS loads of the prefill are inline assembly that set the M0
 register (the LDS destination) right before each load.  The compiler does not track
 that clobber of a reserved register, so the kernels are correct only while nothing
 else in them keeps a value in M0 across those loads: every instruction that names
-M0 must be one of the load sequences."""
+M0 must be one of the load sequences.
+
+The kernels skip the MFMAs of pruned chunks and pairs by wave-uniform branches.  An
+MFMA placed under an EXEC mask instead (a branch the compiler took for divergent)
+still accumulates when the mask is all zero, so no MFMA may follow an EXEC-mask
+write without a branch or a label in between."""
 import os
 import re
 import shutil
@@ -16,18 +21,25 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 
-@pytest.mark.skipif(not os.path.exists(HIPCC) and shutil.which("hipcc") is None,
-                    reason="needs hipcc")
-def test_prefill_m0_only_in_lds_load_sequences(tmp_path):
-    out = tmp_path / "prefill.s"
+needs_hipcc = pytest.mark.skipif(not os.path.exists(HIPCC) and shutil.which("hipcc") is None,
+                                 reason="needs hipcc")
+
+
+def _assembly(tmp_path, src):
+    out = tmp_path / (src + ".s")
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
            "-I", os.path.join(ROOT, "paper_2608_02947_amd", "csrc"), "-x", "hip",
-           "--cuda-device-only", "-S", os.path.join(ROOT, "paper_2608_02947_amd", "csrc", "prefill.hip"),
+           "--cuda-device-only", "-S", os.path.join(ROOT, "paper_2608_02947_amd", "csrc", src),
            "-o", str(out)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
-    lines = [ln.split(";")[0].strip() for ln in out.read_text().splitlines()]
+    return out.read_text()
+
+
+@needs_hipcc
+def test_prefill_m0_only_in_lds_load_sequences(tmp_path):
+    lines = [ln.split(";")[0].strip() for ln in _assembly(tmp_path, "prefill.hip").splitlines()]
     lines = [ln for ln in lines if ln and not ln.startswith(".")]
     n_seq = 0
     for i, ln in enumerate(lines):
@@ -39,3 +51,58 @@ def test_prefill_m0_only_in_lds_load_sequences(tmp_path):
             lines[i:i + 3]
         n_seq += 1
     assert n_seq > 0
+
+
+def _mfmas_under_exec_mask(asm):
+    """(kernel, line) of every MFMA whose nearest preceding control point is a write
+    of EXEC other than its restore at a join (s_or_b64 exec, exec, ...)."""
+    bad, n_mfma, kernel = [], 0, None
+    last = None  # the last control point: "label", "branch", "restore" or "mask"
+    for raw in asm.splitlines():
+        ln = raw.split(";")[0].strip()
+        if not ln:
+            continue
+        m = re.match(r"^(_Z\w+):$", ln)
+        if m:
+            kernel, last = m.group(1), "label"
+            continue
+        if ln.endswith(":"):
+            last = "label"
+        elif ln.startswith("s_cbranch") or ln.startswith("s_branch"):
+            last = "branch"
+        elif re.match(r"^s_or_b64\s+exec,\s*exec,", ln):
+            last = "restore"
+        elif re.match(r"^s_\w+_b64\s+exec,", ln) or re.match(r"^s_\w+_saveexec_b64\s", ln):
+            last = "mask"
+        elif ln.startswith("v_mfma"):
+            n_mfma += 1
+            if last == "mask":
+                bad.append((kernel, ln))
+    return bad, n_mfma
+
+
+@needs_hipcc
+@pytest.mark.parametrize("src", ["prefill.hip", "decode.hip"])
+def test_no_mfma_under_exec_mask(tmp_path, src):
+    bad, n_mfma = _mfmas_under_exec_mask(_assembly(tmp_path, src))
+    assert n_mfma > 0
+    assert not bad, bad[:5]
+
+
+def test_exec_mask_check_finds_a_masked_mfma():
+    """The check itself: a masked MFMA is found, a branched-around one is not."""
+    masked = """_Zk:
+\ts_and_saveexec_b64 s[4:5], vcc
+\tv_mfma_f32_32x32x16_bf16 v[0:15], v[16:19], v[20:23], v[0:15]
+\ts_or_b64 exec, exec, s[4:5]
+"""
+    branched = """_Zk:
+\ts_and_saveexec_b64 s[4:5], vcc
+\ts_cbranch_execz .LBB0_2
+\tv_mfma_f32_32x32x16_bf16 v[0:15], v[16:19], v[20:23], v[0:15]
+.LBB0_2:
+\ts_or_b64 exec, exec, s[4:5]
+\tv_mfma_f32_32x32x16_bf16 v[0:15], v[16:19], v[20:23], v[0:15]
+"""
+    assert len(_mfmas_under_exec_mask(masked)[0]) == 1
+    assert _mfmas_under_exec_mask(branched) == ([], 2)
