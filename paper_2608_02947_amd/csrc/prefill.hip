@@ -379,15 +379,20 @@ prefill_kernel(const PrefillParams p) {
     auto softmax_pv = [&](int tile) __attribute__((always_inline)) {
         const int j0 = tile * kBN;
         if (wp_min - (j0 + kBN - 1) < 0 || j0 + kBN > p.n_k) {
+            // cell kept iff off <= lim = min(distance base, last key - block start): the
+            // score goes through min(s, +inf) if kept, min(s, -inf) if not, the sign bit of
+            // lim - off choosing the infinity.  (Written with per-cell compares, the 32
+            // lane masks of a tile were all live at once and pushed the kernel's scalar
+            // registers into spills.)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 const int jb = j0 + 32 * kb;
-                const int kbound = p.n_k - jb - 4 * hh;
-                const int zbase = my_pos - jb - 4 * hh;
+                const int lim = min(my_pos - jb, p.n_k - 1 - jb) - 4 * hh;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int off = 8 * (v / 4) + (v % 4);
-                    if (off > zbase || off >= kbound) sacc[kb][v] = -INFINITY;
+                    const uint32_t inf = (uint32_t(lim - off) & 0x80000000u) | 0x7F800000u;
+                    sacc[kb][v] = fminf(sacc[kb][v], __uint_as_float(inf));
                 }
             }
         }

@@ -106,3 +106,34 @@ def test_exec_mask_check_finds_a_masked_mfma():
 """
     assert len(_mfmas_under_exec_mask(masked)[0]) == 1
     assert _mfmas_under_exec_mask(branched) == ([], 2)
+
+
+@needs_hipcc
+@pytest.mark.parametrize("src", ["prefill.hip", "decode.hip"])
+def test_kernels_do_not_spill(tmp_path, src):
+    """No kernel spills vector registers to scratch, and scalar spills (into vector
+    register lanes, a v_writelane/v_readlane pair each) stay a handful: a mask or
+    loop that keeps many lane masks live at once shows up here first."""
+    out = tmp_path / (src + ".o")
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
+           "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
+           "-I", os.path.join(ROOT, "paper_2608_02947_amd", "csrc"), "-x", "hip",
+           "--cuda-device-only", "-c", os.path.join(ROOT, "paper_2608_02947_amd", "csrc", src),
+           "-o", str(out), "-Rpass-analysis=kernel-resource-usage"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    kernels = {}
+    name = None
+    for ln in r.stderr.splitlines():
+        m = re.search(r"Function Name: (\S+)", ln)
+        if m:
+            name = m.group(1)
+            kernels[name] = {}
+            continue
+        m = re.search(r"(VGPRs Spill|SGPRs Spill|ScratchSize \[bytes/lane\]): (\d+)", ln)
+        if m and name:
+            kernels[name][m.group(1)] = int(m.group(2))
+    assert kernels
+    for k, v in kernels.items():
+        assert v.get("VGPRs Spill", 0) == 0 and v.get("ScratchSize [bytes/lane]", 0) == 0, (k, v)
+        assert v.get("SGPRs Spill", 0) <= 8, (k, v)
