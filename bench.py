@@ -68,10 +68,13 @@ def parse():
     ap.add_argument("--profile-kinf", action="store_true", help="profiling driver at k = +inf")
     ap.add_argument("--profile-raw-base", action="store_true",
                     help="profiling driver: window table from the raw RoPE base (Llama shapes)")
+    ap.add_argument("--profile-unrotated", action="store_true",
+                    help="profiling driver, decode workloads: atf_decode_unrotated (RoPE at read "
+                         "time) on the same buffers")
     return ap.parse_args()
 
 
-def profile_driver(name, iters, kinf, raw_base=False):
+def profile_driver(name, iters, kinf, raw_base=False, unrotated=False):
     """Run one workload's prefill or decode `iters` times (for rocprofv3 runs)."""
     import paper_2608_02947_amd as atf
     import workloads as W
@@ -105,7 +108,8 @@ def profile_driver(name, iters, kinf, raw_base=False):
         lsed = torch.empty((wl.batch, wl.h_q), dtype=torch.float32, device=dev)
         ws = torch.empty(atf.atf_decode_workspace_bytes(wl.batch, wl.h_q, wl.h_kv, wl.n_k, d),
                          dtype=torch.uint8, device=dev)
-        run = lambda: atf.atf_decode(qd, kp, vp, od, lsed, wl.q_pos0, win, ws, stream=stream)
+        dec = atf.atf_decode_unrotated if unrotated else atf.atf_decode
+        run = lambda: dec(qd, kp, vp, od, lsed, wl.q_pos0, win, ws, stream=stream)
     ms = []
     for _ in range(iters):
         a = torch.cuda.Event(enable_timing=True)
@@ -552,7 +556,7 @@ def main():
         return
     if args.profile_workload:
         profile_driver(args.profile_workload, args.profile_iters, args.profile_kinf,
-                       args.profile_raw_base)
+                       args.profile_raw_base, args.profile_unrotated)
         return
 
     import paper_2608_02947_amd as atf
