@@ -287,6 +287,8 @@ prefill_kernel(const PrefillParams p) {
 #pragma unroll
     for (int i = 0; i < D / 32; ++i) oacc[i] = zero16();
     float m_run = -INFINITY;  // running (possibly stale) max, log2 domain
+    float m_thr = -INFINITY;  // m_run + kRescale: a tile max above it raises m_run
+    float m_neg = 0.f;        // minus the max the exponentials subtract (0 while m_run = -inf)
     float l_run = 0.f;        // normaliser over this lane's keys
     const float sc = p.scale_log2;
     f32x16_t sacc[2];  // scores of the current tile (two 32-key blocks)
@@ -401,19 +403,23 @@ prefill_kernel(const PrefillParams p) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[kb][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float cand = mx * sc;
-        if (__any(cand > m_run + kRescale)) {
-            const float m_new = fmaxf(m_run, cand);
-            const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
+        // The two lane halves of a row hold the same m_run and sc > 0, so some lane's half
+        // max passes the threshold exactly when some lane's row max does: the halves
+        // exchange their maxima only when the running max is raised.
+        if (__any(mx * sc > m_thr)) {
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx * sc);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2_fast(m_run - m_use);
             m_run = m_new;
+            m_thr = m_new + kRescale;
+            m_neg = -m_use;
             l_run *= alpha;
 #pragma unroll
             for (int i = 0; i < D / 32; ++i)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
         }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
         const uint32_t vb = v_lane + stage_off<C::kStages>(tile, C::kVTile * 2);
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
@@ -422,8 +428,8 @@ prefill_kernel(const PrefillParams p) {
             for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    const float a = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t], sc, -m_use));
-                    const float c2 = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t + 1], sc, -m_use));
+                    const float a = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t], sc, m_neg));
+                    const float c2 = exp2_fast(__builtin_fmaf(sacc[kb][8 * ks + 2 * t + 1], sc, m_neg));
                     l_run += a;
                     l_run += c2;
                     bf16x2_t two;
