@@ -250,7 +250,47 @@ prefill_kernel(const PrefillParams p) {
             if (p.win.chunk_max[c] >= zlo) need |= 1u << c;
         return need;
     };
+    // Fast form for tiles wholly below n_k (all but the last): per wave unit, the
+    // stream base and the first tile from which its chunk is kept (chunk c is kept in
+    // the tile at j0 iff chunk_max[c] >= pos_first - j0 - 63; the thresholds are >= 0)
+    // are fixed, so a tile costs one compare and one 64-bit add per load.
+    const char* kbase[C::kKPerWave];
+    int kfirst[C::kKPerWave];
+#pragma unroll
+    for (int t = 0; t < C::kKPerWave; ++t) {
+        const int u = wave + C::kWaves * t;
+        const int c = u >> 1;
+        kbase[t] = kpcm + c * chunk_bytes + (u & 1) * 1024;
+        kfirst[t] = 0;
+        if (kWin && c != C::kChunks - 1) {
+            const int64_t num = int64_t(pos_first) - (kBN - 1) - p.win.chunk_max[c];
+            kfirst[t] = num <= 0 ? 0 : int(min(int64_t(INT32_MAX), (num + kBN - 1) / kBN));
+        }
+    }
+    auto issue_fast = [&](int j0, int buf) __attribute__((always_inline)) {
+        const int tn = j0 / kBN;
+        const int64_t koff = int64_t(j0) * 32;
+        const int64_t voff = int64_t(j0) * (2 * D);
+        const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
+#pragma unroll
+        for (int t = 0; t < C::kKPerWave; ++t) {
+            const int u = wave + C::kWaves * t;
+            if (tn >= kfirst[t]) load_to_lds(kbase[t] + koff, k_piece, kdst + 1024u * u);
+        }
+        const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
+#pragma unroll
+        for (int t = 0; t < C::kVPer; ++t) {
+            const int u = wave + C::kWaves * t;
+            if constexpr (C::kVLoads % C::kWaves != 0)
+                if (u >= C::kVLoads) break;
+            load_to_lds(vhead + voff + 1024 * u, uint32_t(lane) * 16u, vdst + 1024u * u);
+        }
+    };
     auto issue = [&](int j0, int buf) __attribute__((always_inline)) {
+        if (j0 + kBN <= p.n_k) {
+            issue_fast(j0, buf);
+            return;
+        }
         const uint32_t need = tile_need(j0);
         const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
