@@ -512,8 +512,8 @@ TRAFFIC_RECORDS = {
     "prefill_kernel<128, true>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "1f8b63a80e27becca24aacfbd9e8454fd7f631f9184f3e5cd94916630c2c739c",
-        "fetch_kib": 79575514.44, "write_kib": 933446.66,
+        "sha256": "f3e4f1625eb77f06488c48fa74f20cf8357d4cb6c543079ca8dfc378f208eb80",
+        "fetch_kib": 84980866.06, "write_kib": 933525.31,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
