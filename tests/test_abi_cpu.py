@@ -256,6 +256,44 @@ def _raw_prefill(lib, cw, **kw):
                            args["cache_tokens"], ctypes.byref(cw), 0.0, None)
 
 
+@pytest.mark.parametrize("name", ["qwen05b_prefill_32k", "llama3b_prefill_128k",
+                                  "qwen7b1m_prefill_chunk"])
+@pytest.mark.parametrize("kind", ["k2", "k0.5", "k64", "var16to2", "rounded8", "floor64"])
+def test_prefill_first_kept_tile_matches_the_chunk_test(name, kind):
+    """The prefill stages K chunk c of the 64-key tile at j0 iff some pair of c is kept
+    at the tile's smallest distance, max(0, pos_first - j0 - 63), i.e. iff the chunk's
+    largest threshold reaches it.  Its load issue replaces that per-tile test by one
+    first tile per chunk, ceil((pos_first - 63 - max_c W) / 64) clamped at 0, which
+    holds because thresholds are >= 0 and the distance falls as j0 grows.  Both forms
+    over the window tables the kernels see, and positions from the first tile to 2^31."""
+    wl = W.WORKLOADS[name]
+    d = wl.head_dim
+    th = W.workload_theta(wl)
+    th = None if th is None else th.numpy()
+    kw = {"k2": dict(k=2.0), "k0.5": dict(k=0.5), "k64": dict(k=64.0),
+          "var16to2": dict(k=16.0, k_profile=atf.atf_retention_profile(d, "arithmetic", 16.0, 2.0)),
+          "rounded8": dict(k=2.0, slice_pairs=8), "floor64": dict(k=2.0, beta=64.0)}[kind]
+    k = kw.pop("k")
+    table = atf.atf_window_table(atf.Window(d, wl.rope_base, k, th, **kw)).astype(np.int64)
+    assert table.min() >= 0
+    chunk_max = table.reshape(d // 16, 8).max(axis=1)
+    rng = np.random.default_rng(7)
+    positions = np.concatenate([[0, 1, 62, 63, 64, 65, 127, 128, 4095, 2**31 - 2],
+                                rng.integers(0, 2**31 - 1, size=40)])
+    for pos_first in positions:
+        pos_first = int(pos_first)
+        num = pos_first - 63 - chunk_max
+        first = np.where(num <= 0, 0, np.minimum(2**31 - 1, -(-num // 64)))
+        t_hi = max(0, pos_first + 63) // 64
+        tiles = np.unique(np.concatenate([np.arange(0, 64), np.arange(max(0, t_hi - 64), t_hi + 2),
+                                          first, np.maximum(first - 1, 0), first + 1]))
+        tiles = tiles[(tiles >= 0) & (tiles < 2**25)]
+        zlo = np.maximum(0, pos_first - 64 * tiles - 63)
+        kept = chunk_max[None, :] >= zlo[:, None]
+        by_first = tiles[:, None] >= first[None, :]
+        assert np.array_equal(kept, by_first), (pos_first, np.argwhere(kept != by_first)[:4])
+
+
 def test_prefill_validation_before_launch():
     lib = atf.library()
     good, _ = atf.Window(64, 1e4, 2.0).as_c()
