@@ -41,6 +41,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 # (back-to-back MFMAs on one wave per SIMD; the clock drops below its 2.4 GHz peak under
 # this load); a reference figure beside the published peak, which the roofline uses
 MEASURED_MFMA_BF16_TFLOPS = 1965.9
+# v_exp_f32 throughput measured the same way (16 independent chains per thread, every SIMD)
+MEASURED_V_EXP_PER_S = 1.321e13
 
 
 def parse():
@@ -687,6 +689,9 @@ def main():
         "retained_terms_per_head": T, "causal_cells_per_head": C,
         "qk_pruned": round(1 - T / (C * d / 2), 4),
         "ceiling_2_over_1_plus_s": round(flops_prefill_full / flops_prefill, 4),
+        # the transcendental lower bound beside the MFMA roofline: one v_exp_f32 per causal
+        # (row, key) cell of every query head, at the measured v_exp_f32 rate
+        "exp_floor_ms": round(B * pf.h_q * C / MEASURED_V_EXP_PER_S * 1e3, 2),
     }
     decode_info = {
         "ms_median": round(dec_med, 4), "ms_min": round(min(dec_ms), 4),
