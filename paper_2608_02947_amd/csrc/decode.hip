@@ -281,6 +281,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
 #pragma unroll
     for (int i = 0; i < kDB; ++i) oacc[i] = zero16();
     float m_run = -INFINITY;
+    float m_thr = -INFINITY;  // m_run + kRescale: a block max above it raises m_run
+    float m_neg = 0.f;        // minus the max the exponentials subtract (0 while m_run = -inf)
     float l_run = 0.f;
     const float sc = p.scale_log2;
 
@@ -496,26 +498,30 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
         float mx = -INFINITY;
 #pragma unroll
         for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float cand = mx * sc;
-        if (__any(cand > m_run + kRescale)) {
-            const float m_new = fmaxf(m_run, cand);
-            const float alpha = exp2_fast(m_run - (m_new == -INFINITY ? 0.f : m_new));
+        // the two lane halves of a column share m_run and sc > 0: some lane's half max
+        // passes the threshold exactly when some column max does, so the halves exchange
+        // their maxima only when the running max is raised
+        if (__any(mx * sc > m_thr)) {
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx * sc);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2_fast(m_run - m_use);
             m_run = m_new;
+            m_thr = m_new + kRescale;
+            m_neg = -m_use;
             l_run *= alpha;
 #pragma unroll
             for (int i = 0; i < kDB; ++i)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) oacc[i][v] *= alpha;
         }
-        const float m_use = m_run == -INFINITY ? 0.f : m_run;
         u32x4_t pb[2];
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
-                const float a = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t], sc, -m_use));
-                const float c2 = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t + 1], sc, -m_use));
+                const float a = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t], sc, m_neg));
+                const float c2 = exp2_fast(__builtin_fmaf(sacc[8 * ks + 2 * t + 1], sc, m_neg));
                 l_run += a;
                 l_run += c2;
                 bf16x2_t two;
