@@ -520,8 +520,8 @@ TRAFFIC_RECORDS = {
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp"],
-        "sha256": "c500721d4f3b3ed688c9c604a4a920de3c347a9f2e2009a0189ee9be813f6470",
-        "fetch_kib": 737826.23, "write_kib": 4065.45,
+        "sha256": "259b2d1855f6a8f0bc0f9e9667b73a91c9c6760da0d8333a196051e78bcafa1a",
+        "fetch_kib": 737789.75, "write_kib": 4066.45,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.02, "write": 1048576.0}  # counters for a 1 GiB copy
