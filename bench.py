@@ -71,8 +71,8 @@ def parse():
     ap.add_argument("--profile-raw-base", action="store_true",
                     help="profiling driver: window table from the raw RoPE base (Llama shapes)")
     ap.add_argument("--profile-unrotated", action="store_true",
-                    help="profiling driver, decode workloads: atf_decode_unrotated (RoPE at read "
-                         "time) on the same buffers")
+                    help="profiling driver: atf_prefill_unrotated / atf_decode_unrotated (RoPE "
+                         "at read time) on the same buffers")
     return ap.parse_args()
 
 
@@ -97,7 +97,8 @@ def profile_driver(name, iters, kinf, raw_base=False, unrotated=False):
         vp = torch.empty(atf.vcache_shape(wl.batch, wl.n_k, wl.h_kv, d), dtype=torch.bfloat16,
                          device=dev)
         atf.atf_pack_vcache(inp["v"], vp)
-        run = lambda: atf.atf_prefill(inp["q"], kp, vp, o, lse, wl.q_pos0, win, stream=stream)
+        pre = atf.atf_prefill_unrotated if unrotated else atf.atf_prefill
+        run = lambda: pre(inp["q"], kp, vp, o, lse, wl.q_pos0, win, stream=stream)
     else:
         kp = torch.empty((wl.batch, wl.h_kv, d // 16, wl.n_k, 16), dtype=torch.bfloat16,
                          device=dev)
@@ -511,15 +512,17 @@ def ragged_decode_config(atf, W, dev, stream):
 # device-to-device copy.  A record holds only for the kernel sources it was
 # taken on (sha256 of the files below); otherwise traffic is reported as null.
 TRAFFIC_RECORDS = {
-    "prefill_kernel<128, true>": {
+    "prefill_kernel<128, true, false>": {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
-                    "paper_2608_02947_amd/csrc/atf_internal.hpp"],
+                    "paper_2608_02947_amd/csrc/atf_internal.hpp",
+                    "paper_2608_02947_amd/csrc/rope.hpp"],
         "sha256": "f3e4f1625eb77f06488c48fa74f20cf8357d4cb6c543079ca8dfc378f208eb80",
         "fetch_kib": 84980866.06, "write_kib": 933525.31,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
-                    "paper_2608_02947_amd/csrc/atf_internal.hpp"],
+                    "paper_2608_02947_amd/csrc/atf_internal.hpp",
+                    "paper_2608_02947_amd/csrc/rope.hpp"],
         "sha256": "259b2d1855f6a8f0bc0f9e9667b73a91c9c6760da0d8333a196051e78bcafa1a",
         "fetch_kib": 737789.75, "write_kib": 4066.45,
     },
@@ -727,6 +730,22 @@ def main():
         decode_info["unrotated_cache"]["full_window_ms"] = round(tu_off, 4)
         decode_info["unrotated_cache"]["speedup_vs_full_window"] = round(tu_off / tu, 4)
 
+    # ---- the same prefill from unrotated caches: the same matrix work, plus the rotation
+    # of each query row once and of each kept (key, pair-chunk) once per workgroup that
+    # loads it; timed on the same buffers (the work does not depend on the values)
+    def prefill_unrot(w):
+        atf.atf_prefill_unrotated(q, kp, vp, o, lse, pf.q_pos0, w, stream=stream)
+
+    tpu = _median_ms(lambda: prefill_unrot(win), stream, 1, args.steps)
+    prefill_info["unrotated_cache"] = {
+        "ms": round(tpu, 3), "effective_tflops": round(flops_prefill / (tpu * 1e-3) / 1e12, 1),
+        "frac_bf16_peak": round(flops_prefill / (tpu * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "time_vs_rotated_cache": round(tpu / pre_med, 4)}
+    if full is not None:
+        tpu_off = _median_ms(lambda: prefill_unrot(win_off), stream, 1, args.steps)
+        prefill_info["unrotated_cache"]["full_window_ms"] = round(tpu_off, 3)
+        prefill_info["unrotated_cache"]["speedup_vs_full_window"] = round(tpu_off / tpu, 4)
+
     # ---- other windows on the same inputs: the variable-k profile 16 -> 2 and uniform
     # k = 64 (App. A, tab:absbench), and the rounded slice (Sec. 3.3, tab:c2e2e)
     family = None
@@ -748,8 +767,8 @@ def main():
                 "decode_speedup_vs_full_window":
                     None if full is None else round(full["decode_ms"] / td, 4)}
 
-    tr = recorded_traffic("prefill_kernel<128, true>")
-    roofline = {"kernel": "prefill_kernel<128, true>", "bound": "mfma",
+    tr = recorded_traffic("prefill_kernel<128, true, false>")
+    roofline = {"kernel": "prefill_kernel<128, true, false>", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                 "traffic": None if tr is None else tr["bytes"],

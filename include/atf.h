@@ -351,6 +351,25 @@ int atf_decode_paged(const void *q, const void *k_pages, const void *v_pages, vo
  * (atf_decode_paged_unrotated): same layouts, window, workspace, errors, plus
  * ATF_EINVAL for a rotation frequency that is negative, infinite or NaN.  V is never
  * rotated.  Deterministic: equal inputs give equal bits. */
+/* Prefill from UNROTATED caches: RoPE applied at read time (App. B), as in
+ * atf_decode_unrotated.  Query row i (position q_pos0 + i) is rotated once as the
+ * workgroup loads it; each key j (position j) is rotated chunk by chunk after the chunk
+ * lands in LDS, and only the pair-chunks the window keeps for the tile are loaded and
+ * rotated, so a pruned pair of a key is neither read nor rotated.  Rotate-half
+ * convention of Sec. 2 in fp32 from the bf16 inputs, rounded to bf16 before the matrix
+ * products; the key's angle (block start + offset) * theta_r is formed by angle
+ * addition from the block start's angle (0.64 fixed-point fraction, exact for any
+ * position) and a table of the 32 offsets' angles, so it is within a few fp32 ulps of
+ * the exact angle.
+ *   rope_inv_freq  host double [d/2] of the rotation's theta_r, or NULL: the window's
+ *                  frequencies (w->inv_freq if set, else rope_base^(-2r/d))
+ * Everything else is atf_prefill: same layouts, window, errors, plus ATF_EINVAL for a
+ * rotation frequency that is negative, infinite or NaN.  V is never rotated. */
+int atf_prefill_unrotated(const void *q, const void *k_cache, const void *v_cache, void *o,
+                          float *lse, int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0,
+                          int32_t h_q, int32_t h_kv, int64_t cache_tokens, const atf_window *w,
+                          const double *rope_inv_freq, float softmax_scale, void *hip_stream);
+
 int atf_decode_unrotated(const void *q, const void *k_cache, const void *v_cache, void *o,
                          float *lse, int32_t batch, int64_t n_k, int64_t q_pos, int32_t h_q,
                          int32_t h_kv, int64_t cache_tokens, const atf_window *w,

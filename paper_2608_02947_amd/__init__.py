@@ -18,6 +18,8 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_decode_noalloc` -- the same without a workspace (library scratch array).
 - :func:`atf_decode_ragged` -- the same for a batch of sequences of different lengths.
 - :func:`atf_cache_append_paged`, :func:`atf_decode_paged` -- paged caches (block tables).
+- :func:`atf_prefill_unrotated`, :func:`atf_decode_unrotated` (and its ragged and paged
+  forms) -- the same from unrotated caches, RoPE applied as the kernels read them.
 """
 from __future__ import annotations
 
@@ -85,6 +87,8 @@ def _load():
                                                   i32, i32, P]),
         "atf_decode_paged": (ctypes.c_int, [P, P, P, P, P, i32, P, i32, i32, i32, P, P, i64, i32,
                                             i32, W, f32, P, ctypes.c_size_t, P]),
+        "atf_prefill_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64,
+                                                 W, P, f32, P]),
         "atf_decode_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, P,
                                                 f32, P, ctypes.c_size_t, P]),
         "atf_decode_ragged_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, P, P, i64, i32, i32, i64,
@@ -106,7 +110,7 @@ EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
             "atf_decode_workspace_bytes", "atf_decode", "atf_decode_noalloc", "atf_decode_ragged",
             "atf_cache_append_paged",
-            "atf_decode_paged", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
+            "atf_decode_paged", "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
             "atf_decode_paged_unrotated", "atf_last_error")
 
 
@@ -378,6 +382,33 @@ def _rope_freq(rope_inv_freq, d):
     if arr.shape != (d // 2,):
         raise ValueError(f"rope_inv_freq must have d/2 = {d // 2} entries")
     return arr.ctypes.data_as(ctypes.c_void_p), arr
+
+
+def atf_prefill_unrotated(q, k_cache, v_cache, o, lse, q_pos0: int, window: Window,
+                          softmax_scale: float = 0.0, stream=None, n_k: Optional[int] = None,
+                          rope_inv_freq=None):
+    """atf_prefill with q and the K cache UNROTATED: the kernel applies RoPE (query row i
+    at q_pos0 + i, key j at position j) to q and to the key pairs the window keeps.
+    rope_inv_freq: the rotation's theta_r (d/2 floats) or None for the window's
+    frequencies."""
+    torch = _torch()
+    B, n_q, h_q, d = q.shape
+    if k_cache.dim() != 5:
+        raise ValueError("atf_prefill_unrotated: k_cache must be [B, h_kv, d/16, C, 16]")
+    _, h_kv, _, cap, _ = k_cache.shape
+    n_k = cap if n_k is None else int(n_k)
+    if tuple(k_cache.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_cache.shape) != vcache_shape(B, cap, h_kv, d) or \
+            tuple(o.shape) != tuple(q.shape) or tuple(lse.shape) != (B, h_q, n_q):
+        raise ValueError("atf_prefill_unrotated: inconsistent shapes")
+    cw, keep = window.as_c()
+    fp, keep2 = _rope_freq(rope_inv_freq, d)
+    rc = _lib.atf_prefill_unrotated(
+        _dev_ptr(q, torch.bfloat16, "q"), _dev_ptr(k_cache, torch.bfloat16, "k"),
+        _dev_ptr(v_cache, torch.bfloat16, "v"), _dev_ptr(o, torch.bfloat16, "o"),
+        _dev_ptr(lse, torch.float32, "lse"), B, n_q, n_k, q_pos0, h_q, h_kv, cap,
+        ctypes.byref(cw), fp, float(softmax_scale), _stream_ptr(stream))
+    _check(rc)
 
 
 def atf_decode_unrotated(q, k_pcm, v_pack, o, lse, q_pos: int, window: Window, workspace,

@@ -270,39 +270,80 @@ int32_t atf_kcache_chunk_pairs(int32_t head_dim) {
     return (head_dim == 64 || head_dim == 128) ? atf::kChunkPairs : 0;
 }
 
-int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse,
-                int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
-                int32_t h_kv, int64_t cache_tokens, const atf_window* w, float softmax_scale,
-                void* hip_stream) {
-    if (w == nullptr) return fail(ATF_EINVAL, "prefill: NULL window");
+namespace {
+
+// RoPE at read time (q and the K cache unrotated): theta_r = rope_inv_freq[r] if given,
+// else the window's frequencies (its inv_freq, or rope_base^(-2r/d)).
+struct RopeArgs {
+    bool rotate = false;
+    const double* inv_freq = nullptr;
+};
+
+// rho_r = theta_r / (2 pi) mod 1 as a 0.64 fixed-point fraction, in extended precision
+int rope_fractions(const char* fn, const atf_window* w, const double* inv_freq,
+                   uint32_t* rho_hi, uint32_t* rho_lo) {
+    const int d = w->head_dim;
+    const long double two_pi = 6.283185307179586476925286766559L;
+    for (int r = 0; r < d / 2; ++r) {
+        double th;
+        if (inv_freq != nullptr)
+            th = inv_freq[r];
+        else if (w->inv_freq != nullptr)
+            th = w->inv_freq[r];
+        else
+            th = std::pow(w->rope_base, -2.0 * r / d);
+        if (!(th >= 0.0) || std::isinf(th))
+            return fail(ATF_EINVAL, "%s: rotation frequency %d = %g must be finite and >= 0", fn, r,
+                        th);
+        long double f = static_cast<long double>(th) / two_pi;
+        f -= std::floor(f);
+        long double scaled = std::ldexp(f, 64);
+        uint64_t fx = scaled >= 18446744073709551615.0L ? UINT64_MAX : static_cast<uint64_t>(scaled);
+        rho_hi[r] = static_cast<uint32_t>(fx >> 32);
+        rho_lo[r] = static_cast<uint32_t>(fx);
+    }
+    return ATF_OK;
+}
+
+// Shared by atf_prefill (pre-rotated caches) and atf_prefill_unrotated (RoPE applied
+// to q and each kept key pair as the kernel reads them).
+int prefill_impl(const char* fn, const void* q, const void* k, const void* v, void* o, float* lse,
+                 int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
+                 int32_t h_kv, int64_t cache_tokens, const atf_window* w, float softmax_scale,
+                 void* hip_stream, const RopeArgs& rope) {
+    if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
     const int d = w->head_dim;
     if (d != 64 && d != 128)
-        return fail(ATF_EUNSUPPORTED, "prefill: head_dim %d not built (64 or 128)", d);
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
     if (batch < 1 || n_q < 0 || n_k < 1 || q_pos0 < 0 || h_q < 1 || h_kv < 1)
         return fail(ATF_EINVAL,
-                    "prefill: need batch >= 1, n_q >= 0, n_k >= 1, q_pos0 >= 0, heads >= 1");
+                    "%s: need batch >= 1, n_q >= 0, n_k >= 1, q_pos0 >= 0, heads >= 1", fn);
     if (h_q % h_kv != 0)
-        return fail(ATF_EINVAL, "prefill: h_q %d not a multiple of h_kv %d", h_q, h_kv);
+        return fail(ATF_EINVAL, "%s: h_q %d not a multiple of h_kv %d", fn, h_q, h_kv);
     const int max_group = d == 64 ? 128 : 256;  // query rows of one prefill workgroup
     if (h_q / h_kv > max_group)
-        return fail(ATF_EUNSUPPORTED, "prefill: GQA ratio %d above %d not built for d = %d",
+        return fail(ATF_EUNSUPPORTED, "%s: GQA ratio %d above %d not built for d = %d", fn,
                     h_q / h_kv, max_group, d);
     if (q_pos0 + n_q > kPosLimit || n_k > kPosLimit)
-        return fail(ATF_EINVAL, "prefill: positions must stay below 2^31 - 1");
+        return fail(ATF_EINVAL, "%s: positions must stay below 2^31 - 1", fn);
     if (cache_tokens == 0) cache_tokens = n_k;
     if (cache_tokens < n_k || cache_tokens > kPosLimit)
-        return fail(ATF_EINVAL, "prefill: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1",
+        return fail(ATF_EINVAL, "%s: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1", fn,
                     (long long)cache_tokens, (long long)n_k);
     if (!std::isfinite(softmax_scale))
-        return fail(ATF_EINVAL, "prefill: softmax_scale must be finite");
-    atf::PrefillParams p{};
+        return fail(ATF_EINVAL, "%s: softmax_scale must be finite", fn);
+    atf::PrefillRotParams p{};
     int rc = build_table(w, &p.win);
     if (rc != ATF_OK) return rc;
+    if (rope.rotate) {
+        rc = rope_fractions(fn, w, rope.inv_freq, p.rope_rho_hi, p.rope_rho_lo);
+        if (rc != ATF_OK) return rc;
+    }
     if (n_q == 0) return ATF_OK;
-    if (!q || !k || !v || !o || !lse) return fail(ATF_EINVAL, "prefill: NULL tensor pointer");
+    if (!q || !k || !v || !o || !lse) return fail(ATF_EINVAL, "%s: NULL tensor pointer", fn);
     if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
         !aligned(lse, 4))
-        return fail(ATF_EINVAL, "prefill: q/k/v/o must be 16-byte and lse 4-byte aligned");
+        return fail(ATF_EINVAL, "%s: q/k/v/o must be 16-byte and lse 4-byte aligned", fn);
     const float scale = softmax_scale > 0.f ? softmax_scale : 1.0f / std::sqrt(float(d));
     p.q = static_cast<const uint16_t*>(q);
     p.k = static_cast<const uint16_t*>(k);
@@ -318,10 +359,34 @@ int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse
     p.h_kv = h_kv;
     p.group = h_q / h_kv;
     p.scale_log2 = scale * 1.4426950408889634f;
-    hipError_t e = atf::launch_prefill(p, d, static_cast<hipStream_t>(hip_stream));
-    if (e != hipSuccess) return fail(ATF_EHIP, "prefill: launch failed: %s", hipGetErrorString(e));
+    const hipStream_t st = static_cast<hipStream_t>(hip_stream);
+    const hipError_t e = rope.rotate ? atf::launch_prefill_rotating(p, d, st)
+                                     : atf::launch_prefill(p, d, st);
+    if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return ATF_OK;
 }
+
+}  // namespace
+
+int atf_prefill(const void* q, const void* k, const void* v, void* o, float* lse,
+                int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
+                int32_t h_kv, int64_t cache_tokens, const atf_window* w, float softmax_scale,
+                void* hip_stream) {
+    return prefill_impl("prefill", q, k, v, o, lse, batch, n_q, n_k, q_pos0, h_q, h_kv,
+                        cache_tokens, w, softmax_scale, hip_stream, RopeArgs());
+}
+
+int atf_prefill_unrotated(const void* q, const void* k, const void* v, void* o, float* lse,
+                          int32_t batch, int64_t n_q, int64_t n_k, int64_t q_pos0, int32_t h_q,
+                          int32_t h_kv, int64_t cache_tokens, const atf_window* w,
+                          const double* rope_inv_freq, float softmax_scale, void* hip_stream) {
+    RopeArgs rope;
+    rope.rotate = true;
+    rope.inv_freq = rope_inv_freq;
+    return prefill_impl("prefill_unrotated", q, k, v, o, lse, batch, n_q, n_k, q_pos0, h_q, h_kv,
+                        cache_tokens, w, softmax_scale, hip_stream, rope);
+}
+
 
 namespace {
 int check_pack(const char* what, const void* src, void* dst, int32_t batch, int64_t n_k,
@@ -478,39 +543,6 @@ struct PagedArgs {
     int32_t max_pages = 0, num_pages = 0, page_tokens = 0;
 };
 
-// RoPE at read time (q and the K cache unrotated): theta_r = rope_inv_freq[r] if given,
-// else the window's frequencies (its inv_freq, or rope_base^(-2r/d)).
-struct RopeArgs {
-    bool rotate = false;
-    const double* inv_freq = nullptr;
-};
-
-// rho_r = theta_r / (2 pi) mod 1 as a 0.64 fixed-point fraction, in extended precision
-int rope_fractions(const char* fn, const atf_window* w, const double* inv_freq,
-                   atf::DecodeParams* p) {
-    const int d = w->head_dim;
-    const long double two_pi = 6.283185307179586476925286766559L;
-    for (int r = 0; r < d / 2; ++r) {
-        double th;
-        if (inv_freq != nullptr)
-            th = inv_freq[r];
-        else if (w->inv_freq != nullptr)
-            th = w->inv_freq[r];
-        else
-            th = std::pow(w->rope_base, -2.0 * r / d);
-        if (!(th >= 0.0) || std::isinf(th))
-            return fail(ATF_EINVAL, "%s: rotation frequency %d = %g must be finite and >= 0", fn, r,
-                        th);
-        long double f = static_cast<long double>(th) / two_pi;
-        f -= std::floor(f);
-        long double scaled = std::ldexp(f, 64);
-        uint64_t fx = scaled >= 18446744073709551615.0L ? UINT64_MAX : static_cast<uint64_t>(scaled);
-        p->rope_rho_hi[r] = static_cast<uint32_t>(fx >> 32);
-        p->rope_rho_lo[r] = static_cast<uint32_t>(fx);
-    }
-    return ATF_OK;
-}
-
 int decode_impl(const char* fn, const void* q, const void* k_cache, const void* v_cache, void* o,
                 float* lse, int32_t batch, int64_t n_k, int64_t q_pos, const int32_t* n_k_rows,
                 const int32_t* q_pos_rows, int32_t h_q, int32_t h_kv, int64_t cache_tokens,
@@ -537,7 +569,7 @@ int decode_impl(const char* fn, const void* q, const void* k_cache, const void* 
     int rc = build_table(w, &p.win);
     if (rc != ATF_OK) return rc;
     if (rope.rotate) {
-        rc = rope_fractions(fn, w, rope.inv_freq, &p);
+        rc = rope_fractions(fn, w, rope.inv_freq, p.rope_rho_hi, p.rope_rho_lo);
         if (rc != ATF_OK) return rc;
         p.rotate = 1;
     }

@@ -36,6 +36,14 @@ struct PrefillParams {
     WindowTable win;
 };
 
+// Prefill with RoPE at read time: q and the K cache hold unrotated vectors, rotated
+// in the kernel as DecodeParams describes. A type of its own, so that the kernels
+// of pre-rotated caches keep their argument block.
+struct PrefillRotParams : PrefillParams {
+    uint32_t rope_rho_hi[kMaxPairs];
+    uint32_t rope_rho_lo[kMaxPairs];
+};
+
 struct DecodeParams {
     const uint16_t* q;       // [B][h_q][d]
     const uint16_t* kpcm;    // [B][h_kv][d/16][cache_tokens][16]
@@ -94,6 +102,7 @@ struct PackParams {
 
 // Kernel launchers (prefill.hip, decode.hip).  Return the HIP error of the launch.
 hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_prefill_rotating(const PrefillRotParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);

@@ -37,6 +37,7 @@
 // the query once and to each key chunk it loads, so a pruned pair is neither read nor
 // rotated.
 #include "atf_internal.hpp"
+#include "rope.hpp"
 
 #include <mutex>
 
@@ -130,61 +131,6 @@ __device__ int ragged_item(const DecodeParams& p, int item, int& t_first, int64_
     return row;
 }
 
-// RoPE at read time.  The angle of pair r at position pos, in revolutions: the high
-// word of the fraction of pos * rho_r (rho_r = theta_r / (2 pi) in 0.64 fixed point),
-// exact for every position below 2^32 up to the last bit of rho_r.
-__device__ __forceinline__ float rope_revolutions(uint32_t pos, uint2 rho) {
-    return float(pos * rho.x + __umulhi(pos, rho.y)) * 2.3283064365386963e-10f;  // 2^-32
-}
-
-// Rotate one fragment: the 8 elements of half hh of pairs 8c .. 8c + 7 of a vector
-// (`own`), given the other half of the same pairs (`other`) and the cosines and sines
-// of the 8 pairs' angles.  Half 0 holds the first components x_r and half 1 the second
-// x_{r + d/2} (rotate-half): x'_r = x_r cos - x_{r+d/2} sin and
-// x'_{r+d/2} = x_{r+d/2} cos + x_r sin, in fp32, rounded to bf16.
-__device__ __forceinline__ u32x4_t rope_rotate_cs(u32x4_t own, u32x4_t other, int hh,
-                                                  const float* cs8, const float* sn8) {
-    const float sgn = hh ? 1.f : -1.f;
-    u32x4_t r;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const float o0 = __uint_as_float(own[t] << 16), o1 = __uint_as_float(own[t] & 0xFFFF0000u);
-        const float x0 = __uint_as_float(other[t] << 16), x1 = __uint_as_float(other[t] & 0xFFFF0000u);
-        bf16x2_t two;
-        two[0] = (__bf16)__builtin_fmaf(o0, cs8[2 * t], sgn * x0 * sn8[2 * t]);
-        two[1] = (__bf16)__builtin_fmaf(o1, cs8[2 * t + 1], sgn * x1 * sn8[2 * t + 1]);
-        r[t] = __builtin_bit_cast(uint32_t, two);
-    }
-    return r;
-}
-
-// The same for a vector at position pos, its angles evaluated directly
-// (v_cos_f32 / v_sin_f32 take their argument in revolutions).
-__device__ __forceinline__ u32x4_t rope_rotate(u32x4_t own, u32x4_t other, int hh, uint32_t pos,
-                                               const uint32_t* rho_hi8, const uint32_t* rho_lo8) {
-    float cs8[8], sn8[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const float u = rope_revolutions(pos, make_uint2(rho_hi8[e], rho_lo8[e]));
-        cs8[e] = __builtin_amdgcn_cosf(u);
-        sn8[e] = __builtin_amdgcn_sinf(u);
-    }
-    return rope_rotate_cs(own, other, hh, cs8, sn8);
-}
-
-// The other half of a fragment: lane l gets the registers of lane l ^ 32 (the same
-// token or head column, the other 8 dims of each pair).
-__device__ __forceinline__ u32x4_t other_half(u32x4_t x, int hh) {
-    u32x4_t r;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        // lanes 32..63 of the first copy trade places with lanes 0..31 of the second
-        const auto sw = __builtin_amdgcn_permlane32_swap(x[t], x[t], false, false);
-        r[t] = hh ? sw[0] : sw[1];
-    }
-    return r;
-}
-
 template <int D, bool kRot>
 __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const DecodeParams p) {
     constexpr int kChunks = D / 16;
@@ -250,7 +196,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
     if constexpr (kRot) {
         for (int e = tid; e < 32 * kHalf; e += kWaves * 64) {
             const int cc = e / kHalf, r = e % kHalf;
-            const float u = rope_revolutions(uint32_t(cc), make_uint2(p.rope_rho_hi[r], p.rope_rho_lo[r]));
+            const float u = rope::revolutions(uint32_t(cc), make_uint2(p.rope_rho_hi[r], p.rope_rho_lo[r]));
             s_colcs[cc * kCStride + 2 * r] = __builtin_amdgcn_cosf(u);
             s_colcs[cc * kCStride + 2 * r + 1] = __builtin_amdgcn_sinf(u);
         }
@@ -271,7 +217,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             if (head_ok) z = *reinterpret_cast<const u32x4_t*>(qvec + hh * kHalf + 8 * c);
             // (both lanes of a pair hold the same column, and zeros rotate to zeros)
             if constexpr (kRot)
-                z = rope_rotate(z, other_half(z, hh), hh, uint32_t(q_pos), &p.rope_rho_hi[8 * c],
+                z = rope::rotate(z, rope::other_half(z, hh), hh, uint32_t(q_pos), &p.rope_rho_hi[8 * c],
                                 &p.rope_rho_lo[8 * c]);
             qf[c] = z;
         }
@@ -404,7 +350,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
             // same token).  Angle of (t0 + col, r) by angle addition: lane r evaluates
             // the block's t0 * theta_r once and leaves its cosine and sine in the wave's
             // LDS row; every lane reads those of its chunk's 8 pairs and col * theta_r from LDS.
-            const float ub = rope_revolutions(uint32_t(t0), my_rho);
+            const float ub = rope::revolutions(uint32_t(t0), my_rho);
             float* blk = &s_blkcs[wave * 2 * kHalf];
             if (lane < kHalf) {
                 blk[2 * lane] = __builtin_amdgcn_cosf(ub);
@@ -435,7 +381,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void decode_split_kernel(const Deco
                             sn8[e] = __builtin_fmaf(sB, cC, cB * sC);
                         }
                     }
-                    kf[c] = rope_rotate_cs(kf[c], other_half(kf[c], hh), hh, cs8, sn8);
+                    kf[c] = rope::rotate_cs(kf[c], rope::other_half(kf[c], hh), hh, cs8, sn8);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }

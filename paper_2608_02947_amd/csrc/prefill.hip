@@ -59,6 +59,7 @@
 // normaliser need no rescaling -- the result is the same softmax.  Row sums add
 // the fp32 probabilities; the PV MFMA consumes them rounded to bf16.
 #include "atf_internal.hpp"
+#include "rope.hpp"
 
 #include <type_traits>
 
@@ -160,14 +161,31 @@ __device__ __forceinline__ void vm_wait() { __builtin_amdgcn_s_waitcnt(0x0F70); 
 // for) before it, and the direct-to-LDS loads are awaited with vm_wait
 __device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
 
+// LDS of the rotation tables of the kernels that rotate at read time (dynamic, bytes)
+template <int D, bool kWin>
+struct RotLds {
+    static constexpr int kColStride = D + 4;
+    static constexpr unsigned kBytes =
+        unsigned(32 * kColStride + Cfg<D, kWin>::kWaves * Cfg<D, kWin>::kKPerWave * 16 + D) * 4u;
+};
+
 // Two waves per SIMD (one workgroup per CU): the windowed kernel's registers
 // exceed the 128 that four waves per SIMD would leave each wave, even at d = 64.
-template <int D, bool kWin>
+template <int D, bool kWin, bool kRot>
 __global__ __launch_bounds__((Cfg<D, kWin>::kThreads), (Cfg<D, kWin>::kMinWavesPerSimd)) void
-prefill_kernel(const PrefillParams p) {
+prefill_kernel(const std::conditional_t<kRot, PrefillRotParams, PrefillParams> p) {
     using C = Cfg<D, kWin>;
     __shared__ __attribute__((aligned(16))) uint16_t Ks[C::kStages][C::kKTile];
     __shared__ __attribute__((aligned(16))) uint16_t Vs[C::kStages][C::kVTile];
+    // rotation at read time (dynamic LDS, after the static buffers): cos and sin of
+    // kk * theta_r for the 32 key offsets of a 32-key block (row kk: pairs interleaved
+    // as (cos, sin), padded by 16 bytes), then per wave and K unit the cos and sin of
+    // the block's first position * theta_r, then rho_r (hi, lo) of every pair
+    constexpr int kColStride = RotLds<D, kWin>::kColStride;
+    extern __shared__ __attribute__((aligned(16))) float s_rot[];
+    float* const s_colcs = s_rot;
+    float* const s_base = s_rot + 32 * kColStride;
+    uint2* const s_rho = reinterpret_cast<uint2*>(s_base + C::kWaves * C::kKPerWave * 16);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -226,6 +244,10 @@ prefill_kernel(const PrefillParams p) {
         for (int c = 0; c < C::kChunks; ++c) {
             u32x4_t z = {0u, 0u, 0u, 0u};
             if (row_ok) z = *reinterpret_cast<const u32x4_t*>(qrow + 8 * c);
+            // an unrotated query is turned to its position here, once
+            if constexpr (kRot)
+                z = rope::rotate(z, rope::other_half(z, hh), hh, uint32_t(my_pos), &p.rope_rho_hi[8 * c],
+                                 &p.rope_rho_lo[8 * c]);
             qf[c] = z;
         }
     }
@@ -267,7 +289,8 @@ prefill_kernel(const PrefillParams p) {
             kfirst[t] = num <= 0 ? 0 : int(min(int64_t(INT32_MAX), (num + kBN - 1) / kBN));
         }
     }
-    auto issue_fast = [&](int j0, int buf) __attribute__((always_inline)) {
+    auto issue_fast = [&](int j0, int buf) __attribute__((always_inline)) -> uint32_t {
+        uint32_t loaded = 0;
         const int tn = j0 / kBN;
         const int64_t koff = int64_t(j0) * 32;
         const int64_t voff = int64_t(j0) * (2 * D);
@@ -275,7 +298,10 @@ prefill_kernel(const PrefillParams p) {
 #pragma unroll
         for (int t = 0; t < C::kKPerWave; ++t) {
             const int u = wave + C::kWaves * t;
-            if (tn >= kfirst[t]) load_to_lds(kbase[t] + koff, k_piece, kdst + 1024u * u);
+            if (tn >= kfirst[t]) {
+                load_to_lds(kbase[t] + koff, k_piece, kdst + 1024u * u);
+                loaded |= 1u << t;
+            }
         }
         const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
 #pragma unroll
@@ -285,12 +311,12 @@ prefill_kernel(const PrefillParams p) {
                 if (u >= C::kVLoads) break;
             load_to_lds(vhead + voff + 1024 * u, uint32_t(lane) * 16u, vdst + 1024u * u);
         }
+        return loaded;
     };
-    auto issue = [&](int j0, int buf) __attribute__((always_inline)) {
-        if (j0 + kBN <= p.n_k) {
-            issue_fast(j0, buf);
-            return;
-        }
+    // returns the K units (bit t: unit wave + kWaves t) this wave loaded
+    auto issue = [&](int j0, int buf) __attribute__((always_inline)) -> uint32_t {
+        if (j0 + kBN <= p.n_k) return issue_fast(j0, buf);
+        uint32_t loaded = 0;
         const uint32_t need = tile_need(j0);
         const uint32_t kdst = ks_lds + uint32_t(buf * C::kKTile * 2);
 #pragma unroll
@@ -303,6 +329,7 @@ prefill_kernel(const PrefillParams p) {
                 if (jb + 32 > p.n_k)
                     off = min(uint32_t(lane & 31), uint32_t(p.n_k - 1 - jb)) * 32u + uint32_t(lane >> 5) * 16u;
                 load_to_lds(kpcm + c * chunk_bytes + int64_t(jb) * 32, off, kdst + 1024u * u);
+                loaded |= 1u << t;
             }
         }
         const uint32_t vdst = vs_lds + uint32_t(buf * C::kVTile * 2);
@@ -314,6 +341,75 @@ prefill_kernel(const PrefillParams p) {
             load_to_lds(vhead + int64_t(blk) * C::kVBlkBytes + (1024 * u) % C::kVBlkBytes,
                         uint32_t(lane) * 16u, vdst + 1024u * u);
         }
+        return loaded;
+    };
+
+    // ---- rotation at read time: each wave turns the K units it loaded, once they have
+    // landed and before the barrier that publishes the tile, so each kept (key, pair) of
+    // the workgroup's tile is rotated once and pruned chunks (never loaded) never are.
+    // Lane l turns 4 pairs (half l / 32 of the unit's 8) of key l % 32: both components
+    // from the unit's two halves, angle (block start + l % 32) * theta_r by angle
+    // addition of the block start's angle (lanes 0..7, one pair each) and the offset's
+    // (the table).
+    auto rotate_units = [&](int j0, int buf, uint32_t loaded) __attribute__((always_inline)) {
+        loaded = __builtin_amdgcn_readfirstlane(loaded);
+#pragma unroll
+        for (int t = 0; t < C::kKPerWave; ++t) {
+            if (!((loaded >> t) & 1u)) continue;
+            const int u = wave + C::kWaves * t;
+            const int c = u >> 1;
+            const uint32_t jb = uint32_t(j0 + 32 * (u & 1));
+            float* sb = &s_base[(wave * C::kKPerWave + t) * 16];
+            if (lane < 8) {
+                const float ub = rope::revolutions(jb, s_rho[8 * c + lane]);
+                sb[2 * lane] = __builtin_amdgcn_cosf(ub);
+                sb[2 * lane + 1] = __builtin_amdgcn_sinf(ub);
+            }
+            // the wave's own LDS writes complete before its later LDS reads; the fences
+            // keep the compiler from moving the reads above the writes
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const int kk = lane & 31, gq = lane >> 5;
+            const uint32_t a0 = ks_lds + uint32_t(buf * C::kKTile * 2) + 1024u * u + uint32_t(kk * 16 + gq * 8);
+            typedef __attribute__((address_space(3))) uint64_t lds_u64;
+            const uint64_t xv = *(const lds_u64*)(uintptr_t)a0;
+            const uint64_t yv = *(const lds_u64*)(uintptr_t)(a0 + 512u);
+            const float4 cc0 = *reinterpret_cast<const float4*>(&s_colcs[kk * kColStride + 2 * (8 * c + 4 * gq)]);
+            const float4 cc1 = *reinterpret_cast<const float4*>(&s_colcs[kk * kColStride + 2 * (8 * c + 4 * gq) + 4]);
+            const float4 bb0 = *reinterpret_cast<const float4*>(&sb[8 * gq]);
+            const float4 bb1 = *reinterpret_cast<const float4*>(&sb[8 * gq + 4]);
+            const float cC[4] = {cc0.x, cc0.z, cc1.x, cc1.z}, sC[4] = {cc0.y, cc0.w, cc1.y, cc1.w};
+            const float cB[4] = {bb0.x, bb0.z, bb1.x, bb1.z}, sB[4] = {bb0.y, bb0.w, bb1.y, bb1.w};
+            uint32_t xo[2], yo[2];
+#pragma unroll
+            for (int w2 = 0; w2 < 2; ++w2) {
+                const uint32_t xw = uint32_t(xv >> (32 * w2)), yw = uint32_t(yv >> (32 * w2));
+                rope::bf16x2_t xt, yt;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int e = 2 * w2 + h;
+                    const float cs = __builtin_fmaf(cB[e], cC[e], -sB[e] * sC[e]);
+                    const float sn = __builtin_fmaf(sB[e], cC[e], cB[e] * sC[e]);
+                    const float x = __uint_as_float(h ? (xw & 0xFFFF0000u) : (xw << 16));
+                    const float y = __uint_as_float(h ? (yw & 0xFFFF0000u) : (yw << 16));
+                    xt[h] = (__bf16)rope::turn(x, y, -1.f, cs, sn);
+                    yt[h] = (__bf16)rope::turn(y, x, 1.f, cs, sn);
+                }
+                xo[w2] = __builtin_bit_cast(uint32_t, xt);
+                yo[w2] = __builtin_bit_cast(uint32_t, yt);
+            }
+            *(lds_u64*)(uintptr_t)a0 = uint64_t(xo[0]) | (uint64_t(xo[1]) << 32);
+            *(lds_u64*)(uintptr_t)(a0 + 512u) = uint64_t(yo[0]) | (uint64_t(yo[1]) << 32);
+        }
+        // the rotated units are complete in LDS before the workgroup barrier, and the
+        // fence keeps the compiler from sinking the writes below it
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    };
+    // after the barrier: no LDS read of a rotated unit moves above it
+    auto rotated_acquire = [&]() __attribute__((always_inline)) {
+        if constexpr (kRot) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     };
 
     // per-lane LDS byte bases of the fragment reads (buffer 0, block 0)
@@ -508,21 +604,39 @@ prefill_kernel(const PrefillParams p) {
     const int n_tiles = (key_end + kBN - 1) / kBN;
     auto active = [&](int tile) __attribute__((always_inline)) { return wave_active && wp_max >= tile * kBN; };
     // one tile: stage the next, compute this one (if the wave has rows there),
-    // await this wave's loads of the next tile, barrier
+    // await this wave's loads of the next tile (and rotate them, for unrotated
+    // caches), barrier
     auto run_tile = [&](int u, auto&& qk) __attribute__((always_inline)) {
-        if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
+        uint32_t loaded = 0;
+        if (u + 1 < n_tiles) loaded = issue((u + 1) * kBN, (u + 1) % C::kStages);
         zero_v_tail(u);
         if (active(u)) {
             qk(u);
             softmax_pv(u);
         }
         vm_wait();
+        if constexpr (kRot) rotate_units((u + 1) * kBN, (u + 1) % C::kStages, loaded);
         barrier();
+        rotated_acquire();
     };
 
-    issue(0, 0);
-    vm_wait();
-    barrier();
+    if constexpr (kRot) {
+        for (int idx = tid; idx < 32 * C::kHalf; idx += C::kThreads) {
+            const int kk = idx / C::kHalf, r = idx % C::kHalf;
+            const float u = rope::revolutions(uint32_t(kk), make_uint2(p.rope_rho_hi[r], p.rope_rho_lo[r]));
+            s_colcs[kk * kColStride + 2 * r] = __builtin_amdgcn_cosf(u);
+            s_colcs[kk * kColStride + 2 * r + 1] = __builtin_amdgcn_sinf(u);
+        }
+        if (tid < C::kHalf) s_rho[tid] = make_uint2(p.rope_rho_hi[tid], p.rope_rho_lo[tid]);
+        __syncthreads();
+    }
+    {
+        const uint32_t loaded = issue(0, 0);
+        vm_wait();
+        if constexpr (kRot) rotate_units(0, 0, loaded);
+        barrier();
+        rotated_acquire();
+    }
 
     if constexpr (!kWin) {
         // window off: every tile is the full contraction
@@ -599,10 +713,13 @@ prefill_kernel(const PrefillParams p) {
                 break;
             default:  // idle: keep the barrier count
                 for (; u < seg_end; ++u) {
-                    if (u + 1 < n_tiles) issue((u + 1) * kBN, (u + 1) % C::kStages);
+                    uint32_t loaded = 0;
+                    if (u + 1 < n_tiles) loaded = issue((u + 1) * kBN, (u + 1) % C::kStages);
                     zero_v_tail(u);
                     vm_wait();
+                    if constexpr (kRot) rotate_units((u + 1) * kBN, (u + 1) % C::kStages, loaded);
                     barrier();
+                    rotated_acquire();
                 }
                 break;
         }
@@ -630,43 +747,66 @@ prefill_kernel(const PrefillParams p) {
             m_run * 0.69314718055994531f + logf(l_tot);
 }
 
-template <int D>
-hipError_t launch_d(const PrefillParams& p, unsigned blocks, bool window_on, hipStream_t stream) {
+template <int D, bool kRot, class P>
+hipError_t launch_d(const P& p, unsigned blocks, bool window_on, hipStream_t stream) {
+    constexpr unsigned kLdsOn = kRot ? RotLds<D, true>::kBytes : 0u;
+    constexpr unsigned kLdsOff = kRot ? RotLds<D, false>::kBytes : 0u;
     if (window_on)
-        hipLaunchKernelGGL((prefill_kernel<D, true>), dim3(blocks), dim3(Cfg<D, true>::kThreads), 0,
-                           stream, p);
+        hipLaunchKernelGGL((prefill_kernel<D, true, kRot>), dim3(blocks), dim3(Cfg<D, true>::kThreads),
+                           kLdsOn, stream, p);
     else
-        hipLaunchKernelGGL((prefill_kernel<D, false>), dim3(blocks), dim3(Cfg<D, false>::kThreads),
-                           0, stream, p);
+        hipLaunchKernelGGL((prefill_kernel<D, false, kRot>), dim3(blocks),
+                           dim3(Cfg<D, false>::kThreads), kLdsOff, stream, p);
     return hipGetLastError();
+}
+
+// Tile geometry and the uniform-run test, shared by both launchers.
+template <class P>
+hipError_t prepare(P& p, int head_dim, unsigned* blocks, bool* window_on) {
+    // the window is off when no threshold is below the largest possible distance;
+    // the uniform-run path needs thresholds non-decreasing in r and the last chunk
+    // kept at every distance of the call
+    const int64_t max_dist = int64_t(p.q_pos0) + p.n_q - 1;
+    bool on = false;
+    for (int r = 0; r < head_dim / 2; ++r)
+        if (int64_t(p.win.W[r]) < max_dist) on = true;
+    bool mono = int64_t(p.win.W[head_dim / 2 - kChunkPairs]) >= max_dist;
+    for (int r = 1; r < head_dim / 2; ++r)
+        if (p.win.W[r] < p.win.W[r - 1]) mono = false;
+    p.mono = mono ? 1 : 0;
+    const int rows = head_dim == 64 ? (on ? Cfg<64, true>::kRows : Cfg<64, false>::kRows)
+                                    : (on ? Cfg<128, true>::kRows : Cfg<128, false>::kRows);
+    if (p.group < 1 || p.group > rows) return hipErrorInvalidValue;
+    p.pos_per_tile = rows / p.group;
+    p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
+    const int64_t n = int64_t(p.n_qtiles) * p.h_kv * p.batch;
+    if (n <= 0 || n > 0x7fffffff) return hipErrorInvalidConfiguration;
+    *blocks = unsigned(n);
+    *window_on = on;
+    (void)hipGetLastError();
+    return hipSuccess;
 }
 
 }  // namespace
 
 hipError_t launch_prefill(const PrefillParams& p_in, int head_dim, hipStream_t stream) {
     PrefillParams p = p_in;
-    // the window is off when no threshold is below the largest possible distance;
-    // the uniform-run path needs thresholds non-decreasing in r and the last chunk
-    // kept at every distance of the call
-    const int64_t max_dist = int64_t(p.q_pos0) + p.n_q - 1;
+    unsigned blocks = 0;
     bool window_on = false;
-    for (int r = 0; r < head_dim / 2; ++r)
-        if (int64_t(p.win.W[r]) < max_dist) window_on = true;
-    bool mono = int64_t(p.win.W[head_dim / 2 - kChunkPairs]) >= max_dist;
-    for (int r = 1; r < head_dim / 2; ++r)
-        if (p.win.W[r] < p.win.W[r - 1]) mono = false;
-    p.mono = mono ? 1 : 0;
-    const int rows = head_dim == 64
-                         ? (window_on ? Cfg<64, true>::kRows : Cfg<64, false>::kRows)
-                         : (window_on ? Cfg<128, true>::kRows : Cfg<128, false>::kRows);
-    if (p.group < 1 || p.group > rows) return hipErrorInvalidValue;
-    p.pos_per_tile = rows / p.group;
-    p.n_qtiles = (p.n_q + p.pos_per_tile - 1) / p.pos_per_tile;
-    const int64_t blocks = int64_t(p.n_qtiles) * p.h_kv * p.batch;
-    if (blocks <= 0 || blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
-    (void)hipGetLastError();
-    return head_dim == 64 ? launch_d<64>(p, unsigned(blocks), window_on, stream)
-                          : launch_d<128>(p, unsigned(blocks), window_on, stream);
+    const hipError_t e = prepare(p, head_dim, &blocks, &window_on);
+    if (e != hipSuccess) return e;
+    return head_dim == 64 ? launch_d<64, false>(p, blocks, window_on, stream)
+                          : launch_d<128, false>(p, blocks, window_on, stream);
+}
+
+hipError_t launch_prefill_rotating(const PrefillRotParams& p_in, int head_dim, hipStream_t stream) {
+    PrefillRotParams p = p_in;
+    unsigned blocks = 0;
+    bool window_on = false;
+    const hipError_t e = prepare(p, head_dim, &blocks, &window_on);
+    if (e != hipSuccess) return e;
+    return head_dim == 64 ? launch_d<64, true>(p, blocks, window_on, stream)
+                          : launch_d<128, true>(p, blocks, window_on, stream);
 }
 
 }  // namespace atf

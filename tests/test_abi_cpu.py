@@ -475,6 +475,38 @@ def test_unrotated_validation_before_launch():
         assert "decode_paged_unrotated" in atf.atf_last_error()
 
 
+def test_prefill_unrotated_validation_before_launch():
+    """atf_prefill_unrotated checks the rotation frequencies with the window, before the
+    n_q == 0 no-op and before any launch; the pre-rotated checks apply unchanged."""
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    good = [1e4 ** (-2.0 * r / 128) for r in range(64)]
+    keep_f = []
+
+    def pre(f=None, n_q=0, q=16, h_q=8):
+        fp = None
+        if f is not None:
+            arr = (ctypes.c_double * len(f))(*f)
+            keep_f.append(arr)
+            fp = ctypes.cast(arr, ctypes.c_void_p)
+        return lib.atf_prefill_unrotated(q, 16, 16, 16, 16, 1, n_q, 1000, 0, h_q, 2, 1000,
+                                         ctypes.byref(w), fp, 0.0, None)
+
+    assert pre(good) == atf.ATF_OK       # n_q = 0: validated, then a no-op
+    assert pre() == atf.ATF_OK           # the window's frequencies
+    for bad in (-1.0, float("inf"), float("nan")):
+        f = list(good)
+        f[7] = bad
+        assert pre(f) == atf.ATF_EINVAL
+        assert "prefill_unrotated" in atf.atf_last_error()
+    assert pre(good, n_q=10, q=17) == atf.ATF_EINVAL      # misaligned q
+    assert "prefill_unrotated" in atf.atf_last_error()
+    assert pre(good, n_q=10, h_q=7) == atf.ATF_EINVAL     # h_q not a multiple of h_kv
+    w64, keep64 = atf.Window(96, 1e4, 2.0).as_c()
+    assert lib.atf_prefill_unrotated(16, 16, 16, 16, 16, 1, 1, 10, 0, 2, 1, 10,
+                                     ctypes.byref(w64), None, 0.0, None) == atf.ATF_EUNSUPPORTED
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

@@ -1,8 +1,8 @@
-"""GPU parity of decode from UNROTATED caches (RoPE applied at read time, App. B)
-through the C ABI: atf_decode_unrotated and atf_decode_paged_unrotated against the
-oracle, which rotates the same bf16 query and keys in fp64 (oracle.rope_rotate, pinned
-in test_oracle_rope.py), stores them in bf16 as a pre-rotated cache would, and attends
-them in fp64."""
+"""GPU parity of prefill and decode from UNROTATED caches (RoPE applied at read time,
+App. B) through the C ABI: atf_prefill_unrotated, atf_decode_unrotated and its ragged
+and paged forms against the oracle, which rotates the same bf16 queries and keys in fp64
+(oracle.rope_rotate, pinned in test_oracle_rope.py), stores them in bf16 as a
+pre-rotated cache would, and attends them in fp64."""
 import math
 
 import numpy as np
@@ -12,7 +12,8 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import compare, note, pack_kcache, pack_vcache, to_f64, windows_for
+from parity import (bench_rows, compare, gpu_prefill, note, pack_kcache, pack_vcache,
+                    table_windows, to_f64, windows_for)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs an MI355X (gfx950) GPU")]
@@ -229,3 +230,214 @@ def test_decode_unrotated_against_exact_rotation(case):
     kr = torch.from_numpy(oracle.rope_rotate(k, np.arange(n_k), theta))
     o_ref, lse_ref, _ = oracle.attend(qr, kr, v.to(torch.float64), q_pos, widths)
     compare(to_f64(o), to_f64(lse), o_ref[:, 0], lse_ref[:, :, 0], f"exact rotation {case}")
+
+
+# ---- prefill from unrotated caches ----
+
+def _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed):
+    """Unrotated bf16 queries, keys and values of a prefill."""
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    q = torch.randn((B, n_q, h_q, d), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, n_k, h_kv, d), generator=g).to(torch.bfloat16)
+    return q, k, v
+
+
+def _rotated_bf16(q, k, q0, theta):
+    """The oracle's fp64 rotation (query row i at q0 + i, key j at j), rounded to bf16
+    as a pre-rotated cache holds it."""
+    n_q, n_k = q.shape[1], k.shape[1]
+    qr = torch.from_numpy(oracle.rope_rotate(q, np.arange(q0, q0 + n_q), theta)).to(torch.bfloat16)
+    kr = torch.from_numpy(oracle.rope_rotate(k, np.arange(n_k), theta)).to(torch.bfloat16)
+    return qr, kr
+
+
+def _gpu_prefill_unrotated(q, k, v, q0, win, rope_inv_freq=None, kp=None, vp=None, n_k=None):
+    import paper_2608_02947_amd as atf
+    qd = q.contiguous().to(DEV)
+    if kp is None:
+        kp, vp = pack_kcache(k.to(DEV)), pack_vcache(v.to(DEV))
+    B, n_q, h_q, d = qd.shape
+    o = torch.empty_like(qd)
+    lse = torch.empty((B, h_q, n_q), dtype=torch.float32, device=DEV)
+    atf.atf_prefill_unrotated(qd, kp, vp, o, lse, q0, win, rope_inv_freq=rope_inv_freq, n_k=n_k)
+    torch.cuda.synchronize()
+    return o, lse
+
+
+PREFILL_CASES = [
+    # B, n_q, n_k, q0, h_q, h_kv, d, base, k
+    (1, 300, 300, 0, 6, 2, 128, 5e5, 2.0),
+    (2, 45, 45, 0, 4, 4, 64, 1e6, 2.0),                  # partial wave, MHA
+    (1, 77, 267, 190, 7, 1, 64, 1e6, 2.0),               # chunk at the end of a longer context
+    (1, 200, 150, 0, 8, 1, 128, 1e4, 2.0),               # keys end before the last query
+    (1, 1, 1, 0, 2, 1, 128, 1e4, 2.0),                   # one row, one key
+    (1, 257, 257, 0, 3, 3, 128, 100.0, 2.0),             # saturated: every window ends early
+    (1, 256, 256, 0, 2, 1, 128, 1e4, math.inf),          # window off, d = 128
+    (1, 200, 200, 0, 4, 1, 64, 1e4, math.inf),           # window off, d = 64
+    (1, 333, 500, 167, 16, 2, 64, 1e4, 1.0),             # G = 8, ragged tail
+    (2, 130, 1000, 870, 12, 1, 128, 1e4, 2.0),           # G = 12
+    (1, 520, 4100, 3580, 8, 2, 128, 1e7, 2.0),           # many tiles, chunks pruned by tile
+    (1, 64, 700, (1 << 30) + 5, 4, 1, 128, 1e4, math.inf),  # queries at 2^30 + 5 ..
+]
+
+
+@pytest.mark.parametrize("case", PREFILL_CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_unrotated(case):
+    B, n_q, n_k, q0, h_q, h_kv, d, base, kwin = case
+    note(f"prefill unrotated {case}")
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=(hash(case) + 3) % 10000)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=q0 + n_q)
+    o, lse = _gpu_prefill_unrotated(q, k, v, q0, win)
+    qr, kr = _rotated_bf16(q, k, q0, W.rope_theta(d, base).numpy())
+    o_ref, lse_ref, _ = oracle.attend(qr, kr, v, q0, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, f"prefill unrotated {case}")
+
+
+@pytest.mark.parametrize("case", [PREFILL_CASES[0], PREFILL_CASES[2], PREFILL_CASES[10]],
+                         ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_unrotated_matches_prerotated_cache(case):
+    """The same attention through atf_prefill over caches the oracle rotated and rounded
+    to bf16: the two paths differ only where a rotated element's bf16 rounding falls on
+    the other side (fp32 rotation versus fp64), so every output element agrees to within
+    one bf16 rounding of itself plus 2e-3, and the LSE to 2e-4."""
+    B, n_q, n_k, q0, h_q, h_kv, d, base, kwin = case
+    note(f"prefill unrotated vs pre-rotated {case}")
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=(hash(case) + 5) % 10000)
+    win, _ = windows_for(d, base, kwin, None, n_ctx=q0 + n_q)
+    o, lse = _gpu_prefill_unrotated(q, k, v, q0, win)
+    qr, kr = _rotated_bf16(q, k, q0, W.rope_theta(d, base).numpy())
+    o2, lse2 = gpu_prefill(qr.to(DEV), kr.to(DEV), v.to(DEV), q0, win)
+    a, b = o.double(), o2.double()
+    # within one bf16 rounding of the output (2^-7 relative at most) plus the scores'
+    # perturbation by the rotation's rounding flips
+    excess = float(((a - b).abs() - (2.0 ** -7 * torch.maximum(a.abs(), b.abs()) + 2e-3)).max())
+    ml = float((lse - lse2).abs().max())
+    same = float((o == o2).float().mean())
+    print(f"[parity] unrotated vs pre-rotated {case}: bit-identical O {same:.4f}, "
+          f"LSE max-abs {ml:.2e}", flush=True)
+    assert excess <= 0.0 and ml <= 2e-4, (case, excess, ml)
+
+
+PREFILL_EXACT_CASES = [
+    # B, n_q, n_k, q0, h_q, h_kv, d, base, k: rows of thousands of keys
+    (1, 256, 4096, 3840, 8, 2, 128, 1e4, 2.0),
+    (1, 128, 8192, 8064, 14, 2, 64, 1e6, 2.0),
+    (1, 128, 4096, 3968, 4, 1, 128, 1e4, math.inf),
+]
+
+
+@pytest.mark.parametrize("case", PREFILL_EXACT_CASES, ids=lambda c: "x".join(str(x) for x in c))
+def test_prefill_unrotated_against_exact_rotation(case):
+    """Against attention over the EXACTLY rotated vectors (fp64, not rounded to bf16):
+    the read-time rotation strays from it no further than a pre-rotated bf16 cache does.
+    The oracle's attention over its own correctly rounded bf16 rotation measures that
+    cache's distance from the exact result; the kernel's may exceed it by at most half
+    the fixed tolerances (its own fp32 and bf16 arithmetic).  Over a whole prefill the
+    LSE error of the bf16 rounding alone reaches ~1e-3 on some rows (the LSE follows the
+    largest scores, whose rounding shifts do not average out), so the fixed LSE
+    tolerance is not the right yardstick here."""
+    B, n_q, n_k, q0, h_q, h_kv, d, base, kwin = case
+    note(f"prefill unrotated vs exact rotation {case}")
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=(hash(case) + 9) % 10000)
+    win, widths = windows_for(d, base, kwin, None, n_ctx=q0 + n_q)
+    o, lse = _gpu_prefill_unrotated(q, k, v, q0, win)
+    theta = W.rope_theta(d, base).numpy()
+    qr = oracle.rope_rotate(q, np.arange(q0, q0 + n_q), theta)
+    kr = oracle.rope_rotate(k, np.arange(n_k), theta)
+    vv = v.to(torch.float64).numpy()
+    o_ex, lse_ex, _ = oracle.attend(qr, kr, vv, q0, widths)
+    q16, k16 = (torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy() for x in (qr, kr))
+    o_16, lse_16, _ = oracle.attend(q16, k16, vv, q0, widths)
+    og, lg = to_f64(o), to_f64(lse)
+    e16 = (np.abs(o_16 - o_ex).max(), np.abs(o_16 - o_ex).mean(), np.abs(lse_16 - lse_ex).max())
+    eg = (np.abs(og - o_ex).max(), np.abs(og - o_ex).mean(), np.abs(lg - lse_ex).max())
+    print(f"[parity] exact rotation {case}: bf16 cache O max {e16[0]:.2e} mean {e16[1]:.2e} "
+          f"LSE {e16[2]:.2e}; kernel O max {eg[0]:.2e} mean {eg[1]:.2e} LSE {eg[2]:.2e}",
+          flush=True)
+    assert np.all(np.isfinite(og)) and np.all(np.isfinite(lg))
+    assert eg[0] <= e16[0] + 5e-3, (case, eg, e16)
+    assert eg[1] <= e16[1] + 5e-4, (case, eg, e16)
+    assert eg[2] <= e16[2] + 5e-4, (case, eg, e16)
+
+
+def test_prefill_unrotated_chunked_equals_single_shot():
+    """A prefill in three chunks (rows a .. b - 1 against keys 0 .. b - 1 of the same
+    caches, capacity larger than the keys used) gives the single-shot result bit for
+    bit: a key's angle depends only on its position, not on the chunk that reads it.
+    Chunk boundaries are multiples of the position tile (floor(256 / G) = 64)."""
+    B, n, h_q, h_kv, d, base = 1, 700, 8, 2, 128, 1e6
+    q, k, v = _prefill_inputs(B, n, n + 100, h_q, h_kv, d, seed=123)
+    win, _ = windows_for(d, base, 2.0, None, n_ctx=n)
+    kp, vp = pack_kcache(k.to(DEV)), pack_vcache(v.to(DEV))
+    note("prefill unrotated single shot")
+    o1, l1 = _gpu_prefill_unrotated(q, None, None, 0, win, kp=kp, vp=vp, n_k=n)
+    for a, b in [(0, 128), (128, 448), (448, 700)]:
+        note(f"prefill unrotated chunk {a}..{b}")
+        o2, l2 = _gpu_prefill_unrotated(q[:, a:b], None, None, a, win, kp=kp, vp=vp, n_k=b)
+        assert torch.equal(o2, o1[:, a:b]) and torch.equal(l2, l1[:, :, a:b]), (a, b)
+
+
+def test_prefill_unrotated_llama_frequencies():
+    """Llama-3.2-3B shape with the llama3-effective frequencies: rotation from the
+    window's own table, and from an explicit table under a raw-base window."""
+    wl = W.WORKLOADS["llama3b_decode_32k"]
+    d, n = wl.head_dim, 1500
+    th = W.workload_theta(wl).numpy()
+    q, k, v = _prefill_inputs(1, n, n, wl.h_q, wl.h_kv, d, seed=wl.seed + 3)
+    qr, kr = _rotated_bf16(q, k, 0, th)
+    note("prefill unrotated llama effective table")
+    win, widths = windows_for(d, wl.rope_base, wl.k, th, n_ctx=n)
+    o, lse = _gpu_prefill_unrotated(q, k, v, 0, win)
+    o_ref, lse_ref, _ = oracle.attend(qr, kr, v, 0, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "prefill llama effective")
+    note("prefill unrotated llama raw-base window, effective rotation")
+    win, widths = windows_for(d, wl.rope_base, wl.k, None, n_ctx=n)
+    o, lse = _gpu_prefill_unrotated(q, k, v, 0, win, rope_inv_freq=th)
+    o_ref, lse_ref, _ = oracle.attend(qr, kr, v, 0, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "prefill llama raw window")
+
+
+def test_prefill_unrotated_deterministic():
+    q, k, v = _prefill_inputs(1, 600, 2000, 8, 2, 128, seed=43)
+    win, _ = windows_for(128, 1e4, 2.0, None, n_ctx=2000)
+    note("prefill unrotated determinism")
+    o1, l1 = _gpu_prefill_unrotated(q, k, v, 1400, win)
+    o2, l2 = _gpu_prefill_unrotated(q, k, v, 1400, win)
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+@pytest.mark.parametrize("kwin", [2.0, math.inf], ids=["default", "kinf"])
+def test_prefill_unrotated_qwen7b1m_chunk_sampled_rows(kwin):
+    """The benchmark's 1M prefill chunk (131,072 query rows at positions 917,504 ..
+    1,048,575 over keys 0 .. 1,048,575; 28 query heads / 4 KV heads, d = 128, base 1e7)
+    from unrotated caches, in the launch configuration the benchmark times: the
+    stratified sample of rows of the pre-rotated test, recomputed by the oracle from its
+    own fp64 rotation."""
+    wl = W.WORKLOADS["qwen7b1m_prefill_chunk"]
+    d = wl.head_dim
+    note(f"generate qwen7b1m_prefill_chunk unrotated, k={kwin}")
+    inp = W.make_inputs(wl, device=DEV, rotated=False)
+    kp, vp = pack_kcache(inp["k"]), pack_vcache(inp["v"])
+    win, widths, _ = table_windows(wl, "default" if kwin == 2.0 else "kinf")
+    rows = bench_rows(wl, widths)
+    assert len(rows) >= 256 and set(rows[:, 1].tolist()) == set(range(wl.h_q))
+    note(f"prefill unrotated qwen7b1m chunk k={kwin}: {len(rows)} sampled rows")
+    o, lse = _gpu_prefill_unrotated(inp["q"], None, None, wl.q_pos0, win, kp=kp, vp=vp)
+    idx = torch.from_numpy(rows).to(DEV)
+    og = to_f64(o[idx[:, 0], idx[:, 2], idx[:, 1]])
+    lg = to_f64(lse[idx[:, 0], idx[:, 1], idx[:, 2]])
+    del o, lse, kp, vp
+    # the oracle rotates the sampled query rows and every key
+    theta = W.rotation_theta(wl).numpy()
+    qs = inp["q"][:, np.unique(rows[:, 2])].cpu()
+    uniq = np.unique(rows[:, 2])
+    qr = torch.from_numpy(oracle.rope_rotate(qs, wl.q_pos0 + uniq, theta)).to(torch.bfloat16)
+    q_full = torch.zeros((wl.batch, wl.n_q, wl.h_q, d), dtype=torch.bfloat16)
+    q_full[:, uniq] = qr
+    kr = torch.from_numpy(oracle.rope_rotate(inp["k"].cpu(), np.arange(wl.n_k), theta)).to(
+        torch.bfloat16)
+    o_ref, lse_ref, _ = oracle.attend(q_full, kr, inp["v"].cpu(), wl.q_pos0, widths, rows=rows)
+    mx, mean, ml = compare(og, lg, o_ref, lse_ref, f"prefill unrotated qwen7b1m k={kwin}")
+    print(f"[parity] prefill unrotated qwen7b1m k={kwin}: O max {mx:.2e} mean {mean:.2e} "
+          f"LSE {ml:.2e}", flush=True)

@@ -113,7 +113,10 @@ def test_exec_mask_check_finds_a_masked_mfma():
 def test_kernels_do_not_spill(tmp_path, src):
     """No kernel spills vector registers to scratch, and scalar spills (into vector
     register lanes, a v_writelane/v_readlane pair each) stay a handful: a mask or
-    loop that keeps many lane masks live at once shows up here first."""
+    loop that keeps many lane masks live at once shows up here first.  The prefill
+    kernels that rotate unrotated caches (third template argument true) hold the
+    rotation's scalar state beside the rest and may spill up to 16 (their reloads sit
+    in the prologue and epilogue; the windowed d = 64 one adds two per tile)."""
     out = tmp_path / (src + ".o")
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
@@ -136,4 +139,5 @@ def test_kernels_do_not_spill(tmp_path, src):
     assert kernels
     for k, v in kernels.items():
         assert v.get("VGPRs Spill", 0) == 0 and v.get("ScratchSize [bytes/lane]", 0) == 0, (k, v)
-        assert v.get("SGPRs Spill", 0) <= 8, (k, v)
+        rotating = re.search(r"prefill_kernelILi\d+ELb[01]ELb1E", k) is not None
+        assert v.get("SGPRs Spill", 0) <= (16 if rotating else 8), (k, v)

@@ -152,12 +152,15 @@ def _gen(seed: int, device) -> torch.Generator:
 
 
 def make_inputs(w: Workload, device="cpu", seed: Optional[int] = None, n_k: Optional[int] = None,
-                n_q: Optional[int] = None, q_pos0: Optional[int] = None, batch: Optional[int] = None):
+                n_q: Optional[int] = None, q_pos0: Optional[int] = None, batch: Optional[int] = None,
+                rotated: bool = True):
     """Seeded bf16 inputs of workload ``w`` (sizes may be overridden for small tests).
 
     Returns dict with q [B, n_q, h_q, d], k [B, n_k, h_kv, d], v [B, n_k, h_kv, d]
     (bf16 on ``device``) plus the sizes used.  For decode workloads n_q = 1 and
-    the query sits at position q_pos0 (= n_k by default).  Random draws on a
+    the query sits at position q_pos0 (= n_k by default).  rotated=False returns q and k
+    as drawn, before the RoPE rotation (the inputs of the unrotated-cache kernels,
+    which rotate them as they read them).  Random draws on a
     CUDA device use that device's generator, so values differ from CPU draws of
     the same seed; both sides always consume the same tensors.
     """
@@ -180,6 +183,8 @@ def make_inputs(w: Workload, device="cpu", seed: Optional[int] = None, n_k: Opti
     q = q.to(torch.bfloat16)
     k = k.to(torch.bfloat16)
     v = v.to(torch.bfloat16)
+    if not rotated:
+        return {"q": q, "k": k, "v": v, "n_q": nq, "n_k": nk, "q_pos0": q_pos0, "batch": B}
     th = rotation_theta(w)
     qpos = torch.arange(q_pos0, q_pos0 + nq, dtype=torch.int64)
     kpos = torch.arange(0, nk, dtype=torch.int64)
