@@ -349,42 +349,52 @@ prefill_kernel(const std::conditional_t<kRot, PrefillRotParams, PrefillParams> p
     // the workgroup's tile is rotated once and pruned chunks (never loaded) never are.
     // Lane l turns 4 pairs (half l / 32 of the unit's 8) of key l % 32: both components
     // from the unit's two halves, angle (block start + l % 32) * theta_r by angle
-    // addition of the block start's angle (lanes 0..7, one pair each) and the offset's
-    // (the table).
+    // addition of the block start's angle (lanes 0 .. 8 kKPerWave - 1, one pair of one
+    // unit each) and the offset's (the table).
     auto rotate_units = [&](int j0, int buf, uint32_t loaded) __attribute__((always_inline)) {
         loaded = __builtin_amdgcn_readfirstlane(loaded);
+        if (loaded == 0u) return;
+        // block-start angles of all the wave's units at once: lane 8 t + e holds pair
+        // 8 c + e of unit t (c its chunk); a unit not loaded gets an unused angle
+        if (lane < 8 * C::kKPerWave) {
+            const int u = wave + C::kWaves * (lane >> 3);
+            const float ub = rope::revolutions(uint32_t(j0 + 32 * (u & 1)), s_rho[8 * (u >> 1) + (lane & 7)]);
+            s_base[wave * C::kKPerWave * 16 + 2 * lane] = __builtin_amdgcn_cosf(ub);
+            s_base[wave * C::kKPerWave * 16 + 2 * lane + 1] = __builtin_amdgcn_sinf(ub);
+        }
+        // the wave's own LDS writes complete before its later LDS reads; the fences
+        // keep the compiler from moving the reads above the writes
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // every unit's elements are read before any is rotated, so the reads' latencies
+        // overlap (reading a unit that was not loaded is harmless: it is not written)
+        typedef __attribute__((address_space(3))) uint64_t lds_u64;
+        const int kk = lane & 31, gq = lane >> 5;
+        uint64_t xv[C::kKPerWave], yv[C::kKPerWave];
+#pragma unroll
+        for (int t = 0; t < C::kKPerWave; ++t) {
+            const int u = wave + C::kWaves * t;
+            const uint32_t a0 = ks_lds + uint32_t(buf * C::kKTile * 2) + 1024u * u + uint32_t(kk * 16 + gq * 8);
+            xv[t] = *(const lds_u64*)(uintptr_t)a0;
+            yv[t] = *(const lds_u64*)(uintptr_t)(a0 + 512u);
+        }
 #pragma unroll
         for (int t = 0; t < C::kKPerWave; ++t) {
             if (!((loaded >> t) & 1u)) continue;
             const int u = wave + C::kWaves * t;
-            const int c = u >> 1;
-            const uint32_t jb = uint32_t(j0 + 32 * (u & 1));
-            float* sb = &s_base[(wave * C::kKPerWave + t) * 16];
-            if (lane < 8) {
-                const float ub = rope::revolutions(jb, s_rho[8 * c + lane]);
-                sb[2 * lane] = __builtin_amdgcn_cosf(ub);
-                sb[2 * lane + 1] = __builtin_amdgcn_sinf(ub);
-            }
-            // the wave's own LDS writes complete before its later LDS reads; the fences
-            // keep the compiler from moving the reads above the writes
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            const int kk = lane & 31, gq = lane >> 5;
-            const uint32_t a0 = ks_lds + uint32_t(buf * C::kKTile * 2) + 1024u * u + uint32_t(kk * 16 + gq * 8);
-            typedef __attribute__((address_space(3))) uint64_t lds_u64;
-            const uint64_t xv = *(const lds_u64*)(uintptr_t)a0;
-            const uint64_t yv = *(const lds_u64*)(uintptr_t)(a0 + 512u);
-            const float4 cc0 = *reinterpret_cast<const float4*>(&s_colcs[kk * kColStride + 2 * (8 * c + 4 * gq)]);
-            const float4 cc1 = *reinterpret_cast<const float4*>(&s_colcs[kk * kColStride + 2 * (8 * c + 4 * gq) + 4]);
-            const float4 bb0 = *reinterpret_cast<const float4*>(&sb[8 * gq]);
-            const float4 bb1 = *reinterpret_cast<const float4*>(&sb[8 * gq + 4]);
+            const float* cr = &s_colcs[kk * kColStride + 2 * (8 * (u >> 1) + 4 * gq)];
+            const float4 cc0 = *reinterpret_cast<const float4*>(cr);
+            const float4 cc1 = *reinterpret_cast<const float4*>(cr + 4);
+            const float* br = &s_base[(wave * C::kKPerWave + t) * 16 + 8 * gq];
+            const float4 bb0 = *reinterpret_cast<const float4*>(br);
+            const float4 bb1 = *reinterpret_cast<const float4*>(br + 4);
             const float cC[4] = {cc0.x, cc0.z, cc1.x, cc1.z}, sC[4] = {cc0.y, cc0.w, cc1.y, cc1.w};
             const float cB[4] = {bb0.x, bb0.z, bb1.x, bb1.z}, sB[4] = {bb0.y, bb0.w, bb1.y, bb1.w};
             uint32_t xo[2], yo[2];
 #pragma unroll
             for (int w2 = 0; w2 < 2; ++w2) {
-                const uint32_t xw = uint32_t(xv >> (32 * w2)), yw = uint32_t(yv >> (32 * w2));
+                const uint32_t xw = uint32_t(xv[t] >> (32 * w2)), yw = uint32_t(yv[t] >> (32 * w2));
                 rope::bf16x2_t xt, yt;
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
@@ -399,6 +409,7 @@ prefill_kernel(const std::conditional_t<kRot, PrefillRotParams, PrefillParams> p
                 xo[w2] = __builtin_bit_cast(uint32_t, xt);
                 yo[w2] = __builtin_bit_cast(uint32_t, yt);
             }
+            const uint32_t a0 = ks_lds + uint32_t(buf * C::kKTile * 2) + 1024u * u + uint32_t(kk * 16 + gq * 8);
             *(lds_u64*)(uintptr_t)a0 = uint64_t(xo[0]) | (uint64_t(xo[1]) << 32);
             *(lds_u64*)(uintptr_t)(a0 + 512u) = uint64_t(yo[0]) | (uint64_t(yo[1]) << 32);
         }

@@ -89,6 +89,18 @@ def test_no_mfma_under_exec_mask(tmp_path, src):
     assert not bad, bad[:5]
 
 
+def test_scratch_loop_check_finds_a_spill_in_a_loop():
+    asm = """_Zk:
+\tscratch_store_dword off, v1, off
+.LBB0_1:                                ; =>This Inner Loop Header: Depth=1
+\tscratch_load_dword v1, off, off
+.LBB0_2:
+\tscratch_load_dword v2, off, off
+.Lfunc_end0:
+"""
+    assert _scratch_in_loops(asm) == {"_Zk": [3, 1]}
+
+
 def test_exec_mask_check_finds_a_masked_mfma():
     """The check itself: a masked MFMA is found, a branched-around one is not."""
     masked = """_Zk:
@@ -108,6 +120,31 @@ def test_exec_mask_check_finds_a_masked_mfma():
     assert _mfmas_under_exec_mask(branched) == ([], 2)
 
 
+def _scratch_in_loops(asm):
+    """Per kernel of the assembly: (scratch instructions, those inside a loop).  A block
+    is inside a loop when the compiler's block comment says so ("Loop Header" or "in
+    Loop"); the kernel's straight-line prologue and epilogue are not."""
+    out = {}
+    name, in_loop = None, False
+    for ln in asm.splitlines():
+        m = re.match(r"^(_Z\S+):", ln)
+        if m:
+            name, in_loop = m.group(1), False
+            out[name] = [0, 0]
+            continue
+        if name is None:
+            continue
+        if ln.startswith(".Lfunc_end"):
+            name = None
+            continue
+        if re.match(r"^\.LBB\d+_\d+:", ln) or ln.startswith("; %bb."):
+            in_loop = "Loop" in ln
+        if re.match(r"\s+scratch_", ln):
+            out[name][0] += 1
+            out[name][1] += in_loop
+    return out
+
+
 @needs_hipcc
 @pytest.mark.parametrize("src", ["prefill.hip", "decode.hip"])
 def test_kernels_do_not_spill(tmp_path, src):
@@ -115,8 +152,10 @@ def test_kernels_do_not_spill(tmp_path, src):
     register lanes, a v_writelane/v_readlane pair each) stay a handful: a mask or
     loop that keeps many lane masks live at once shows up here first.  The prefill
     kernels that rotate unrotated caches (third template argument true) hold the
-    rotation's scalar state beside the rest and may spill up to 16 (their reloads sit
-    in the prologue and epilogue; the windowed d = 64 one adds two per tile)."""
+    rotation's state beside the rest: they may spill up to 16 scalar registers (their
+    reloads sit in the prologue and epilogue; the windowed d = 64 one adds two per
+    tile) and up to 4 vector registers, provided that no scratch access lies inside a
+    loop."""
     out = tmp_path / (src + ".o")
     cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
@@ -137,7 +176,13 @@ def test_kernels_do_not_spill(tmp_path, src):
         if m and name:
             kernels[name][m.group(1)] = int(m.group(2))
     assert kernels
+    loops = _scratch_in_loops(_assembly(tmp_path, src))
     for k, v in kernels.items():
-        assert v.get("VGPRs Spill", 0) == 0 and v.get("ScratchSize [bytes/lane]", 0) == 0, (k, v)
         rotating = re.search(r"prefill_kernelILi\d+ELb[01]ELb1E", k) is not None
+        if rotating:
+            assert v.get("VGPRs Spill", 0) <= 4, (k, v)
+            assert loops[k][1] == 0, (k, "scratch access inside a loop", loops[k])
+        else:
+            assert v.get("VGPRs Spill", 0) == 0 and v.get("ScratchSize [bytes/lane]", 0) == 0, \
+                (k, v)
         assert v.get("SGPRs Spill", 0) <= (16 if rotating else 8), (k, v)
