@@ -516,15 +516,15 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "f3e4f1625eb77f06488c48fa74f20cf8357d4cb6c543079ca8dfc378f208eb80",
-        "fetch_kib": 84980866.06, "write_kib": 933525.31,
+        "sha256": "87eb8d0b6e41959a2664d5ea9e294de235471d1dad5ad1de1ad290f911823750",
+        "fetch_kib": 85358633.27, "write_kib": 933554.69,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "259b2d1855f6a8f0bc0f9e9667b73a91c9c6760da0d8333a196051e78bcafa1a",
-        "fetch_kib": 737789.75, "write_kib": 4066.45,
+        "sha256": "8fa288b495dcf8370044ffb1f1162a89bd06d876808a3c9a104884da55385220",
+        "fetch_kib": 737790.98, "write_kib": 4075.71,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.02, "write": 1048576.0}  # counters for a 1 GiB copy
