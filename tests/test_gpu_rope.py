@@ -279,6 +279,8 @@ PREFILL_CASES = [
     (2, 130, 1000, 870, 12, 1, 128, 1e4, 2.0),           # G = 12
     (1, 520, 4100, 3580, 8, 2, 128, 1e7, 2.0),           # many tiles, chunks pruned by tile
     (1, 64, 700, (1 << 30) + 5, 4, 1, 128, 1e4, math.inf),  # queries at 2^30 + 5 ..
+    (1, 3, 200, 50, 128, 1, 64, 1e4, 2.0),               # G = 128: one position per workgroup
+    (1, 2, 150, 20, 256, 1, 128, 1e4, 2.0),              # G = 256
 ]
 
 
@@ -359,6 +361,30 @@ def test_prefill_unrotated_against_exact_rotation(case):
     assert eg[0] <= e16[0] + 5e-3, (case, eg, e16)
     assert eg[1] <= e16[1] + 5e-4, (case, eg, e16)
     assert eg[2] <= e16[2] + 5e-4, (case, eg, e16)
+
+
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_unrotated_cache_capacity_and_nan_tail(d):
+    """Caches allocated for more tokens than written, the slots past n_k filled with NaN:
+    the rotation of a tile that crosses n_k turns only loaded keys (the slots past n_k
+    re-read the last key), and the result equals the call over caches of exactly n_k
+    tokens bit for bit."""
+    import paper_2608_02947_amd as atf
+    B, n_q, n_k, cap, h_q, h_kv = 2, 150, 333, 400, 6, 2
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=29 + d)
+    win, widths = windows_for(d, 1e4, 2.0, None, n_ctx=n_k)
+    kc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    vc = torch.full((B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16)
+    kc[:, :n_k] = k
+    vc[:, :n_k] = v
+    note(f"prefill unrotated cache capacity d={d}")
+    kp, vp = pack_kcache(kc.to(DEV)), pack_vcache(vc.to(DEV))
+    o, lse = _gpu_prefill_unrotated(q, None, None, n_k - n_q, win, kp=kp, vp=vp, n_k=n_k)
+    o2, lse2 = _gpu_prefill_unrotated(q, k, v, n_k - n_q, win)
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+    qr, kr = _rotated_bf16(q, k, n_k - n_q, W.rope_theta(d, 1e4).numpy())
+    o_ref, lse_ref, _ = oracle.attend(qr, kr, v, n_k - n_q, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, f"unrotated capacity d={d}")
 
 
 def test_prefill_unrotated_chunked_equals_single_shot():
