@@ -9,7 +9,9 @@ One step = one windowed prefill call + one windowed decode call (all of the
 hot path: window table, tile classification, K/V staging, QK and PV MFMAs,
 boundary and causal masking, online softmax, epilogue, decode split + merge).
 The same kernels at an infinite window (k = +inf) are timed too, for the
-speedup the window buys.  Inputs are resident in HBM before timing starts.
+speedup the window buys, and the same prefill and decode from unrotated caches
+(RoPE applied as the kernels read, App. B).  Inputs are resident in HBM before
+timing starts.
 
 Prints ONE JSON line.  Effective TFLOP/s counts only the work the method must
 do: per query head 4*T + 2*d*C flops, T = retained (cell, pair) terms, C =
