@@ -8,6 +8,7 @@ from __future__ import annotations
 
 import math
 import sys
+import zlib
 
 import numpy as np
 import torch
@@ -18,6 +19,12 @@ import workloads as W
 O_MAX_ABS = 1e-2
 O_MEAN_ABS = 1e-3
 LSE_MAX_ABS = 1e-3
+
+
+def case_seed(case) -> int:
+    """A seed for a parametrised test case that is the same in every process (Python
+    salts the hash of a str per process, so hash() of a case holding a name is not)."""
+    return zlib.crc32(repr(case).encode()) % 10000
 
 
 def note(msg: str):

@@ -14,7 +14,7 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (compare_rounding_bound, compare, decode_budget, family_windows_for, gpu_decode, note, pack_kcache, pack_vcache,
+from parity import (case_seed, compare_rounding_bound, compare, decode_budget, family_windows_for, gpu_decode, note, pack_kcache, pack_vcache,
                     to_f64, windows_for, workload_window)
 
 pytestmark = [pytest.mark.gpu,
@@ -165,7 +165,7 @@ FAMILY_CASES = [
 def test_decode_window_family(case):
     """Members of the window family of App. A (eq:family)."""
     fam, B, n_k, q_pos, h_q, h_kv, d, base = case
-    q, k, v = _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed=hash(case) % 10000)
+    q, k, v = _decode_inputs(B, n_k, q_pos, h_q, h_kv, d, base, seed=case_seed(case))
     win, widths = family_windows_for(d, base, None, fam)
     _decode_parity(q, k, v, q_pos, win, widths, f"family{case}")
 

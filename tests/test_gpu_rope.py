@@ -12,8 +12,9 @@ import torch
 from conftest import gpu_available
 import oracle
 import workloads as W
-from parity import (LSE_MAX_ABS, O_MAX_ABS, O_MEAN_ABS, bench_rows, compare, gpu_prefill, note,
-                    pack_kcache, pack_vcache, table_windows, to_f64, windows_for)
+from parity import (LSE_MAX_ABS, O_MAX_ABS, O_MEAN_ABS, bench_rows, compare, family_windows_for,
+                    gpu_prefill, note, pack_kcache, pack_vcache, table_windows, to_f64,
+                    windows_for)
 
 pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs an MI355X (gfx950) GPU")]
@@ -362,6 +363,27 @@ def test_prefill_unrotated_against_exact_rotation(case):
     assert eg[0] <= e16[0] + O_MAX_ABS, (case, eg, e16)
     assert eg[1] <= e16[1] + O_MEAN_ABS, (case, eg, e16)
     assert eg[2] <= e16[2] + LSE_MAX_ABS, (case, eg, e16)
+
+
+@pytest.mark.parametrize("window", ["rounded8", "var16to2", "k2_floor40_cap180", "sliding100"])
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_unrotated_other_windows(window, d):
+    """The rounded slice (Sec. 3.3) and members of the window family (App. A) from
+    unrotated caches: the rotation follows whatever chunks the window keeps."""
+    B, n_q, n_k, q0, h_q, h_kv, base = 1, 300, 900, 600, 6, 2, 1e4
+    seed = 211 + d + ["rounded8", "var16to2", "k2_floor40_cap180", "sliding100"].index(window)
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=seed)
+    if window == "rounded8":
+        win, widths = windows_for(d, base, 2.0, None, n_ctx=q0 + n_q, slice_pairs=8)
+        atom = 8
+    else:
+        win, widths = family_windows_for(d, base, None, window)
+        atom = 0
+    note(f"prefill unrotated {window} d={d}")
+    o, lse = _gpu_prefill_unrotated(q, k, v, q0, win)
+    qr, kr = _rotated_bf16(q, k, q0, W.rope_theta(d, base).numpy())
+    o_ref, lse_ref, _ = oracle.attend(qr, kr, v, q0, widths, atom=atom)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, f"unrotated {window} d={d}")
 
 
 @pytest.mark.parametrize("d", [128, 64])
