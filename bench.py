@@ -747,6 +747,16 @@ def main():
         tpu_off = _median_ms(lambda: prefill_unrot(win_off), stream, 1, args.steps)
         prefill_info["unrotated_cache"]["full_window_ms"] = round(tpu_off, 3)
         prefill_info["unrotated_cache"]["speedup_vs_full_window"] = round(tpu_off / tpu, 4)
+    # the write-time alternative: the whole K cache rotated once into a copy
+    # (atf_rotate_kcache), which the pre-rotated prefill then reads
+    k_rot = torch.empty_like(kp)
+    trk = _median_ms(lambda: atf.atf_rotate_kcache(kp, k_rot, win, stream=stream), stream, 1,
+                     args.steps)
+    rot_bytes = 2 * kp.numel() * 2
+    prefill_info["unrotated_cache"]["rotate_kcache_ms"] = round(trk, 4)
+    prefill_info["unrotated_cache"]["rotate_kcache_GBps"] = round(rot_bytes / (trk * 1e-3) / 1e9, 1)
+    prefill_info["unrotated_cache"]["rotate_then_prefill_ms"] = round(trk + pre_med, 3)
+    del k_rot
 
     # ---- other windows on the same inputs: the variable-k profile 16 -> 2 and uniform
     # k = 64 (App. A, tab:absbench), and the rounded slice (Sec. 3.3, tab:c2e2e)

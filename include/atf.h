@@ -168,6 +168,29 @@ int32_t atf_kcache_chunk_pairs(int32_t head_dim);
 int atf_pack_kcache(const void *k_bshd, void *k_pcm, int32_t batch, int64_t n_k,
                     int32_t h_kv, int32_t head_dim, void *hip_stream);
 
+/* Rotate a whole unrotated K cache in one pass (RoPE at write time, the alternative
+ * to rotating at read time of App. B): key t of every (batch, kv head) is turned to
+ * position t, rotate-half convention of Sec. 2, in fp32 from the bf16 input and
+ * rounded to bf16, and written to a second cache of the same layout, which
+ * atf_prefill and atf_decode read as a pre-rotated cache.  Every (key, pair) is
+ * rotated, whatever a window later keeps; the cost is one read and one write of the
+ * cache and the rotated copy's memory.  Angles as in atf_prefill_unrotated (the
+ * fixed-point fraction, exact for any position), evaluated directly per (key, pair).
+ *   k_pcm  bf16 [batch][h_kv][d/16][cache_tokens][16], unrotated  (device, read)
+ *   k_rot  bf16, same layout; keys 0 .. n_k - 1 written, later slots untouched
+ *          (device, written; must not overlap k_pcm)
+ *   w      the window whose head_dim, and whose frequencies unless rope_inv_freq
+ *          is given, define the rotation (its thresholds are not used)
+ *   rope_inv_freq  host double [d/2] of theta_r, or NULL (as atf_prefill_unrotated)
+ * cache_tokens 0 means n_k.
+ * Errors: ATF_EINVAL (NULL/misaligned/overlapping buffers, batch < 1, n_k < 1,
+ * h_kv < 1, n_k or cache_tokens >= 2^31 - 1, cache_tokens < n_k, a rotation frequency
+ * that is negative, infinite or NaN); ATF_EUNSUPPORTED (d not 64 or 128, or
+ * batch * h_kv * d/16 above 65535); ATF_EHIP. */
+int atf_rotate_kcache(const void *k_pcm, void *k_rot, int32_t batch, int64_t n_k, int32_t h_kv,
+                      int64_t cache_tokens, const atf_window *w, const double *rope_inv_freq,
+                      void *hip_stream);
+
 /* Bytes of the packed decode V cache for these sizes:
  * batch * h_kv * ceil(n_k / 16) * 16 * head_dim * 2.  Returns 0 for invalid sizes. */
 size_t atf_vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_dim);

@@ -20,6 +20,8 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_cache_append_paged`, :func:`atf_decode_paged` -- paged caches (block tables).
 - :func:`atf_prefill_unrotated`, :func:`atf_decode_unrotated` (and its ragged and paged
   forms) -- the same from unrotated caches, RoPE applied as the kernels read them.
+- :func:`atf_rotate_kcache` -- RoPE over a whole unrotated K cache in one pass, into a
+  pre-rotated copy.
 """
 from __future__ import annotations
 
@@ -87,6 +89,7 @@ def _load():
                                                   i32, i32, P]),
         "atf_decode_paged": (ctypes.c_int, [P, P, P, P, P, i32, P, i32, i32, i32, P, P, i64, i32,
                                             i32, W, f32, P, ctypes.c_size_t, P]),
+        "atf_rotate_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i64, W, P, P]),
         "atf_prefill_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64,
                                                  W, P, f32, P]),
         "atf_decode_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, P,
@@ -110,7 +113,7 @@ EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
             "atf_decode_workspace_bytes", "atf_decode", "atf_decode_noalloc", "atf_decode_ragged",
             "atf_cache_append_paged",
-            "atf_decode_paged", "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
+            "atf_decode_paged", "atf_rotate_kcache", "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
             "atf_decode_paged_unrotated", "atf_last_error")
 
 
@@ -382,6 +385,23 @@ def _rope_freq(rope_inv_freq, d):
     if arr.shape != (d // 2,):
         raise ValueError(f"rope_inv_freq must have d/2 = {d // 2} entries")
     return arr.ctypes.data_as(ctypes.c_void_p), arr
+
+
+def atf_rotate_kcache(k_pcm, k_rot, window: Window, n_k: Optional[int] = None,
+                      rope_inv_freq=None, stream=None):
+    """k_pcm [B, h_kv, d/16, C, 16] unrotated -> k_rot (same shape) with key t turned to
+    position t, for t < n_k (default C); later slots of k_rot are not written."""
+    torch = _torch()
+    if k_pcm.dim() != 5 or tuple(k_rot.shape) != tuple(k_pcm.shape):
+        raise ValueError("atf_rotate_kcache: caches must both be [B, h_kv, d/16, C, 16]")
+    B, h_kv, nc, cap, _ = k_pcm.shape
+    d = 16 * nc
+    n_k = cap if n_k is None else int(n_k)
+    cw, keep = window.as_c()
+    fp, keep2 = _rope_freq(rope_inv_freq, d)
+    _check(_lib.atf_rotate_kcache(_dev_ptr(k_pcm, torch.bfloat16, "k_pcm"),
+                                  _dev_ptr(k_rot, torch.bfloat16, "k_rot"), B, n_k, h_kv, cap,
+                                  ctypes.byref(cw), fp, _stream_ptr(stream)))
 
 
 def atf_prefill_unrotated(q, k_cache, v_cache, o, lse, q_pos0: int, window: Window,

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libatf.so")
-SOURCES = ["atf_host.cpp", "prefill.hip", "decode.hip"]
+SOURCES = ["atf_host.cpp", "prefill.hip", "decode.hip", "rotate.hip"]
 # device-limit microbenchmarks timed by bench.py --peaks (not part of the attention ABI)
 PROBE_SOURCES = ["peaks.hip"]
 PROBE_LIB = os.path.join(PKG, "libatf_peaks.so")

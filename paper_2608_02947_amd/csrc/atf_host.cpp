@@ -423,6 +423,43 @@ int atf_pack_kcache(const void* k_bshd, void* k_pcm, int32_t batch, int64_t n_k,
     return ATF_OK;
 }
 
+int atf_rotate_kcache(const void* k_pcm, void* k_rot, int32_t batch, int64_t n_k, int32_t h_kv,
+                      int64_t cache_tokens, const atf_window* w, const double* rope_inv_freq,
+                      void* hip_stream) {
+    const char* fn = "rotate_kcache";
+    if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
+    const int d = w->head_dim;
+    if (d != 64 && d != 128)
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
+    if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit)
+        return fail(ATF_EINVAL, "%s: need batch >= 1, 1 <= n_k < 2^31, h_kv >= 1", fn);
+    if (cache_tokens == 0) cache_tokens = n_k;
+    if (cache_tokens < n_k || cache_tokens > kPosLimit)
+        return fail(ATF_EINVAL, "%s: cache_tokens %lld must be >= n_k %lld and < 2^31 - 1", fn,
+                    (long long)cache_tokens, (long long)n_k);
+    if (int64_t(batch) * h_kv * (d / 16) > 65535)
+        return fail(ATF_EUNSUPPORTED, "%s: batch * h_kv * d/16 above 65535", fn);
+    atf::RotateParams p{};
+    int rc = rope_fractions(fn, w, rope_inv_freq, p.rope_rho_hi, p.rope_rho_lo);
+    if (rc != ATF_OK) return rc;
+    if (!k_pcm || !k_rot) return fail(ATF_EINVAL, "%s: NULL pointer", fn);
+    if (!aligned(k_pcm, 16) || !aligned(k_rot, 16))
+        return fail(ATF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
+    const size_t bytes = size_t(batch) * size_t(h_kv) * size_t(d) * size_t(cache_tokens) * 2;
+    const char* a = static_cast<const char*>(k_pcm);
+    const char* b = static_cast<const char*>(k_rot);
+    if (a < b + bytes && b < a + bytes) return fail(ATF_EINVAL, "%s: buffers overlap", fn);
+    p.src = static_cast<const uint16_t*>(k_pcm);
+    p.dst = static_cast<uint16_t*>(k_rot);
+    p.batch = batch;
+    p.n_k = static_cast<int32_t>(n_k);
+    p.h_kv = h_kv;
+    p.cache_tokens = static_cast<int32_t>(cache_tokens);
+    const hipError_t e = atf::launch_rotate_kcache(p, d, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+    return ATF_OK;
+}
+
 size_t atf_vcache_bytes(int32_t batch, int64_t n_k, int32_t h_kv, int32_t head_dim) {
     if (batch < 1 || n_k < 1 || h_kv < 1 || n_k > kPosLimit || (head_dim != 64 && head_dim != 128))
         return 0;

@@ -100,13 +100,24 @@ struct PackParams {
     int32_t zero_tail;     // V: write zeros to the slots of the touched blocks past the source
 };
 
-// Kernel launchers (prefill.hip, decode.hip).  Return the HIP error of the launch.
+// One pass of RoPE over a pair-chunk-major K cache (rotate.hip): key t of every
+// (batch, kv head) at position t, tokens 0 .. n_k - 1.
+struct RotateParams {
+    const uint16_t* src;   // [B][h_kv][d/16][cache_tokens][16], unrotated
+    uint16_t* dst;         // same layout, rotated (tokens past n_k are not written)
+    int32_t batch, n_k, h_kv, cache_tokens;
+    uint32_t rope_rho_hi[kMaxPairs];
+    uint32_t rope_rho_lo[kMaxPairs];
+};
+
+// Kernel launchers (prefill.hip, decode.hip, rotate.hip).  Return the HIP error of the launch.
 hipError_t launch_prefill(const PrefillParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_prefill_rotating(const PrefillRotParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_rotate_kcache(const RotateParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan of a uniform batch: number of KV splits per (batch, kv head).
 int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);

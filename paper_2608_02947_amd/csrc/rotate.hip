@@ -1,0 +1,61 @@
+// RoPE over a whole K cache in one pass: the keys of an unrotated cache turned once,
+// each to its own position, into a second cache that the pre-rotated prefill and decode
+// read.  This is the write-time alternative to rotating at read time (App. B): it
+// costs one read and one write of the cache and every (key, pair) rotation, whatever
+// the window keeps, and the rotated copy's memory; a long prefill over an unrotated
+// cache can take it instead of the read-time path when that memory is at hand.
+//
+// Memory-bound.  One thread per (key, pair-chunk): the chunk's 32 bytes (the first
+// components of its 8 pairs, then the second) are read as two 16-byte loads, the 8
+// angles evaluated directly (0.64 fixed-point fraction, v_cos_f32 / v_sin_f32 in
+// revolutions), rotated in fp32 and rounded to bf16.  Grid: y = (batch, kv head,
+// chunk) stream, x over its tokens, so a block's chunk and its 8 frequencies are
+// uniform and consecutive threads touch consecutive 32-byte records.
+
+#include "atf_internal.hpp"
+#include "rope.hpp"
+
+namespace atf {
+namespace {
+
+template <int D>
+__global__ __launch_bounds__(256) void rotate_kcache_kernel(const RotateParams p) {
+    constexpr int kChunks = D / 16;
+    const int stream = blockIdx.y;  // (b * h_kv + g) * kChunks + c
+    const int c = stream % kChunks;
+    const int64_t off = int64_t(stream) * p.cache_tokens * 16;
+    const uint16_t* src = p.src + off;
+    uint16_t* dst = p.dst + off;
+    for (int64_t t = int64_t(blockIdx.x) * 256 + threadIdx.x; t < p.n_k;
+         t += int64_t(gridDim.x) * 256) {
+        const rope::u32x4_t x = *reinterpret_cast<const rope::u32x4_t*>(src + 16 * t);
+        const rope::u32x4_t y = *reinterpret_cast<const rope::u32x4_t*>(src + 16 * t + 8);
+        float cs8[8], sn8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float u = rope::revolutions(uint32_t(t), make_uint2(p.rope_rho_hi[8 * c + e],
+                                                                      p.rope_rho_lo[8 * c + e]));
+            cs8[e] = __builtin_amdgcn_cosf(u);
+            sn8[e] = __builtin_amdgcn_sinf(u);
+        }
+        *reinterpret_cast<rope::u32x4_t*>(dst + 16 * t) = rope::rotate_cs(x, y, 0, cs8, sn8);
+        *reinterpret_cast<rope::u32x4_t*>(dst + 16 * t + 8) = rope::rotate_cs(y, x, 1, cs8, sn8);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_rotate_kcache(const RotateParams& p, int head_dim, hipStream_t stream) {
+    const int64_t streams = int64_t(p.batch) * p.h_kv * (head_dim / 16);
+    if (streams < 1 || streams > 65535 || p.n_k < 1) return hipErrorInvalidConfiguration;
+    const int64_t xb = (int64_t(p.n_k) + 255) / 256;
+    const dim3 grid(unsigned(xb < 1024 ? xb : 1024), unsigned(streams));
+    (void)hipGetLastError();
+    if (head_dim == 64)
+        hipLaunchKernelGGL(rotate_kcache_kernel<64>, grid, dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL(rotate_kcache_kernel<128>, grid, dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace atf

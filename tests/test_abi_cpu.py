@@ -507,6 +507,28 @@ def test_prefill_unrotated_validation_before_launch():
                                      ctypes.byref(w64), None, 0.0, None) == atf.ATF_EUNSUPPORTED
 
 
+def test_rotate_kcache_validation_before_launch():
+    """Every call below fails host validation, so nothing is launched."""
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    w96, keep96 = atf.Window(96, 1e4, 2.0).as_c()
+    bad_f = (ctypes.c_double * 64)(*([1.0] * 63 + [float("nan")]))
+
+    def rot(src=16, dst=1 << 30, batch=1, n_k=100, h_kv=2, cap=0, win=w, f=None):
+        return lib.atf_rotate_kcache(src, dst, batch, n_k, h_kv, cap, ctypes.byref(win), f, None)
+
+    assert rot(win=w96) == atf.ATF_EUNSUPPORTED
+    assert rot(batch=0) == atf.ATF_EINVAL
+    assert rot(n_k=0) == atf.ATF_EINVAL
+    assert rot(cap=50) == atf.ATF_EINVAL                       # capacity below n_k
+    assert rot(batch=4096, h_kv=4) == atf.ATF_EUNSUPPORTED    # 4096 * 4 * 8 streams
+    assert rot(f=ctypes.cast(bad_f, ctypes.c_void_p)) == atf.ATF_EINVAL
+    assert "rotate_kcache" in atf.atf_last_error()
+    assert rot(src=None) == atf.ATF_EINVAL
+    assert rot(src=17) == atf.ATF_EINVAL                       # misaligned
+    assert rot(src=16, dst=16 + 4096) == atf.ATF_EINVAL        # overlap: 2 * 2 * 128 * 100 bytes
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

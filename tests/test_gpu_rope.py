@@ -490,3 +490,80 @@ def test_prefill_unrotated_qwen7b1m_chunk_sampled_rows(kwin):
     mx, mean, ml = compare(og, lg, o_ref, lse_ref, f"prefill unrotated qwen7b1m k={kwin}")
     print(f"[parity] prefill unrotated qwen7b1m k={kwin}: O max {mx:.2e} mean {mean:.2e} "
           f"LSE {ml:.2e}", flush=True)
+
+
+# ---- the whole cache rotated in one pass (write-time alternative) ----
+
+def _unpack_kcache(kp):
+    """[B, h_kv, d/16, n, 16] pair-chunk-major -> [B, n, h_kv, d] (pure re-indexing)."""
+    B, h_kv, C, n, _ = kp.shape
+    g = kp.permute(0, 3, 1, 2, 4)
+    lo = g[..., :8].reshape(B, n, h_kv, 8 * C)
+    hi = g[..., 8:].reshape(B, n, h_kv, 8 * C)
+    return torch.cat([lo, hi], dim=-1)
+
+
+@pytest.mark.parametrize("shape", [(2, 1000, 1100, 2, 128), (1, 777, 777, 3, 64),
+                                   (1, 262144, 262144, 1, 64)],
+                         ids=lambda c: "x".join(str(x) for x in c))
+def test_rotate_kcache_against_the_oracle(shape):
+    """atf_rotate_kcache against the oracle's fp64 rotation rounded to bf16 (key t at
+    position t; keys up to position 262143 in the last case), element by element:
+    |got - ref| <= one bf16 step of the larger of the two (each is a rounding of its
+    own rotation) + 2^-20 (|x_r| + |x_{r+d/2}|) (the fp32 rotation's error: products and
+    fma of bf16 inputs with fp32 cosines and sines, and the hardware cosine and sine,
+    each within a few fp32 units of the pair's magnitude).  Elements that differ at
+    all are rare, and the slots past n_k are untouched."""
+    import paper_2608_02947_amd as atf
+    B, n_k, cap, h_kv, d = shape
+    g = torch.Generator(device="cpu").manual_seed(31 + n_k)
+    k = torch.randn((B, cap, h_kv, d), generator=g).to(torch.bfloat16)
+    win, _ = windows_for(d, 1e4, 2.0, None, n_ctx=n_k)
+    note(f"rotate kcache {shape}")
+    kp = pack_kcache(k.to(DEV))
+    kr = torch.full_like(kp, float("nan"))
+    atf.atf_rotate_kcache(kp, kr, win, n_k=n_k)
+    torch.cuda.synchronize()
+    theta = W.rope_theta(d, 1e4).numpy()
+    ref = torch.from_numpy(oracle.rope_rotate(k[:, :n_k], np.arange(n_k), theta)).to(torch.bfloat16)
+    got = _unpack_kcache(kr[:, :, :, :n_k].cpu()).double()
+    ref = ref.double()
+    x = k[:, :n_k].double().abs()
+    mag = torch.cat([x[..., :d // 2] + x[..., d // 2:]] * 2, dim=-1)
+    big = torch.maximum(got.abs(), ref.abs())
+    step = torch.where(big > 0, torch.exp2(torch.floor(torch.log2(big)) - 7), torch.zeros_like(big))
+    excess = float(((got - ref).abs() - (step + 2.0 ** -20 * mag)).max())
+    frac = float((got != ref).double().mean())
+    print(f"[parity] rotate kcache {shape}: elements that differ {frac:.2e}, "
+          f"largest excess over the bound {excess:.2e}", flush=True)
+    assert excess <= 0.0 and frac < 1e-3, (shape, excess, frac)
+    if cap > n_k:
+        assert torch.isnan(kr[:, :, :, n_k:].float()).all()
+
+
+def test_rotate_kcache_then_prefill_and_decode():
+    """The rotated copy read as a pre-rotated cache: atf_prefill and atf_decode over it
+    against the oracle's attention over its own bf16 rotation."""
+    import paper_2608_02947_amd as atf
+    B, n_q, n_k, h_q, h_kv, d, base = 1, 300, 2000, 8, 2, 128, 1e6
+    q, k, v = _prefill_inputs(B, n_q, n_k, h_q, h_kv, d, seed=57)
+    q0 = n_k - n_q
+    win, widths = windows_for(d, base, 2.0, None, n_ctx=n_k + 1)
+    theta = W.rope_theta(d, base).numpy()
+    kp, vp = pack_kcache(k.to(DEV)), pack_vcache(v.to(DEV))
+    kr = torch.empty_like(kp)
+    note("rotate kcache then prefill and decode")
+    atf.atf_rotate_kcache(kp, kr, win, rope_inv_freq=theta)
+    qr, kr_ref = _rotated_bf16(q, k, q0, theta)
+    o, lse = gpu_prefill(qr.to(DEV), None, None, q0, win, kp=kr, vp=vp)
+    o_ref, lse_ref, _ = oracle.attend(qr, kr_ref, v, q0, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "rotated copy, prefill")
+    qd = torch.from_numpy(oracle.rope_rotate(q[:, -1:], [n_k], theta)).to(torch.bfloat16)
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, n_k, d), dtype=torch.uint8,
+                     device=DEV)
+    od = torch.empty((B, h_q, d), dtype=torch.bfloat16, device=DEV)
+    lsed = torch.empty((B, h_q), dtype=torch.float32, device=DEV)
+    atf.atf_decode(qd[:, 0].contiguous().to(DEV), kr, vp, od, lsed, n_k, win, ws)
+    torch.cuda.synchronize()
+    o_ref, lse_ref, _ = oracle.attend(qd, kr_ref, v, n_k, widths)
+    compare(to_f64(od), to_f64(lsed), o_ref[:, 0], lse_ref[:, :, 0], "rotated copy, decode")
