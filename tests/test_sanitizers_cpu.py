@@ -8,6 +8,7 @@ in a child process with the sanitizer runtime preloaded: tests/test_abi_cpu.py f
 library (no device work), tests/test_oracle.py for the oracle.  A sanitizer report
 fails the child (halt on error), and its output is checked for reports too."""
 import glob
+import importlib.util
 import os
 import subprocess
 import sys
@@ -58,7 +59,12 @@ def test_library_host_code_under_asan_ubsan(tmp_path):
              "-Xarch_host", "-fno-omit-frame-pointer",
              "-I", os.path.join(ROOT, "include"), "-I", csrc]
     objs = []
-    for src in ("atf_host.cpp", "prefill.hip", "decode.hip"):
+    # the library's own source list (build.py), loaded without importing the package
+    spec = importlib.util.spec_from_file_location(
+        "atf_build_sources", os.path.join(ROOT, "paper_2608_02947_amd", "build.py"))
+    build = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(build)
+    for src in build.SOURCES:
         obj = str(tmp_path / (src.split(".")[0] + ".o"))
         subprocess.run([HIPCC, *flags, "-x", "hip", "-c", os.path.join(csrc, src), "-o", obj],
                        check=True, capture_output=True)
