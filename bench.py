@@ -518,15 +518,15 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "87eb8d0b6e41959a2664d5ea9e294de235471d1dad5ad1de1ad290f911823750",
-        "fetch_kib": 85358633.27, "write_kib": 933554.69,
+        "sha256": "9b4d07b59d89c358af25f261daa2bcabe6667fc3611a5cd11ce7a41ad2daca78",
+        "fetch_kib": 122279796.54, "write_kib": 933559.49,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "8fa288b495dcf8370044ffb1f1162a89bd06d876808a3c9a104884da55385220",
-        "fetch_kib": 737790.98, "write_kib": 4075.71,
+        "sha256": "9250b3ed947886d3d3a4ee305d77e078db5408dcb4c6edb95c46503caa6d74ca",
+        "fetch_kib": 737785.83, "write_kib": 4068.94,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.02, "write": 1048576.0}  # counters for a 1 GiB copy
