@@ -178,12 +178,13 @@ int atf_pack_kcache(const void *k_bshd, void *k_pcm, int32_t batch, int64_t n_k,
  * fixed-point fraction, exact for any position), evaluated directly per (key, pair).
  *   k_pcm  bf16 [batch][h_kv][d/16][cache_tokens][16], unrotated  (device, read)
  *   k_rot  bf16, same layout; keys 0 .. n_k - 1 written, later slots untouched
- *          (device, written; must not overlap k_pcm)
+ *          (device, written; either k_pcm itself, which rotates the cache in place,
+ *          or a buffer that does not overlap it)
  *   w      the window whose head_dim, and whose frequencies unless rope_inv_freq
  *          is given, define the rotation (its thresholds are not used)
  *   rope_inv_freq  host double [d/2] of theta_r, or NULL (as atf_prefill_unrotated)
  * cache_tokens 0 means n_k.
- * Errors: ATF_EINVAL (NULL/misaligned/overlapping buffers, batch < 1, n_k < 1,
+ * Errors: ATF_EINVAL (NULL/misaligned/partly overlapping buffers, batch < 1, n_k < 1,
  * h_kv < 1, n_k or cache_tokens >= 2^31 - 1, cache_tokens < n_k, a rotation frequency
  * that is negative, infinite or NaN); ATF_EUNSUPPORTED (d not 64 or 128, or
  * batch * h_kv * d/16 above 65535); ATF_EHIP. */

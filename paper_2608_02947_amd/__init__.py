@@ -390,7 +390,8 @@ def _rope_freq(rope_inv_freq, d):
 def atf_rotate_kcache(k_pcm, k_rot, window: Window, n_k: Optional[int] = None,
                       rope_inv_freq=None, stream=None):
     """k_pcm [B, h_kv, d/16, C, 16] unrotated -> k_rot (same shape) with key t turned to
-    position t, for t < n_k (default C); later slots of k_rot are not written."""
+    position t, for t < n_k (default C); later slots of k_rot are not written.  k_rot may
+    be k_pcm itself (in place)."""
     torch = _torch()
     if k_pcm.dim() != 5 or tuple(k_rot.shape) != tuple(k_pcm.shape):
         raise ValueError("atf_rotate_kcache: caches must both be [B, h_kv, d/16, C, 16]")

@@ -448,7 +448,9 @@ int atf_rotate_kcache(const void* k_pcm, void* k_rot, int32_t batch, int64_t n_k
     const size_t bytes = size_t(batch) * size_t(h_kv) * size_t(d) * size_t(cache_tokens) * 2;
     const char* a = static_cast<const char*>(k_pcm);
     const char* b = static_cast<const char*>(k_rot);
-    if (a < b + bytes && b < a + bytes) return fail(ATF_EINVAL, "%s: buffers overlap", fn);
+    // in place (the same buffer) is allowed: each thread reads a record, then writes it
+    if (a != b && a < b + bytes && b < a + bytes)
+        return fail(ATF_EINVAL, "%s: buffers overlap", fn);
     p.src = static_cast<const uint16_t*>(k_pcm);
     p.dst = static_cast<uint16_t*>(k_rot);
     p.batch = batch;

@@ -539,6 +539,10 @@ def test_rotate_kcache_against_the_oracle(shape):
     assert excess <= 0.0 and frac < 1e-3, (shape, excess, frac)
     if cap > n_k:
         assert torch.isnan(kr[:, :, :, n_k:].float()).all()
+    # in place: the same bits as into a second buffer
+    atf.atf_rotate_kcache(kp, kp, win, n_k=n_k)
+    torch.cuda.synchronize()
+    assert torch.equal(kp[:, :, :, :n_k], kr[:, :, :, :n_k])
 
 
 def test_rotate_kcache_then_prefill_and_decode():
