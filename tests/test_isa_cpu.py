@@ -146,7 +146,7 @@ def _scratch_in_loops(asm):
 
 
 @needs_hipcc
-@pytest.mark.parametrize("src", ["prefill.hip", "decode.hip"])
+@pytest.mark.parametrize("src", ["prefill.hip", "decode.hip", "rotate.hip"])
 def test_kernels_do_not_spill(tmp_path, src):
     """No kernel spills vector registers to scratch, and scalar spills (into vector
     register lanes, a v_writelane/v_readlane pair each) stay a handful: a mask or
