@@ -227,6 +227,22 @@ int atf_cache_append(const void *k_new, const void *v_new, void *k_cache, void *
                      int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
                      int64_t cache_tokens, void *hip_stream);
 
+/* atf_cache_append with RoPE on the way in: the new keys are given unrotated, as the
+ * projections produce them, and key t is turned to its cache position pos0 + t
+ * (rotate-half convention of Sec. 2, in fp32 from the bf16 input, rounded to bf16;
+ * angles as in atf_rotate_kcache) while it is written into the pair-chunk-major cache:
+ * the write-time rotation of App. B fused with the append, so the caches hold rotated
+ * keys for atf_prefill and atf_decode.  Values as atf_cache_append.
+ *   w              the window whose head_dim, and whose frequencies unless
+ *                  rope_inv_freq is given, define the rotation (thresholds unused)
+ *   rope_inv_freq  host double [d/2] of theta_r, or NULL (as atf_prefill_unrotated)
+ * Everything else, errors included, as atf_cache_append, plus ATF_EINVAL for a NULL
+ * window or a rotation frequency that is negative, infinite or NaN. */
+int atf_cache_append_rotated(const void *k_new, const void *v_new, void *k_cache, void *v_cache,
+                             int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv,
+                             int64_t cache_tokens, const atf_window *w,
+                             const double *rope_inv_freq, void *hip_stream);
+
 /* Bytes of device workspace that atf_decode and atf_decode_ragged need for these
  * sizes (split-KV partial softmax states; the figure covers the split plans of both
  * calls).  Returns 0 for invalid sizes. */

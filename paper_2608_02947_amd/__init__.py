@@ -21,7 +21,7 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_prefill_unrotated`, :func:`atf_decode_unrotated` (and its ragged and paged
   forms) -- the same from unrotated caches, RoPE applied as the kernels read them.
 - :func:`atf_rotate_kcache` -- RoPE over a whole unrotated K cache in one pass, into a
-  pre-rotated copy.
+  pre-rotated copy; :func:`atf_cache_append_rotated` -- the append with RoPE on the way in.
 """
 from __future__ import annotations
 
@@ -90,6 +90,7 @@ def _load():
         "atf_decode_paged": (ctypes.c_int, [P, P, P, P, P, i32, P, i32, i32, i32, P, P, i64, i32,
                                             i32, W, f32, P, ctypes.c_size_t, P]),
         "atf_rotate_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i64, W, P, P]),
+        "atf_cache_append_rotated": (ctypes.c_int, [P, P, P, P, i32, i64, i64, i32, i64, W, P, P]),
         "atf_prefill_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64,
                                                  W, P, f32, P]),
         "atf_decode_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, P,
@@ -113,7 +114,8 @@ EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf
             "atf_pack_kcache", "atf_vcache_bytes", "atf_pack_vcache", "atf_cache_append",
             "atf_decode_workspace_bytes", "atf_decode", "atf_decode_noalloc", "atf_decode_ragged",
             "atf_cache_append_paged",
-            "atf_decode_paged", "atf_rotate_kcache", "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
+            "atf_decode_paged", "atf_rotate_kcache", "atf_cache_append_rotated",
+            "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
             "atf_decode_paged_unrotated", "atf_last_error")
 
 
@@ -403,6 +405,26 @@ def atf_rotate_kcache(k_pcm, k_rot, window: Window, n_k: Optional[int] = None,
     _check(_lib.atf_rotate_kcache(_dev_ptr(k_pcm, torch.bfloat16, "k_pcm"),
                                   _dev_ptr(k_rot, torch.bfloat16, "k_rot"), B, n_k, h_kv, cap,
                                   ctypes.byref(cw), fp, _stream_ptr(stream)))
+
+
+def atf_cache_append_rotated(k_new, v_new, k_cache, v_cache, pos0: int, window: Window,
+                             rope_inv_freq=None, stream=None):
+    """atf_cache_append with the new keys given unrotated: key t is turned to its cache
+    position pos0 + t as it is written.  k_new, v_new [B, n_new, h_kv, d] bf16."""
+    torch = _torch()
+    B, n_new, h_kv, d = k_new.shape
+    if k_cache.dim() != 5 or tuple(v_new.shape) != tuple(k_new.shape):
+        raise ValueError("atf_cache_append_rotated: inconsistent shapes")
+    cap = k_cache.shape[3]
+    if tuple(k_cache.shape) != kcache_shape(B, cap, h_kv, d) or \
+            tuple(v_cache.shape) != vcache_shape(B, cap, h_kv, d):
+        raise ValueError("atf_cache_append_rotated: inconsistent cache shapes")
+    cw, keep = window.as_c()
+    fp, keep2 = _rope_freq(rope_inv_freq, d)
+    _check(_lib.atf_cache_append_rotated(
+        _dev_ptr(k_new, torch.bfloat16, "k_new"), _dev_ptr(v_new, torch.bfloat16, "v_new"),
+        _dev_ptr(k_cache, torch.bfloat16, "k_cache"), _dev_ptr(v_cache, torch.bfloat16, "v_cache"),
+        B, n_new, int(pos0), h_kv, cap, ctypes.byref(cw), fp, _stream_ptr(stream)))
 
 
 def atf_prefill_unrotated(q, k_cache, v_cache, o, lse, q_pos0: int, window: Window,

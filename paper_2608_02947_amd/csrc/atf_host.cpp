@@ -481,20 +481,24 @@ int atf_pack_vcache(const void* v_bshd, void* v_pack, int32_t batch, int64_t n_k
     return ATF_OK;
 }
 
-int atf_cache_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
-                     int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
-                     int64_t cache_tokens, void* hip_stream) {
+namespace {
+// Shared by atf_cache_append (keys stored as given) and atf_cache_append_rotated (keys
+// turned to their cache positions on the way in: rope != nullptr).
+int cache_append_impl(const char* fn, const void* k_new, const void* v_new, void* k_cache,
+                      void* v_cache, int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv,
+                      int32_t head_dim, int64_t cache_tokens, void* hip_stream,
+                      const atf::RotateParams* rope) {
     if (head_dim != 64 && head_dim != 128)
-        return fail(ATF_EUNSUPPORTED, "cache_append: head_dim %d not built", head_dim);
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built", fn, head_dim);
     if (batch < 1 || h_kv < 1 || n_new < 0 || pos0 < 0 || cache_tokens < 1 ||
         cache_tokens > kPosLimit || pos0 > cache_tokens - n_new)
         return fail(ATF_EINVAL,
-                    "cache_append: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0, "
-                    "1 <= cache_tokens < 2^31 and pos0 + n_new <= cache_tokens");
+                    "%s: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0, "
+                    "1 <= cache_tokens < 2^31 and pos0 + n_new <= cache_tokens", fn);
     if (!k_new || !v_new || !k_cache || !v_cache)
-        return fail(ATF_EINVAL, "cache_append: NULL pointer");
+        return fail(ATF_EINVAL, "%s: NULL pointer", fn);
     if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16))
-        return fail(ATF_EINVAL, "cache_append: pointers must be 16-byte aligned");
+        return fail(ATF_EINVAL, "%s: pointers must be 16-byte aligned", fn);
     const size_t row = size_t(h_kv) * size_t(head_dim) * 2;
     const char* bufs[4] = {static_cast<const char*>(k_new), static_cast<const char*>(v_new),
                            static_cast<const char*>(k_cache), static_cast<const char*>(v_cache)};
@@ -504,21 +508,58 @@ int atf_cache_append(const void* k_new, const void* v_new, void* k_cache, void* 
     for (int i = 0; i < 4; ++i)
         for (int j = (i < 2 ? 2 : i + 1); j < 4; ++j)  // written buffers against all others
             if (bufs[i] < bufs[j] + sizes[j] && bufs[j] < bufs[i] + sizes[i])
-                return fail(ATF_EINVAL, "cache_append: buffers overlap");
+                return fail(ATF_EINVAL, "%s: buffers overlap", fn);
     if (n_new == 0) return ATF_OK;
     const hipStream_t st = static_cast<hipStream_t>(hip_stream);
     atf::PackParams pk{static_cast<const uint16_t*>(k_new), static_cast<uint16_t*>(k_cache), batch,
                        static_cast<int32_t>(n_new), h_kv, static_cast<int32_t>(pos0),
                        static_cast<int32_t>(cache_tokens), 0};
-    hipError_t e = atf::launch_pack_kcache(pk, head_dim, st);
+    hipError_t e;
+    if (rope != nullptr) {
+        atf::RotateParams rp = *rope;
+        rp.src = pk.src;
+        rp.dst = pk.dst;
+        rp.batch = batch;
+        rp.n_k = pk.n_k;
+        rp.h_kv = h_kv;
+        rp.cache_tokens = pk.cache_tokens;
+        rp.pos0 = pk.pos0;
+        e = atf::launch_append_rotated_k(rp, head_dim, st);
+    } else {
+        e = atf::launch_pack_kcache(pk, head_dim, st);
+    }
     if (e == hipSuccess) {
         atf::PackParams pv = pk;
         pv.src = static_cast<const uint16_t*>(v_new);
         pv.dst = static_cast<uint16_t*>(v_cache);
         e = atf::launch_pack_vcache(pv, head_dim, st);
     }
-    if (e != hipSuccess) return fail(ATF_EHIP, "cache_append: launch failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return ATF_OK;
+}
+}  // namespace
+
+int atf_cache_append(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                     int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
+                     int64_t cache_tokens, void* hip_stream) {
+    return cache_append_impl("cache_append", k_new, v_new, k_cache, v_cache, batch, n_new, pos0,
+                             h_kv, head_dim, cache_tokens, hip_stream, nullptr);
+}
+
+int atf_cache_append_rotated(const void* k_new, const void* v_new, void* k_cache, void* v_cache,
+                             int32_t batch, int64_t n_new, int64_t pos0, int32_t h_kv,
+                             int64_t cache_tokens, const atf_window* w, const double* rope_inv_freq,
+                             void* hip_stream) {
+    const char* fn = "cache_append_rotated";
+    if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
+    const int d = w->head_dim;
+    if (d != 64 && d != 128)
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
+    atf::RotateParams rp{};
+    const int rc = rope_fractions(fn, w, rope_inv_freq, rp.rope_rho_hi, rp.rope_rho_lo);
+    if (rc != ATF_OK) return rc;
+    return cache_append_impl(fn, k_new, v_new, k_cache, v_cache, batch, n_new, pos0, h_kv, d,
+                             cache_tokens, hip_stream, &rp);
 }
 
 namespace {

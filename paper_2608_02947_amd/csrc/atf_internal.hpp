@@ -100,12 +100,15 @@ struct PackParams {
     int32_t zero_tail;     // V: write zeros to the slots of the touched blocks past the source
 };
 
-// One pass of RoPE over a pair-chunk-major K cache (rotate.hip): key t of every
-// (batch, kv head) at position t, tokens 0 .. n_k - 1.
+// One pass of RoPE into a pair-chunk-major K cache (rotate.hip).  Whole cache: key t
+// of every (batch, kv head) at position t, tokens 0 .. n_k - 1, src in the cache layout.
+// Append: src [B][n_k][h_kv][d] (as the projections give it), token t written at cache
+// position pos0 + t and turned to that position.
 struct RotateParams {
-    const uint16_t* src;   // [B][h_kv][d/16][cache_tokens][16], unrotated
-    uint16_t* dst;         // same layout, rotated (tokens past n_k are not written)
+    const uint16_t* src;   // [B][h_kv][d/16][cache_tokens][16] (whole) or [B][n_k][h_kv][d] (append)
+    uint16_t* dst;         // [B][h_kv][d/16][cache_tokens][16]; only the tokens named are written
     int32_t batch, n_k, h_kv, cache_tokens;
+    int32_t pos0;          // append: cache position of the first source token
     uint32_t rope_rho_hi[kMaxPairs];
     uint32_t rope_rho_lo[kMaxPairs];
 };
@@ -118,6 +121,7 @@ hipError_t launch_pack_kcache(const PackParams& p, int head_dim, hipStream_t str
 hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_rotate_kcache(const RotateParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_append_rotated_k(const RotateParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan of a uniform batch: number of KV splits per (batch, kv head).
 int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);

@@ -1,6 +1,6 @@
 // RoPE over a whole K cache in one pass: the keys of an unrotated cache turned once,
-// each to its own position, into a second cache that the pre-rotated prefill and decode
-// read.  This is the write-time alternative to rotating at read time (App. B): it
+// each to its own position, into a second cache (or in place) that the pre-rotated
+// prefill and decode read; and the same rotation fused into the cache append.  This is the write-time alternative to rotating at read time (App. B): it
 // costs one read and one write of the cache and every (key, pair) rotation, whatever
 // the window keeps, and the rotated copy's memory; a long prefill over an unrotated
 // cache can take it instead of the read-time path when that memory is at hand.
@@ -43,7 +43,53 @@ __global__ __launch_bounds__(256) void rotate_kcache_kernel(const RotateParams p
     }
 }
 
+// Append with RoPE: keys as the projections give them ([B][n_k][h_kv][d], unrotated),
+// each turned to its cache position pos0 + t and written into the pair-chunk-major
+// cache, one thread per (token, kv head, chunk) as atf_pack_kcache lays them out.
+template <int D>
+__global__ __launch_bounds__(256) void append_rotated_k_kernel(const RotateParams p) {
+    constexpr int kChunks = D / 16;
+    const int64_t total = int64_t(p.batch) * p.n_k * p.h_kv * kChunks;
+    for (int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x; idx < total;
+         idx += int64_t(gridDim.x) * 256) {
+        const int c = int(idx % kChunks);
+        int64_t r = idx / kChunks;
+        const int g = int(r % p.h_kv);
+        r /= p.h_kv;
+        const int t = int(r % p.n_k);
+        const int b = int(r / p.n_k);
+        const uint16_t* src = p.src + ((int64_t(b) * p.n_k + t) * p.h_kv + g) * D;
+        const rope::u32x4_t x = *reinterpret_cast<const rope::u32x4_t*>(src + 8 * c);
+        const rope::u32x4_t y = *reinterpret_cast<const rope::u32x4_t*>(src + D / 2 + 8 * c);
+        const uint32_t pos = uint32_t(p.pos0 + t);
+        float cs8[8], sn8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float u = rope::revolutions(pos, make_uint2(p.rope_rho_hi[8 * c + e],
+                                                              p.rope_rho_lo[8 * c + e]));
+            cs8[e] = __builtin_amdgcn_cosf(u);
+            sn8[e] = __builtin_amdgcn_sinf(u);
+        }
+        uint16_t* dst = p.dst + (((int64_t(b) * p.h_kv + g) * kChunks + c) * p.cache_tokens + pos) * 16;
+        *reinterpret_cast<rope::u32x4_t*>(dst) = rope::rotate_cs(x, y, 0, cs8, sn8);
+        *reinterpret_cast<rope::u32x4_t*>(dst + 8) = rope::rotate_cs(y, x, 1, cs8, sn8);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_append_rotated_k(const RotateParams& p, int head_dim, hipStream_t stream) {
+    const int64_t total = int64_t(p.batch) * p.n_k * p.h_kv * (head_dim / 16);
+    if (total < 1) return hipErrorInvalidConfiguration;
+    const int64_t blocks = (total + 255) / 256;
+    const unsigned grid = unsigned(blocks < 16384 ? blocks : 16384);
+    (void)hipGetLastError();
+    if (head_dim == 64)
+        hipLaunchKernelGGL(append_rotated_k_kernel<64>, dim3(grid), dim3(256), 0, stream, p);
+    else
+        hipLaunchKernelGGL(append_rotated_k_kernel<128>, dim3(grid), dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
 
 hipError_t launch_rotate_kcache(const RotateParams& p, int head_dim, hipStream_t stream) {
     const int64_t streams = int64_t(p.batch) * p.h_kv * (head_dim / 16);

@@ -529,6 +529,27 @@ def test_rotate_kcache_validation_before_launch():
     assert rot(src=16, dst=16 + 4096) == atf.ATF_EINVAL        # overlap: 2 * 2 * 128 * 100 bytes
 
 
+def test_cache_append_rotated_validation_before_launch():
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    w96, keep96 = atf.Window(96, 1e4, 2.0).as_c()
+    bad_f = (ctypes.c_double * 64)(*([1.0] * 10 + [-1.0] + [1.0] * 53))
+
+    def app(win=w, n_new=10, pos0=0, cap=100, f=None, k_new=16):
+        wp = None if win is None else ctypes.byref(win)
+        return lib.atf_cache_append_rotated(k_new, 1 << 20, 1 << 24, 1 << 28, 1, n_new, pos0, 2,
+                                            cap, wp, f, None)
+
+    assert app(win=None) == atf.ATF_EINVAL
+    assert app(win=w96) == atf.ATF_EUNSUPPORTED
+    assert app(f=ctypes.cast(bad_f, ctypes.c_void_p)) == atf.ATF_EINVAL
+    assert "cache_append_rotated" in atf.atf_last_error()
+    assert app(pos0=95) == atf.ATF_EINVAL          # past the capacity
+    assert app(k_new=None) == atf.ATF_EINVAL
+    assert app(k_new=17) == atf.ATF_EINVAL         # misaligned
+    assert app(n_new=0) == atf.ATF_OK              # a no-op after validation
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

@@ -571,3 +571,36 @@ def test_rotate_kcache_then_prefill_and_decode():
     torch.cuda.synchronize()
     o_ref, lse_ref, _ = oracle.attend(qd, kr_ref, v, n_k, widths)
     compare(to_f64(od), to_f64(lsed), o_ref[:, 0], lse_ref[:, :, 0], "rotated copy, decode")
+
+
+def test_cache_append_rotated():
+    """Unrotated keys appended in three chunks with RoPE on the way in: the K cache is
+    the one-pass rotation of the whole unrotated cache bit for bit (the same angle and
+    rotation per (token, pair)), the V cache is atf_cache_append's, slots past the
+    appended tokens keep their contents, and a prefill over the caches matches the
+    oracle."""
+    import paper_2608_02947_amd as atf
+    B, n, cap, h_q, h_kv, d, base = 2, 900, 1000, 8, 2, 128, 1e6
+    q, k, v = _prefill_inputs(B, 200, n, h_q, h_kv, d, seed=73)
+    win, widths = windows_for(d, base, 2.0, None, n_ctx=n)
+    kd, vd = k.to(DEV), v.to(DEV)
+    kc = torch.full(atf.kcache_shape(B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16, device=DEV)
+    vc = torch.full(atf.vcache_shape(B, cap, h_kv, d), float("nan"), dtype=torch.bfloat16, device=DEV)
+    vc2 = vc.clone()
+    kc2 = torch.full_like(kc, float("nan"))
+    note("cache append rotated")
+    for a, b in [(0, 300), (300, 301), (301, 900)]:
+        atf.atf_cache_append_rotated(kd[:, a:b].contiguous(), vd[:, a:b].contiguous(), kc, vc, a, win)
+        atf.atf_cache_append(kd[:, a:b].contiguous(), vd[:, a:b].contiguous(), kc2, vc2, a)
+    kr = torch.full_like(kc, float("nan"))
+    atf.atf_rotate_kcache(kc2, kr, win, n_k=n)
+    torch.cuda.synchronize()
+    assert torch.equal(kc[:, :, :, :n], kr[:, :, :, :n])
+    assert torch.isnan(kc[:, :, :, n:].float()).all()
+    assert torch.equal(vc.view(torch.int16), vc2.view(torch.int16))
+    q0 = n - 200
+    theta = W.rope_theta(d, base).numpy()
+    qr, kr_ref = _rotated_bf16(q, k, q0, theta)
+    o, lse = gpu_prefill(qr.to(DEV), None, None, q0, win, kp=kc, vp=vc, n_k=n)
+    o_ref, lse_ref, _ = oracle.attend(qr, kr_ref, v, q0, widths)
+    compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "append rotated, prefill")
