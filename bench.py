@@ -518,15 +518,15 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "9b4d07b59d89c358af25f261daa2bcabe6667fc3611a5cd11ce7a41ad2daca78",
-        "fetch_kib": 122279796.54, "write_kib": 933559.49,
+        "sha256": "7d436e2d349ffe18f8e0b91d0c355918cc227226503961269aeb7ca9bc43c49d",
+        "fetch_kib": 92981796.48, "write_kib": 933532.5,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "9250b3ed947886d3d3a4ee305d77e078db5408dcb4c6edb95c46503caa6d74ca",
-        "fetch_kib": 737785.83, "write_kib": 4068.94,
+        "sha256": "0cca9ac8645a5f8b770738b34fa5c41ee5088dfb0984a61d9045489ec4826afe",
+        "fetch_kib": 737788.79, "write_kib": 4071.25,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.02, "write": 1048576.0}  # counters for a 1 GiB copy
