@@ -1,16 +1,17 @@
-// RoPE over a whole K cache in one pass: the keys of an unrotated cache turned once,
-// each to its own position, into a second cache (or in place) that the pre-rotated
-// prefill and decode read; and the same rotation fused into the cache append.  This is the write-time alternative to rotating at read time (App. B): it
-// costs one read and one write of the cache and every (key, pair) rotation, whatever
-// the window keeps, and the rotated copy's memory; a long prefill over an unrotated
-// cache can take it instead of the read-time path when that memory is at hand.
+// RoPE at write time (App. B sets it against rotating at read time): the keys of an
+// unrotated K cache turned once, each to its own position, into a second cache or in
+// place, and the same rotation fused into the cache append; the pre-rotated prefill and
+// decode then read the result.  It costs one read and one write of the keys and every
+// (key, pair) rotation, whatever the window keeps, and a rotated copy's memory; a long
+// prefill over an unrotated cache can take it instead of the read-time path when that
+// memory is at hand.
 //
 // Memory-bound.  One thread per (key, pair-chunk): the chunk's 32 bytes (the first
 // components of its 8 pairs, then the second) are read as two 16-byte loads, the 8
 // angles evaluated directly (0.64 fixed-point fraction, v_cos_f32 / v_sin_f32 in
-// revolutions), rotated in fp32 and rounded to bf16.  Grid: y = (batch, kv head,
-// chunk) stream, x over its tokens, so a block's chunk and its 8 frequencies are
-// uniform and consecutive threads touch consecutive 32-byte records.
+// revolutions), rotated in fp32 and rounded to bf16.  Whole cache: grid y = the
+// (batch, kv head, chunk) stream, x over its tokens, so a block's chunk and its 8
+// frequencies are uniform and consecutive threads touch consecutive 32-byte records.
 
 #include "atf_internal.hpp"
 #include "rope.hpp"
