@@ -359,6 +359,19 @@ int atf_cache_append_paged(const void *k_new, const void *v_new, void *k_pages, 
                            int64_t n_new, int64_t pos0, int32_t h_kv, int32_t head_dim,
                            void *hip_stream);
 
+/* atf_cache_append_paged with RoPE on the way in: the new keys are given unrotated and
+ * key t of row b is turned to its position pos0 + t as it is written into its page
+ * (rotation as atf_cache_append_rotated).  Values, tables, pools, clamping of table
+ * entries and errors as atf_cache_append_paged, plus ATF_EINVAL for a NULL window or a
+ * rotation frequency that is negative, infinite or NaN.  The head dimension is the
+ * window's. */
+int atf_cache_append_paged_rotated(const void *k_new, const void *v_new, void *k_pages,
+                                   void *v_pages, const int32_t *block_table,
+                                   int32_t max_pages_per_row, int32_t num_pages,
+                                   int32_t page_tokens, int32_t batch, int64_t n_new,
+                                   int64_t pos0, int32_t h_kv, const atf_window *w,
+                                   const double *rope_inv_freq, void *hip_stream);
+
 /* Decode of a ragged batch over paged caches: atf_decode_ragged with row b's keys read
  * through its block table (layouts above).  max_n_k bounds n_k_rows and must not
  * exceed max_pages_per_row * page_tokens; the workspace is

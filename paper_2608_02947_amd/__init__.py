@@ -91,6 +91,8 @@ def _load():
                                             i32, W, f32, P, ctypes.c_size_t, P]),
         "atf_rotate_kcache": (ctypes.c_int, [P, P, i32, i64, i32, i64, W, P, P]),
         "atf_cache_append_rotated": (ctypes.c_int, [P, P, P, P, i32, i64, i64, i32, i64, W, P, P]),
+        "atf_cache_append_paged_rotated": (ctypes.c_int, [P, P, P, P, P, i32, i32, i32, i32, i64,
+                                                          i64, i32, W, P, P]),
         "atf_prefill_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i64, i32, i32, i64,
                                                  W, P, f32, P]),
         "atf_decode_unrotated": (ctypes.c_int, [P, P, P, P, P, i32, i64, i64, i32, i32, i64, W, P,
@@ -115,6 +117,7 @@ EXPORTED = ("atf_window_table", "atf_retention_profile", "atf_count_terms", "atf
             "atf_decode_workspace_bytes", "atf_decode", "atf_decode_noalloc", "atf_decode_ragged",
             "atf_cache_append_paged",
             "atf_decode_paged", "atf_rotate_kcache", "atf_cache_append_rotated",
+            "atf_cache_append_paged_rotated",
             "atf_prefill_unrotated", "atf_decode_unrotated", "atf_decode_ragged_unrotated",
             "atf_decode_paged_unrotated", "atf_last_error")
 
@@ -545,6 +548,25 @@ def atf_cache_append_paged(k_new, v_new, k_pages, v_pages, block_table, pos0: in
         _dev_ptr(block_table, torch.int32, "block_table"), block_table.shape[1], num_pages, pt, B,
         n_new, int(pos0), h_kv, d, _stream_ptr(stream))
     _check(rc)
+
+
+def atf_cache_append_paged_rotated(k_new, v_new, k_pages, v_pages, block_table, pos0: int,
+                                   window: Window, rope_inv_freq=None, stream=None):
+    """atf_cache_append_paged with the new keys given unrotated: key t of each row is
+    turned to its position pos0 + t as it is written into its page."""
+    torch = _torch()
+    num_pages, h_kv, pt, d = _pages(k_pages, v_pages, "atf_cache_append_paged_rotated")
+    B, n_new, hk, dd = k_new.shape
+    if tuple(v_new.shape) != tuple(k_new.shape) or hk != h_kv or dd != d or \
+            block_table.dim() != 2 or block_table.shape[0] != B or window.head_dim != d:
+        raise ValueError("atf_cache_append_paged_rotated: inconsistent shapes")
+    cw, keep = window.as_c()
+    fp, keep2 = _rope_freq(rope_inv_freq, d)
+    _check(_lib.atf_cache_append_paged_rotated(
+        _dev_ptr(k_new, torch.bfloat16, "k_new"), _dev_ptr(v_new, torch.bfloat16, "v_new"),
+        _dev_ptr(k_pages, torch.bfloat16, "k_pages"), _dev_ptr(v_pages, torch.bfloat16, "v_pages"),
+        _dev_ptr(block_table, torch.int32, "block_table"), block_table.shape[1], num_pages, pt, B,
+        n_new, int(pos0), h_kv, ctypes.byref(cw), fp, _stream_ptr(stream)))
 
 
 def atf_decode_paged(q, k_pages, v_pages, o, lse, block_table, n_k_rows, q_pos_rows,

@@ -867,31 +867,35 @@ int atf_decode_paged_unrotated(const void* q, const void* k_pages, const void* v
                              workspace_bytes, hip_stream, rope);
 }
 
-int atf_cache_append_paged(const void* k_new, const void* v_new, void* k_pages, void* v_pages,
-                           const int32_t* block_table, int32_t max_pages_per_row,
-                           int32_t num_pages, int32_t page_tokens, int32_t batch, int64_t n_new,
-                           int64_t pos0, int32_t h_kv, int32_t head_dim, void* hip_stream) {
+namespace {
+// Shared by atf_cache_append_paged and atf_cache_append_paged_rotated (rope != nullptr:
+// the keys turned to their positions on the way in).
+int cache_append_paged_impl(const char* fn, const void* k_new, const void* v_new, void* k_pages,
+                            void* v_pages, const int32_t* block_table, int32_t max_pages_per_row,
+                            int32_t num_pages, int32_t page_tokens, int32_t batch, int64_t n_new,
+                            int64_t pos0, int32_t h_kv, int32_t head_dim, void* hip_stream,
+                            const atf::RotatePagedParams* rope) {
     if (head_dim != 64 && head_dim != 128)
-        return fail(ATF_EUNSUPPORTED, "cache_append_paged: head_dim %d not built", head_dim);
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built", fn, head_dim);
     if (batch < 1 || h_kv < 1 || n_new < 0 || pos0 < 0)
-        return fail(ATF_EINVAL, "cache_append_paged: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0");
+        return fail(ATF_EINVAL, "%s: need batch >= 1, h_kv >= 1, n_new >= 0, pos0 >= 0", fn);
     if (page_tokens < 32 || page_tokens % 32 != 0)
-        return fail(ATF_EINVAL, "cache_append_paged: page_tokens %d must be a positive multiple of 32",
+        return fail(ATF_EINVAL, "%s: page_tokens %d must be a positive multiple of 32", fn,
                     page_tokens);
     if (num_pages < 1 || max_pages_per_row < 1)
-        return fail(ATF_EINVAL, "cache_append_paged: need num_pages >= 1 and max_pages_per_row >= 1");
+        return fail(ATF_EINVAL, "%s: need num_pages >= 1 and max_pages_per_row >= 1", fn);
     const int64_t row_cap = int64_t(max_pages_per_row) * page_tokens;
     if (row_cap > kPosLimit || pos0 + n_new > row_cap)
-        return fail(ATF_EINVAL, "cache_append_paged: tokens %lld .. %lld do not fit the %lld tokens "
-                    "of a row's pages", (long long)pos0, (long long)(pos0 + n_new), (long long)row_cap);
+        return fail(ATF_EINVAL, "%s: tokens %lld .. %lld do not fit the %lld tokens "
+                    "of a row's pages", fn, (long long)pos0, (long long)(pos0 + n_new), (long long)row_cap);
     if (!k_new || !v_new || !k_pages || !v_pages || !block_table)
-        return fail(ATF_EINVAL, "cache_append_paged: NULL pointer");
+        return fail(ATF_EINVAL, "%s: NULL pointer", fn);
     if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(k_pages, 16) ||
         !aligned(v_pages, 16) || !aligned(block_table, 4))
-        return fail(ATF_EINVAL, "cache_append_paged: tensors must be 16-byte, the table 4-byte aligned");
+        return fail(ATF_EINVAL, "%s: tensors must be 16-byte, the table 4-byte aligned", fn);
     if (n_new == 0) return ATF_OK;
     if (int64_t(batch) * n_new * h_kv > kPosLimit)
-        return fail(ATF_EINVAL, "cache_append_paged: too many tokens for one call");
+        return fail(ATF_EINVAL, "%s: too many tokens for one call", fn);
     atf::AppendPagedParams p{};
     p.k_src = static_cast<const uint16_t*>(k_new);
     p.v_src = static_cast<const uint16_t*>(v_new);
@@ -905,9 +909,45 @@ int atf_cache_append_paged(const void* k_new, const void* v_new, void* k_pages, 
     p.max_pages = max_pages_per_row;
     p.num_pages = num_pages;
     p.page_tokens = page_tokens;
-    hipError_t e = atf::launch_append_paged(p, head_dim, static_cast<hipStream_t>(hip_stream));
-    if (e != hipSuccess) return fail(ATF_EHIP, "cache_append_paged: launch failed: %s", hipGetErrorString(e));
+    hipError_t e;
+    if (rope != nullptr) {
+        atf::RotatePagedParams rp = *rope;
+        rp.a = p;
+        e = atf::launch_append_paged_rotated(rp, head_dim, static_cast<hipStream_t>(hip_stream));
+    } else {
+        e = atf::launch_append_paged(p, head_dim, static_cast<hipStream_t>(hip_stream));
+    }
+    if (e != hipSuccess) return fail(ATF_EHIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
     return ATF_OK;
+}
+}  // namespace
+
+int atf_cache_append_paged(const void* k_new, const void* v_new, void* k_pages, void* v_pages,
+                           const int32_t* block_table, int32_t max_pages_per_row,
+                           int32_t num_pages, int32_t page_tokens, int32_t batch, int64_t n_new,
+                           int64_t pos0, int32_t h_kv, int32_t head_dim, void* hip_stream) {
+    return cache_append_paged_impl("cache_append_paged", k_new, v_new, k_pages, v_pages,
+                                   block_table, max_pages_per_row, num_pages, page_tokens, batch,
+                                   n_new, pos0, h_kv, head_dim, hip_stream, nullptr);
+}
+
+int atf_cache_append_paged_rotated(const void* k_new, const void* v_new, void* k_pages,
+                                   void* v_pages, const int32_t* block_table,
+                                   int32_t max_pages_per_row, int32_t num_pages,
+                                   int32_t page_tokens, int32_t batch, int64_t n_new, int64_t pos0,
+                                   int32_t h_kv, const atf_window* w, const double* rope_inv_freq,
+                                   void* hip_stream) {
+    const char* fn = "cache_append_paged_rotated";
+    if (w == nullptr) return fail(ATF_EINVAL, "%s: NULL window", fn);
+    const int d = w->head_dim;
+    if (d != 64 && d != 128)
+        return fail(ATF_EUNSUPPORTED, "%s: head_dim %d not built (64 or 128)", fn, d);
+    atf::RotatePagedParams rp{};
+    const int rc = rope_fractions(fn, w, rope_inv_freq, rp.rope_rho_hi, rp.rope_rho_lo);
+    if (rc != ATF_OK) return rc;
+    return cache_append_paged_impl(fn, k_new, v_new, k_pages, v_pages, block_table,
+                                   max_pages_per_row, num_pages, page_tokens, batch, n_new, pos0,
+                                   h_kv, d, hip_stream, &rp);
 }
 
 }  // extern "C"

@@ -90,6 +90,14 @@ struct AppendPagedParams {
     int32_t batch, n_new, pos0, h_kv, max_pages, num_pages, page_tokens;
 };
 
+// The paged append with RoPE on the way in (rotate.hip): AppendPagedParams' fields, and
+// the rotation's 0.64 fixed-point frequencies.
+struct RotatePagedParams {
+    AppendPagedParams a;
+    uint32_t rope_rho_hi[kMaxPairs];
+    uint32_t rope_rho_lo[kMaxPairs];
+};
+
 struct PackParams {
     const uint16_t* src;  // [B][n_k][h_kv][d]: tokens pos0 .. pos0 + n_k - 1
     uint16_t* dst;        // K: [B][h_kv][d/16][cache_tokens][16];
@@ -122,6 +130,7 @@ hipError_t launch_pack_vcache(const PackParams& p, int head_dim, hipStream_t str
 hipError_t launch_append_paged(const AppendPagedParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_rotate_kcache(const RotateParams& p, int head_dim, hipStream_t stream);
 hipError_t launch_append_rotated_k(const RotateParams& p, int head_dim, hipStream_t stream);
+hipError_t launch_append_paged_rotated(const RotatePagedParams& p, int head_dim, hipStream_t stream);
 
 // Decode split plan of a uniform batch: number of KV splits per (batch, kv head).
 int32_t decode_splits(int32_t batch, int32_t h_kv, int64_t n_k);

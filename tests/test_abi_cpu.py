@@ -550,6 +550,28 @@ def test_cache_append_rotated_validation_before_launch():
     assert app(n_new=0) == atf.ATF_OK              # a no-op after validation
 
 
+def test_cache_append_paged_rotated_validation_before_launch():
+    lib = atf.library()
+    w, keep = atf.Window(128, 1e4, 2.0).as_c()
+    w96, keep96 = atf.Window(96, 1e4, 2.0).as_c()
+    bad_f = (ctypes.c_double * 64)(*([1.0] * 20 + [float("inf")] + [1.0] * 43))
+
+    def app(win=w, pt=64, n_new=10, pos0=0, f=None, bt=16):
+        wp = None if win is None else ctypes.byref(win)
+        return lib.atf_cache_append_paged_rotated(16, 1 << 20, 1 << 24, 1 << 28, bt, 4, 8, pt, 1,
+                                                  n_new, pos0, 2, wp, f, None)
+
+    assert app(win=None) == atf.ATF_EINVAL
+    assert app(win=w96) == atf.ATF_EUNSUPPORTED
+    assert app(f=ctypes.cast(bad_f, ctypes.c_void_p)) == atf.ATF_EINVAL
+    assert "cache_append_paged_rotated" in atf.atf_last_error()
+    assert app(pt=48) == atf.ATF_EINVAL            # not a multiple of 32
+    assert app(pos0=250) == atf.ATF_EINVAL         # past the row's 4 pages of 64
+    assert app(bt=None) == atf.ATF_EINVAL
+    assert app(bt=18) == atf.ATF_EINVAL            # misaligned table
+    assert app(n_new=0) == atf.ATF_OK              # a no-op after validation
+
+
 def test_pack_validation_before_launch():
     lib = atf.library()
     assert lib.atf_pack_kcache(16, 16 + 64, 1, 4, 1, 64, None) == atf.ATF_EINVAL   # overlap

@@ -604,3 +604,54 @@ def test_cache_append_rotated():
     o, lse = gpu_prefill(qr.to(DEV), None, None, q0, win, kp=kc, vp=vc, n_k=n)
     o_ref, lse_ref, _ = oracle.attend(qr, kr_ref, v, q0, widths)
     compare(to_f64(o), to_f64(lse), o_ref, lse_ref, "append rotated, prefill")
+
+
+def test_cache_append_paged_rotated():
+    """Unrotated keys appended into shuffled pages in two chunks with RoPE on the way in:
+    every written K slot equals the contiguous rotated append's bit for bit, the V pages
+    equal atf_cache_append_paged's, pages no row names keep their contents, and the
+    paged decode over them matches the oracle."""
+    import paper_2608_02947_amd as atf
+    B, n, pt, h_q, h_kv, d, base = 3, 700, 64, 6, 2, 128, 1e4
+    pages = -(-n // pt)
+    num_pages = B * pages + 2
+    q, k, v = _prefill_inputs(B, 1, n, h_q, h_kv, d, seed=83)
+    win, widths = windows_for(d, base, 2.0, None, n_ctx=n + 1)
+    perm = np.random.default_rng(9).permutation(num_pages)[:B * pages].reshape(B, pages)
+    btd = torch.from_numpy(perm.astype(np.int32)).to(DEV)
+    kd, vd = k.to(DEV), v.to(DEV)
+    kpool = torch.full(atf.kpages_shape(num_pages, pt, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                       device=DEV)
+    vpool = torch.full(atf.vpages_shape(num_pages, pt, h_kv, d), float("nan"), dtype=torch.bfloat16,
+                       device=DEV)
+    vpool2 = vpool.clone()
+    kpool2 = kpool.clone()
+    note("cache append paged rotated")
+    for a, b in [(0, 250), (250, n)]:
+        ka, va = kd[:, a:b].contiguous(), vd[:, a:b].contiguous()
+        atf.atf_cache_append_paged_rotated(ka, va, kpool, vpool, btd, a, win)
+        atf.atf_cache_append_paged(ka, va, kpool2, vpool2, btd, a)
+    kc = torch.empty(atf.kcache_shape(B, n, h_kv, d), dtype=torch.bfloat16, device=DEV)
+    vc = torch.empty(atf.vcache_shape(B, n, h_kv, d), dtype=torch.bfloat16, device=DEV)
+    atf.atf_cache_append_rotated(kd, vd, kc, vc, 0, win)
+    torch.cuda.synchronize()
+    # K slot of (row b, token t): page bt[b, t // pt], slot t % pt
+    t = torch.arange(n, device=DEV)
+    for b in range(B):
+        pg = btd[b, t // pt].long()
+        got = kpool[pg, :, :, t % pt, :]                   # [n, h_kv, d/16, 16]
+        assert torch.equal(got, kc[b].permute(2, 0, 1, 3)), b
+    assert torch.equal(vpool.view(torch.int16), vpool2.view(torch.int16))
+    unused = sorted(set(range(num_pages)) - set(perm.ravel().tolist()))
+    assert torch.isnan(kpool[unused].float()).all()
+    qd = torch.from_numpy(oracle.rope_rotate(q, [n], W.rope_theta(d, base).numpy())).to(torch.bfloat16)
+    ws = torch.empty(atf.atf_decode_workspace_bytes(B, h_q, h_kv, n, d), dtype=torch.uint8, device=DEV)
+    od = torch.empty((B, h_q, d), dtype=torch.bfloat16, device=DEV)
+    lsed = torch.empty((B, h_q), dtype=torch.float32, device=DEV)
+    rows = torch.full((B,), n, dtype=torch.int32, device=DEV)
+    atf.atf_decode_paged(qd[:, 0].contiguous().to(DEV), kpool, vpool, od, lsed, btd, rows, rows, n,
+                         win, ws)
+    torch.cuda.synchronize()
+    _, kr_ref = _rotated_bf16(q, k, n, W.rope_theta(d, base).numpy())
+    o_ref, lse_ref, _ = oracle.attend(qd, kr_ref, v, n, widths)
+    compare(to_f64(od), to_f64(lsed), o_ref[:, 0], lse_ref[:, :, 0], "paged rotated append, decode")
