@@ -21,7 +21,8 @@ The functions carry the C names of ``include/atf.h``:
 - :func:`atf_prefill_unrotated`, :func:`atf_decode_unrotated` (and its ragged and paged
   forms) -- the same from unrotated caches, RoPE applied as the kernels read them.
 - :func:`atf_rotate_kcache` -- RoPE over a whole unrotated K cache in one pass, into a
-  pre-rotated copy; :func:`atf_cache_append_rotated` -- the append with RoPE on the way in.
+  pre-rotated copy; :func:`atf_cache_append_rotated`, :func:`atf_cache_append_paged_rotated`
+  -- the appends with RoPE on the way in.
 """
 from __future__ import annotations
 
