@@ -518,15 +518,15 @@ TRAFFIC_RECORDS = {
         "sources": ["paper_2608_02947_amd/csrc/prefill.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "7d436e2d349ffe18f8e0b91d0c355918cc227226503961269aeb7ca9bc43c49d",
-        "fetch_kib": 92981796.48, "write_kib": 933532.5,
+        "sha256": "d9c9dcc43bb67ee7c2dd97170a5956149d9e7ae00eb24c84b92ab89fad06588d",
+        "fetch_kib": 80922943.38, "write_kib": 933525.17,
     },
     "decode_split_kernel<128, false>": {
         "sources": ["paper_2608_02947_amd/csrc/decode.hip",
                     "paper_2608_02947_amd/csrc/atf_internal.hpp",
                     "paper_2608_02947_amd/csrc/rope.hpp"],
-        "sha256": "0cca9ac8645a5f8b770738b34fa5c41ee5088dfb0984a61d9045489ec4826afe",
-        "fetch_kib": 737788.79, "write_kib": 4071.25,
+        "sha256": "a45523c72cc5dbb7bffda3e4d025f689c4ccb579daa1f199c7bde058204a3889",
+        "fetch_kib": 737788.15, "write_kib": 4071.24,
     },
 }
 COPY_CALIBRATION_KIB = {"fetch": 524302.02, "write": 1048576.0}  # counters for a 1 GiB copy
